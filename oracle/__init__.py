@@ -1,0 +1,263 @@
+"""QuaRTZ CPU oracle: test infrastructure only.
+
+A ctypes wrapper over ``quartz_oracle.c`` (plain C, no code shared with the HIP
+library).  Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg
+of ``bench.py`` may import this package; the product path never does.
+
+All arrays are numpy arrays.  bf16 and fp16 data travel as ``uint16`` bit
+patterns.  See ``quartz_oracle.c`` for the readings of the paper each function
+follows (Eq. 1, Eq. 2, Section 3, Section 4.4, Appendices A and C).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "quartz_oracle.c")
+_LIB = os.path.join(_HERE, "libquartz_oracle.so")
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle with gcc (IEEE float: no fast-math, no contraction)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-D_DEFAULT_SOURCE", "-ffp-contract=off",
+           "-fno-fast-math", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    I32 = ctypes.c_int
+    lib.qo_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    lib.qo_bf16_to_f32.restype = ctypes.c_float
+    lib.qo_rne.argtypes = [ctypes.c_double]
+    lib.qo_rne.restype = ctypes.c_double
+    lib.qo_f16_to_f32.argtypes = [ctypes.c_uint16]
+    lib.qo_f16_to_f32.restype = ctypes.c_float
+    lib.qo_f32_to_f16_rne_sat.argtypes = [ctypes.c_float]
+    lib.qo_f32_to_f16_rne_sat.restype = ctypes.c_uint16
+    lib.qo_f64_to_bf16_rne.argtypes = [ctypes.c_double]
+    lib.qo_f64_to_bf16_rne.restype = ctypes.c_uint16
+    lib.qo_clz32.argtypes = [ctypes.c_uint32]
+    lib.qo_clz32.restype = I32
+    lib.qo_lzs_flag.argtypes = [ctypes.c_uint32]
+    lib.qo_lzs_flag.restype = I32
+    lib.qo_gelu_tanh.argtypes = [ctypes.c_double]
+    lib.qo_gelu_tanh.restype = ctypes.c_double
+    lib.qo_lzs_subgroup.argtypes = [P, I32, P]
+    lib.qo_lzs_subgroup.restype = I32
+    lib.qo_quantize_act.argtypes = [P, I64, I64, I64, I32, I32, P, P, P, P, P]
+    lib.qo_quantize_act.restype = I32
+    lib.qo_pack_codes.argtypes = [P, I64, I64, P]
+    lib.qo_pack_codes.restype = None
+    lib.qo_unpack_codes.argtypes = [P, I64, I64, P]
+    lib.qo_unpack_codes.restype = None
+    lib.qo_quantize_weight.argtypes = [P, I64, I64, I32, P, P]
+    lib.qo_quantize_weight.restype = I32
+    lib.qo_gemm_i32.argtypes = [P, P, P, I64, I64, I64, I32, P]
+    lib.qo_gemm_i32.restype = I32
+    lib.qo_linear_f64.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P]
+    lib.qo_linear_f64.restype = I32
+    lib.qo_linear_f64_sampled.argtypes = [P, P, P, P, P, P, I64, I32, I32, I32,
+                                          P, P, I64, P, P]
+    lib.qo_linear_f64_sampled.restype = I32
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+# ------------------------------------------------------------------ scalars
+
+def bf16_to_f32(bits: int) -> float:
+    return float(_load().qo_bf16_to_f32(int(bits)))
+
+
+def rne(v: float) -> float:
+    return float(_load().qo_rne(float(v)))
+
+
+def f16_to_f32(bits: int) -> float:
+    return float(_load().qo_f16_to_f32(int(bits)))
+
+
+def f32_to_f16_rne_sat(v: float) -> int:
+    return int(_load().qo_f32_to_f16_rne_sat(float(np.float32(v))))
+
+
+def f64_to_bf16_rne(v: float) -> int:
+    return int(_load().qo_f64_to_bf16_rne(float(v)))
+
+
+def clz32(v: int) -> int:
+    return int(_load().qo_clz32(int(v) & 0xFFFFFFFF))
+
+
+def lzs_flag(m_or: int) -> int:
+    return int(_load().qo_lzs_flag(int(m_or) & 0xFFFFFFFF))
+
+
+def gelu_tanh(v: float) -> float:
+    return float(_load().qo_gelu_tanh(float(v)))
+
+
+def lzs_subgroup(q) -> tuple[int, np.ndarray]:
+    """Stage 2 of one subgroup of int8 codes: returns (FLAG, c)."""
+    q = _c(q, np.int8)
+    c = np.empty_like(q)
+    f = _load().qo_lzs_subgroup(_ptr(q), int(q.size), _ptr(c))
+    return int(f), c
+
+
+# --------------------------------------------------------------- arrays
+
+class ActQuant:
+    """Oracle outputs of the activation quantizer for x [M][K]."""
+
+    def __init__(self, q8, c, flags, scales, zeros, lzs_group):
+        self.q8 = q8          # int8 [M][K]   Stage-1 codes
+        self.c = c            # int8 [M][K]   4-bit values in [-7, 7]
+        self.flags = flags    # uint8 [M][K/lzs_group]
+        self.scales = scales  # uint16 [M][K/64] fp16 bits
+        self.zeros = zeros    # int8 [M][K/64]
+        self.lzs_group = lzs_group
+
+    @property
+    def codes(self) -> np.ndarray:
+        """Packed nibbles in the library's storage layout, uint8 [M][K/2]."""
+        return pack_codes(self.c)
+
+    def decoded(self) -> np.ndarray:
+        """d = c * 2^FLAG as int32 [M][K]."""
+        f = np.repeat(self.flags.astype(np.int32), self.lzs_group, axis=1)
+        return self.c.astype(np.int32) << f
+
+
+def quantize_act(x_bits: np.ndarray, lzs_group: int = 16, group: int = 64,
+                 ldx: int | None = None, K: int | None = None) -> ActQuant:
+    """x_bits: uint16 bf16 bit patterns [M][ldx] (row-major)."""
+    x_bits = _c(x_bits, np.uint16)
+    M = x_bits.shape[0]
+    ldx = x_bits.shape[1] if ldx is None else ldx
+    K = x_bits.shape[1] if K is None else K
+    q8 = np.empty((M, K), np.int8)
+    c = np.empty((M, K), np.int8)
+    flags = np.empty((M, K // lzs_group), np.uint8)
+    scales = np.empty((M, K // group), np.uint16)
+    zeros = np.empty((M, K // group), np.int8)
+    rc = _load().qo_quantize_act(_ptr(x_bits), M, K, ldx, group, lzs_group,
+                                 _ptr(q8), _ptr(c), _ptr(flags), _ptr(scales), _ptr(zeros))
+    if rc != 0:
+        raise ValueError("oracle quantize_act: invalid arguments")
+    return ActQuant(q8, c, flags, scales, zeros, lzs_group)
+
+
+def pack_codes(c: np.ndarray) -> np.ndarray:
+    c = _c(c, np.int8)
+    M, K = c.shape
+    out = np.empty((M, K // 2), np.uint8)
+    _load().qo_pack_codes(_ptr(c), M, K, _ptr(out))
+    return out
+
+
+def unpack_codes(codes: np.ndarray, K: int) -> np.ndarray:
+    codes = _c(codes, np.uint8)
+    M = codes.shape[0]
+    out = np.empty((M, K), np.int8)
+    _load().qo_unpack_codes(_ptr(codes), M, K, _ptr(out))
+    return out
+
+
+def quantize_weight(w_bits: np.ndarray, group: int = 64):
+    """w_bits: uint16 bf16 [N][K]; returns (wq int8 [N][K], sw uint16 [N][K/64])."""
+    w_bits = _c(w_bits, np.uint16)
+    N, K = w_bits.shape
+    wq = np.empty((N, K), np.int8)
+    sw = np.empty((N, K // group), np.uint16)
+    rc = _load().qo_quantize_weight(_ptr(w_bits), N, K, group, _ptr(wq), _ptr(sw))
+    if rc != 0:
+        raise ValueError("oracle quantize_weight: invalid arguments")
+    return wq, sw
+
+
+def gemm_i32(a: ActQuant, wq: np.ndarray) -> np.ndarray:
+    c = _c(a.c, np.int8)
+    flags = _c(a.flags, np.uint8)
+    wq = _c(wq, np.int8)
+    M, K = c.shape
+    N = wq.shape[0]
+    out = np.empty((M, N), np.int32)
+    rc = _load().qo_gemm_i32(_ptr(c), _ptr(flags), _ptr(wq), M, N, K, a.lzs_group, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle gemm_i32: invalid arguments")
+    return out
+
+
+def linear_f64(a: ActQuant, wq: np.ndarray, sw: np.ndarray, bias_bits=None,
+               epilogue: int = 0, group: int = 64):
+    """Returns (y64 float64 [M][N], S float64 [M][N])."""
+    c = _c(a.c, np.int8)
+    flags = _c(a.flags, np.uint8)
+    scales = _c(a.scales, np.uint16)
+    wq = _c(wq, np.int8)
+    sw = _c(sw, np.uint16)
+    bias = None if bias_bits is None else _c(bias_bits, np.uint16)
+    M, K = c.shape
+    N = wq.shape[0]
+    y = np.empty((M, N), np.float64)
+    s = np.empty((M, N), np.float64)
+    rc = _load().qo_linear_f64(_ptr(c), _ptr(flags), _ptr(scales), _ptr(wq), _ptr(sw),
+                               _ptr(bias), M, N, K, group, a.lzs_group, epilogue,
+                               _ptr(y), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle linear_f64: invalid arguments")
+    return y, s
+
+
+def linear_f64_sampled(a: ActQuant, wq, sw, bias_bits, rows, cols, epilogue: int = 0,
+                       group: int = 64):
+    """Outputs (rows[i], cols[i]) only: returns (y64 [count], S [count])."""
+    c = _c(a.c, np.int8)
+    flags = _c(a.flags, np.uint8)
+    scales = _c(a.scales, np.uint16)
+    wq = _c(wq, np.int8)
+    sw = _c(sw, np.uint16)
+    bias = None if bias_bits is None else _c(bias_bits, np.uint16)
+    rows = _c(rows, np.int64)
+    cols = _c(cols, np.int64)
+    K = c.shape[1]
+    y = np.empty(rows.size, np.float64)
+    s = np.empty(rows.size, np.float64)
+    rc = _load().qo_linear_f64_sampled(_ptr(c), _ptr(flags), _ptr(scales), _ptr(wq), _ptr(sw),
+                                       _ptr(bias), K, group, a.lzs_group, epilogue,
+                                       _ptr(rows), _ptr(cols), rows.size, _ptr(y), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle linear_f64_sampled: invalid arguments")
+    return y, s
+
+
+def to_bf16_bits(y64: np.ndarray) -> np.ndarray:
+    """Expected bf16 output bits (RNE) of float64 values."""
+    f = np.vectorize(lambda v: _load().qo_f64_to_bf16_rne(float(v)), otypes=[np.uint16])
+    return f(y64)

@@ -1,0 +1,197 @@
+"""Seeded synthetic workloads for the QuaRTZ W4A4 linear path.
+
+This module only draws inputs: layer shapes and activation / weight / bias
+tensors with the distributions of diffusion-model linear layers (DiT and
+UNet-conv-as-GEMM shapes at the paper's model families, Section 5.1).  It holds
+none of the method's arithmetic (no quantization, no LZS, no GEMM), so both the
+CPU oracle and the HIP path can consume its outputs.
+
+Every tensor is drawn with numpy's PCG64 in float64, cast to float32 and then to
+bf16 with round-to-nearest-even; bf16 tensors are returned as uint16 bit
+patterns.  Seeds: ``250926436 + 100*config + 10*layer + tensor`` with tensor
+0 = x, 1 = w, 2 = bias, 3 = outlier-channel choice.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+SEED_BASE = 250926436
+
+
+@dataclass(frozen=True)
+class Layer:
+    name: str
+    M: int
+    K: int
+    N: int
+    x_kind: str            # activation recipe, see make_x()
+    w_std: float
+    epilogue: int = 0      # 0 = none, 1 = GELU-tanh
+    bias: bool = True
+
+
+@dataclass(frozen=True)
+class Config:
+    index: int
+    name: str
+    layers: tuple = field(default_factory=tuple)
+
+
+CONFIGS = {
+    1: Config(1, "single_linear_m256_k1152_n1152", (
+        Layer("linear", 256, 1152, 1152, "laplace_0.05_out0.5pct_x30", 0.02),
+    )),
+    2: Config(2, "pixart_sigma_1024px_block", (
+        Layer("qkv", 4096, 1152, 3456, "laplace_0.1_out1pct_u1_50", 0.02),
+        Layer("proj", 4096, 1152, 1152, "laplace_0.1_out1pct_u1_50", 0.02),
+        Layer("fc1", 4096, 1152, 4608, "laplace_0.1_out1pct_u1_50", 0.02),
+        Layer("fc2", 4096, 4608, 1152, "post_gelu_clip_-0.17", 0.02),
+    )),
+    3: Config(3, "flux1_schnell_joint_block_m4608", (
+        Layer("qkv", 4608, 3072, 9216, "t3_0.05_out0.2pct_x100", 0.015),
+        Layer("out", 4608, 3072, 3072, "t3_0.05_out0.2pct_x100", 0.015),
+        Layer("fc1", 4608, 3072, 12288, "t3_0.05_out0.2pct_x100", 0.015),
+        Layer("fc2", 4608, 12288, 3072, "post_gelu_t3", 0.015),
+    )),
+    4: Config(4, "flux_mlp_batched_m18432", (
+        Layer("fc1", 18432, 3072, 12288, "t3_0.05_out0.2pct_x100", 0.015, epilogue=1),
+        Layer("fc2", 18432, 12288, 3072, "pipeline", 0.015),
+    )),
+    5: Config(5, "sdxl_unet_conv3x3_im2col", (
+        Layer("conv128x128x320", 16384, 2880, 320, "im2col_silu_c320_h128", 0.02),
+        Layer("conv64x64x640", 4096, 5760, 640, "im2col_silu_c640_h64", 0.02),
+        Layer("conv32x32x1280", 1024, 11520, 1280, "im2col_silu_c1280_h32", 0.02),
+    )),
+}
+
+
+def seed(config: int, layer: int, tensor: int) -> int:
+    return SEED_BASE + 100 * config + 10 * layer + tensor
+
+
+def rng(config: int, layer: int, tensor: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed(config, layer, tensor)))
+
+
+def to_bf16_bits(a) -> np.ndarray:
+    """float64/float32 array -> bf16 bit patterns (float32 first, then RNE)."""
+    f = np.ascontiguousarray(a, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    # round to nearest even on the 16 dropped bits
+    lsb = (u >> 16) & 1
+    u = (u + 0x7FFF + lsb) >> 16
+    return u.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b) -> np.ndarray:
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def _gelu_tanh_np(z):
+    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+
+
+def _outlier_cols(config: int, layer: int, K: int, frac: float,
+                  g3: np.random.Generator | None = None) -> np.ndarray:
+    n = max(1, int(round(frac * K)))
+    g3 = rng(config, layer, 3) if g3 is None else g3
+    return g3.choice(K, n, replace=False)
+
+
+def make_x(config: int, layer_index: int, rows: int | None = None) -> np.ndarray:
+    """Activation x [rows][K] as bf16 bits.  ``rows`` truncates M (same recipe,
+    same leading rows as the full tensor)."""
+    L = CONFIGS[config].layers[layer_index]
+    M = L.M if rows is None else rows
+    K = L.K
+    g = rng(config, layer_index, 0)
+    kind = L.x_kind
+    if kind == "laplace_0.05_out0.5pct_x30":
+        x = g.laplace(0.0, 0.05, size=(M, K))
+        x[:, _outlier_cols(config, layer_index, K, 0.005)] *= 30.0
+    elif kind == "laplace_0.1_out1pct_u1_50":
+        x = g.laplace(0.0, 0.1, size=(M, K))
+        g3 = rng(config, layer_index, 3)
+        cols = _outlier_cols(config, layer_index, K, 0.01, g3)
+        x[:, cols] *= g3.uniform(1.0, 50.0, size=cols.size)
+    elif kind == "post_gelu_clip_-0.17":
+        z = g.laplace(0.0, 0.1, size=(M, K))
+        g3 = rng(config, layer_index, 3)
+        cols = _outlier_cols(config, layer_index, K, 0.01, g3)
+        z[:, cols] *= g3.uniform(1.0, 50.0, size=cols.size)
+        x = np.maximum(_gelu_tanh_np(z), -0.17)
+    elif kind == "t3_0.05_out0.2pct_x100":
+        x = 0.05 * g.standard_t(3.0, size=(M, K))
+        x[:, _outlier_cols(config, layer_index, K, 0.002)] *= 100.0
+    elif kind == "post_gelu_t3":
+        z = 0.05 * g.standard_t(3.0, size=(M, K))
+        z[:, _outlier_cols(config, layer_index, K, 0.002)] *= 100.0
+        x = _gelu_tanh_np(z)
+    elif kind == "pipeline":
+        raise ValueError("the fc2 input of the batched MLP is fc1's output")
+    elif kind.startswith("im2col_silu_"):
+        x = _im2col_silu(config, layer_index, M, K, kind)
+    else:
+        raise ValueError(kind)
+    return to_bf16_bits(x)
+
+
+def _im2col_silu(config, layer_index, M, K, kind):
+    """3x3 conv (padding 1) as GEMM: rows are output pixels, K = 9*C ordered
+    (kh, kw, c) with c fastest; the feature map is SiLU(Laplace(0, 1)) with
+    0.5% of the C input channels x30; border taps read zero padding."""
+    parts = kind.split("_")
+    C = int(parts[2][1:])
+    H = int(parts[3][1:])
+    assert K == 9 * C
+    g = rng(config, layer_index, 0)
+    rows_needed = M
+    n_img_rows = min(H, (rows_needed + H - 1) // H + 1)
+    z = g.laplace(0.0, 1.0, size=(n_img_rows, H, C))
+    fmap = z / (1.0 + np.exp(-z))
+    fmap[:, :, _outlier_cols(config, layer_index, C, 0.005)] *= 30.0
+    out = np.zeros((M, K))
+    for r in range(M):
+        oy, ox = divmod(r, H)
+        for kh in range(3):
+            iy = oy + kh - 1
+            if iy < 0 or iy >= n_img_rows or iy >= H:
+                continue
+            for kw in range(3):
+                ix = ox + kw - 1
+                if ix < 0 or ix >= H:
+                    continue
+                t = kh * 3 + kw
+                out[r, t * C:(t + 1) * C] = fmap[iy, ix]
+    return out
+
+
+def make_w(config: int, layer_index: int, rows: int | None = None) -> np.ndarray:
+    """Weight w [N][K] (nn.Linear layout) as bf16 bits."""
+    L = CONFIGS[config].layers[layer_index]
+    N = L.N if rows is None else rows
+    x = rng(config, layer_index, 1).normal(0.0, L.w_std, size=(N, L.K))
+    return to_bf16_bits(x)
+
+
+def make_bias(config: int, layer_index: int, cols: int | None = None) -> np.ndarray:
+    L = CONFIGS[config].layers[layer_index]
+    N = L.N if cols is None else cols
+    return to_bf16_bits(rng(config, layer_index, 2).normal(0.0, 0.02, size=N))
+
+
+def make_random_x(seed_value: int, M: int, K: int, kind: str = "laplace",
+                  scale: float = 0.1) -> np.ndarray:
+    """Free-form seeded activations for edge-case tests."""
+    g = np.random.Generator(np.random.PCG64(seed_value))
+    if kind == "laplace":
+        x = g.laplace(0.0, scale, size=(M, K))
+    elif kind == "normal":
+        x = g.normal(0.0, scale, size=(M, K))
+    elif kind == "t3":
+        x = scale * g.standard_t(3.0, size=(M, K))
+    else:
+        raise ValueError(kind)
+    return to_bf16_bits(x)
