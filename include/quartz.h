@@ -1,0 +1,149 @@
+/*
+ * quartz.h -- C ABI of libquartz.so, the MI355X (gfx950) W4A4 linear-layer hot
+ * path of QuaRTZ ("Post-Training Quantization via Residual Truncation and Zero
+ * Suppression for Diffusion Models", arXiv 2509.26436).
+ *
+ * The activation side follows the paper's two stages: an 8-bit min-max
+ * quantization per 64-element group (Eq. 1, symmetric reading: s = max|x|/127,
+ * zero point 0) and leading-zero suppression of each subgroup of G_s codes to
+ * 4 bits plus a shift FLAG = max(29 - clz(OR of magnitudes), 0) (Eq. 2), with
+ * the magnitudes right-shifted by FLAG, truncating toward zero (Section 3 and
+ * Appendix A).  Weights are symmetric round-to-nearest int4 per 64-element
+ * group with 16-bit scales (Appendix C; GPTQ is an offline step outside this
+ * library).  The GEMM multiplies the decoded integers d = c * 2^FLAG with the
+ * 4-bit weights exactly per 64-group, which equals the paper's integer MMA
+ * with a per-subgroup power-of-two shift (Section 4.4), then applies the two
+ * fp16 group scales, the bias and an optional GELU.
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers unless stated otherwise; the caller
+ *     allocates and owns every buffer.  The library allocates nothing and
+ *     keeps no state between calls.
+ *   - Work is enqueued asynchronously on `stream` (0 = the null stream);
+ *     outputs are valid once the stream reaches that point.
+ *   - Arguments are validated on the host before anything is launched; on an
+ *     error nothing is launched and no output is written.  A launch failure
+ *     returns QUARTZ_ERR_HIP.  Nothing aborts, throws or prints.
+ *   - Inputs must not alias outputs.  All base pointers must be 16-byte
+ *     aligned (QUARTZ_ERR_ALIGN otherwise).
+ *   - bf16 and fp16 values are passed as their 16-bit IEEE-style patterns.
+ *   - Only group_size = 64 (Appendix C) is supported; lzs_group (the LZS
+ *     subgroup size G_s of Section 3) must be 8, 16, 32 or 64.
+ *   - Input precondition: finite activations and weights; NaN / Inf give
+ *     unspecified codes.
+ */
+#ifndef QUARTZ_H
+#define QUARTZ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum quartz_status {
+    QUARTZ_OK = 0,
+    QUARTZ_ERR_NULL = 1,        /* a required pointer is NULL */
+    QUARTZ_ERR_SHAPE = 2,       /* negative size, K % 64 != 0, ld too small, too large */
+    QUARTZ_ERR_UNSUPPORTED = 3, /* group_size, lzs_group, mode or epilogue not supported */
+    QUARTZ_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+    QUARTZ_ERR_HIP = 5          /* the kernel launch failed */
+} quartz_status;
+
+enum { QUARTZ_MODE_SYMMETRIC = 0 };
+enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
+
+/*
+ * Activation quantizer: Stage 1 (Eq. 1) and Stage 2 (Eq. 2 + right shift) in
+ * one pass over x.
+ *
+ *   x_bf16  bf16 [M][ldx], row-major, ldx >= K.
+ *   M, K    rows (tokens) and reduction size; K % 64 == 0.
+ *   mode    QUARTZ_MODE_SYMMETRIC (s = max|x| / 127 per 64-group, zero point 0).
+ * Outputs (row-major, contiguous):
+ *   codes   u8  [M][K/2]  4-bit codes c in [-7, 7], sign-magnitude nibbles
+ *                         (bit 3 = sign, bits 0..2 = |c|; c = 0 is stored as 0).
+ *                         Per row, elements 8j..8j+7 form the little-endian
+ *                         32-bit word j; element 8j+i is nibble (i/2) + 4*(i%2)
+ *                         of that word (even elements in the low half-word).
+ *   flags   u8  [M][K/lzs_group]  FLAG in 0..4 of each subgroup.
+ *   scales  u16 [M][K/64]  fp16 scale s of each group: fp16(max|x| / 127),
+ *                         round-to-nearest-even, saturating at 65504.
+ *   zeros   i8  [M][K/64] or NULL; the symmetric mode writes 0.
+ * The decoded activation is x~ = s * c * 2^FLAG.
+ * M = 0 returns QUARTZ_OK without launching.
+ */
+quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int64_t ldx,
+                                  int32_t group_size, int32_t lzs_group, int32_t mode,
+                                  uint8_t* codes, uint8_t* flags, uint16_t* scales,
+                                  int8_t* zeros, hipStream_t stream);
+
+/* Size in bytes of the packed weight buffer for an N x K weight. */
+size_t quartz_packed_weight_bytes(int64_t N, int64_t K, int32_t group_size);
+
+/*
+ * Weight pre-pack (once per layer): symmetric round-to-nearest int4 per
+ * 64-group along K (Appendix C), s_w = fp16(max|w| / 7) (RNE, saturating),
+ * wq = clamp(rne(w * (1/s_w)), -7, 7).
+ *
+ *   w_bf16    bf16 [N][K], row-major (the nn.Linear weight layout).
+ *   w_packed  quartz_packed_weight_bytes(N, K, 64) bytes, opaque to callers:
+ *             panels of 64 output columns; per (panel, group) 64 x 32 bytes of
+ *             sign-magnitude nibbles in the activation-code nibble order,
+ *             followed by the 64 fp16 scales; columns past N are zero.
+ *   w_scales  u16 [N][K/64] plain copy of the fp16 scales, or NULL.
+ * N = 0 returns QUARTZ_OK without launching.
+ */
+quartz_status quartz_pack_weight(const void* w_bf16, int64_t N, int64_t K, int32_t group_size,
+                                 void* w_packed, uint16_t* w_scales, hipStream_t stream);
+
+/*
+ * W4A4 linear layer: for every output (m, n)
+ *   y[m][n] = bf16( act( sum_g s_a[m,g] * s_w[n,g] * P_g[m,n] + bias[n] ) )
+ * with P_g = sum over the 64 k of group g of (c[m,k] * 2^FLAG) * wq[n,k],
+ * computed exactly (|P_g| <= 112 * 7 * 64 < 2^24); the scales and the sum
+ * over groups are applied in fp32, act is the identity or GELU (tanh form).
+ *
+ *   codes, flags, scales, zeros   outputs of quartz_quantize_act for the same
+ *                                 M, K, lzs_group (zeros may be NULL; the
+ *                                 symmetric mode never needs it).
+ *   w_packed    output of quartz_pack_weight for N, K.
+ *   bias_bf16   bf16 [N] or NULL.
+ *   y_bf16      bf16 [M][ldy], ldy >= N.
+ *   epilogue    QUARTZ_EPI_NONE or QUARTZ_EPI_GELU_TANH.
+ * M = 0 or N = 0 returns QUARTZ_OK without launching.
+ */
+quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
+                                 const uint16_t* scales, const int8_t* zeros,
+                                 const void* w_packed, const void* bias_bf16, void* y_bf16,
+                                 int64_t M, int64_t N, int64_t K, int64_t ldy,
+                                 int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                 hipStream_t stream);
+
+/*
+ * Test / inspection helpers.
+ *
+ * quartz_unpack_weight: int8 [N][K] weight codes wq recovered from w_packed.
+ * quartz_w4a4_gemm_i32: the exact integer accumulator
+ *   acc[m][n] = sum_k (c[m,k] * 2^FLAG) * wq[n,k]   (int32 [M][N], row-major),
+ * i.e. the sum of the per-group integer MMA results before any scaling.
+ */
+quartz_status quartz_unpack_weight(const void* w_packed, int64_t N, int64_t K,
+                                   int32_t group_size, int8_t* wq_out, hipStream_t stream);
+
+quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
+                                   const void* w_packed, int32_t* acc_out, int64_t M, int64_t N,
+                                   int64_t K, int32_t group_size, int32_t lzs_group,
+                                   hipStream_t stream);
+
+/* Static, NUL-terminated description of a status code (host memory). */
+const char* quartz_status_string(quartz_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QUARTZ_H */

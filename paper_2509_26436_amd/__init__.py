@@ -1,0 +1,231 @@
+"""Python binding of libquartz.so (the QuaRTZ W4A4 linear hot path on gfx950).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch is used for device memory and the current stream.  The
+functions named like the C entry points (``quartz_quantize_act`` ...) take raw
+integers (device addresses, sizes) and return the status code; the tensor
+helpers (``quantize_act``, ``pack_weight``, ``w4a4_linear`` ...) allocate the
+outputs with ``torch.empty`` on the input's device and raise ``QuartzError`` on
+a non-OK status.  There is no fallback: if ``libquartz.so`` is missing or fails
+to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+__all__ = [
+    "QuartzError", "library_path", "load",
+    "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
+    "quartz_w4a4_linear", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
+    "quartz_status_string", "QuantizedAct", "PackedWeight",
+    "quantize_act", "pack_weight", "w4a4_linear", "unpack_weight", "w4a4_gemm_i32",
+    "EXPORTED_SYMBOLS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libquartz.so")
+
+QUARTZ_OK = 0
+MODE_SYMMETRIC = 0
+EPI_NONE = 0
+EPI_GELU_TANH = 1
+GROUP = 64
+
+EXPORTED_SYMBOLS = (
+    "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
+    "quartz_w4a4_linear", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
+    "quartz_status_string",
+)
+
+
+class QuartzError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {quartz_status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load libquartz.so (built in-tree by build.py); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"libquartz.so not found at {_LIB_PATH}; build it with "
+            "`python paper_2509_26436_amd/build.py` (no CPU fallback exists)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.quartz_quantize_act.argtypes = [P, I64, I64, I64, I32, I32, I32, P, P, P, P, P]
+    lib.quartz_quantize_act.restype = I32
+    lib.quartz_packed_weight_bytes.argtypes = [I64, I64, I32]
+    lib.quartz_packed_weight_bytes.restype = SZ
+    lib.quartz_pack_weight.argtypes = [P, I64, I64, I32, P, P, P]
+    lib.quartz_pack_weight.restype = I32
+    lib.quartz_w4a4_linear.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32, P]
+    lib.quartz_w4a4_linear.restype = I32
+    lib.quartz_unpack_weight.argtypes = [P, I64, I64, I32, P, P]
+    lib.quartz_unpack_weight.restype = I32
+    lib.quartz_w4a4_gemm_i32.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P]
+    lib.quartz_w4a4_gemm_i32.restype = I32
+    lib.quartz_status_string.argtypes = [I32]
+    lib.quartz_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+# ----------------------------------------------------------- raw C entry points
+
+def quartz_status_string(status: int) -> str:
+    return load().quartz_status_string(int(status)).decode()
+
+
+def quartz_quantize_act(x, M, K, ldx, group_size, lzs_group, mode, codes, flags, scales,
+                        zeros, stream) -> int:
+    return load().quartz_quantize_act(x, M, K, ldx, group_size, lzs_group, mode, codes, flags,
+                                      scales, zeros, stream)
+
+
+def quartz_packed_weight_bytes(N, K, group_size=GROUP) -> int:
+    return int(load().quartz_packed_weight_bytes(N, K, group_size))
+
+
+def quartz_pack_weight(w, N, K, group_size, w_packed, w_scales, stream) -> int:
+    return load().quartz_pack_weight(w, N, K, group_size, w_packed, w_scales, stream)
+
+
+def quartz_w4a4_linear(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, ldy,
+                       group_size, lzs_group, epilogue, stream) -> int:
+    return load().quartz_w4a4_linear(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, ldy,
+                                     group_size, lzs_group, epilogue, stream)
+
+
+def quartz_unpack_weight(w_packed, N, K, group_size, wq, stream) -> int:
+    return load().quartz_unpack_weight(w_packed, N, K, group_size, wq, stream)
+
+
+def quartz_w4a4_gemm_i32(codes, flags, w_packed, acc, M, N, K, group_size, lzs_group,
+                         stream) -> int:
+    return load().quartz_w4a4_gemm_i32(codes, flags, w_packed, acc, M, N, K, group_size,
+                                       lzs_group, stream)
+
+
+# ------------------------------------------------------------- tensor helpers
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(status: int, what: str):
+    if status != QUARTZ_OK:
+        raise QuartzError(status, what)
+
+
+@dataclass
+class QuantizedAct:
+    codes: "object"     # uint8 [M, K/2]
+    flags: "object"     # uint8 [M, K/lzs_group]
+    scales: "object"    # int16 [M, K/64] (fp16 bit patterns)
+    zeros: "object"     # int8 [M, K/64] or None
+    M: int
+    K: int
+    lzs_group: int
+
+
+@dataclass
+class PackedWeight:
+    data: "object"      # uint8 [quartz_packed_weight_bytes]
+    scales: "object"    # int16 [N, K/64] (fp16 bit patterns) or None
+    N: int
+    K: int
+
+
+def quantize_act(x, lzs_group: int = 16, with_zeros: bool = False, stream=None,
+                 out: QuantizedAct | None = None) -> QuantizedAct:
+    """x: bf16 [M, K] CUDA tensor whose rows are 16-byte aligned (stride(1) == 1)."""
+    torch = _torch()
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+    M, K = x.shape
+    ldx = x.stride(0)
+    if out is None:
+        dev = x.device
+        out = QuantizedAct(
+            codes=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+            flags=torch.empty((M, K // lzs_group), dtype=torch.uint8, device=dev),
+            scales=torch.empty((M, K // GROUP), dtype=torch.int16, device=dev),
+            zeros=torch.empty((M, K // GROUP), dtype=torch.int8, device=dev) if with_zeros else None,
+            M=M, K=K, lzs_group=lzs_group)
+    st = quartz_quantize_act(_ptr(x), M, K, ldx, GROUP, lzs_group, MODE_SYMMETRIC,
+                             _ptr(out.codes), _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),
+                             _stream_handle(stream))
+    _check(st, "quartz_quantize_act")
+    return out
+
+
+def pack_weight(w, with_scales: bool = True, stream=None) -> PackedWeight:
+    """w: bf16 [N, K] contiguous CUDA tensor (nn.Linear weight layout)."""
+    torch = _torch()
+    if w.dtype != torch.bfloat16 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous 2-D bf16 tensor")
+    N, K = w.shape
+    nbytes = quartz_packed_weight_bytes(N, K, GROUP)
+    data = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=w.device)
+    scales = torch.empty((N, K // GROUP), dtype=torch.int16, device=w.device) if with_scales else None
+    st = quartz_pack_weight(_ptr(w), N, K, GROUP, _ptr(data), _ptr(scales), _stream_handle(stream))
+    _check(st, "quartz_pack_weight")
+    return PackedWeight(data=data, scales=scales, N=N, K=K)
+
+
+def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI_NONE,
+                out=None, stream=None):
+    """Returns y bf16 [M, N] (or writes ``out``, a bf16 [M, >=N] view with unit column stride)."""
+    torch = _torch()
+    if a.K != w.K:
+        raise ValueError("K mismatch between activations and weights")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out is None:
+        out = torch.empty((a.M, w.N), dtype=torch.bfloat16, device=a.codes.device)
+    ldy = out.stride(0)
+    st = quartz_w4a4_linear(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                            _ptr(w.data), _ptr(bias), _ptr(out), a.M, w.N, a.K, ldy, GROUP,
+                            a.lzs_group, epilogue, _stream_handle(stream))
+    _check(st, "quartz_w4a4_linear")
+    return out
+
+
+def unpack_weight(w: PackedWeight, stream=None):
+    torch = _torch()
+    out = torch.empty((w.N, w.K), dtype=torch.int8, device=w.data.device)
+    st = quartz_unpack_weight(_ptr(w.data), w.N, w.K, GROUP, _ptr(out), _stream_handle(stream))
+    _check(st, "quartz_unpack_weight")
+    return out
+
+
+def w4a4_gemm_i32(a: QuantizedAct, w: PackedWeight, stream=None):
+    torch = _torch()
+    out = torch.empty((a.M, w.N), dtype=torch.int32, device=a.codes.device)
+    st = quartz_w4a4_gemm_i32(_ptr(a.codes), _ptr(a.flags), _ptr(w.data), _ptr(out), a.M, w.N,
+                              a.K, GROUP, a.lzs_group, _stream_handle(stream))
+    _check(st, "quartz_w4a4_gemm_i32")
+    return out

@@ -1,0 +1,70 @@
+// Internal declarations shared by the HIP sources of libquartz.so (not part of
+// the public ABI; see include/quartz.h for that).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace quartz {
+
+// Packed weight layout: panels of kPanel output columns.  For each (panel p,
+// group g), in [panel][group] order, one chunk of kPanel * 32 bytes of nibbles
+// (column-major within the panel: column c's 64 codes at c * 32) followed by
+// kPanel fp16 scales.
+constexpr int kGroup = 64;
+constexpr int kPanel = 64;
+constexpr int kChunkCodeBytes = kPanel * kGroup / 2;          // 2048
+constexpr int kChunkBytes = kChunkCodeBytes + kPanel * 2;     // 2176
+
+inline int64_t packed_weight_bytes(int64_t N, int64_t K)
+{
+    const int64_t panels = (N + kPanel - 1) / kPanel;
+    return panels * (K / kGroup) * kChunkBytes;
+}
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.  Arguments are validated by the
+// C-ABI layer before these are called.
+hipError_t launch_quantize_act(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
+                               int lzs_group, uint8_t* codes, uint8_t* flags,
+                               uint16_t* scales, int8_t* zeros, hipStream_t stream);
+
+hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
+                              uint16_t* w_scales, hipStream_t stream);
+
+hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, int8_t* wq,
+                                hipStream_t stream);
+
+hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
+                              const uint16_t* scales, const uint8_t* w_packed,
+                              const uint16_t* bias, uint16_t* y, int64_t M, int64_t N, int64_t K,
+                              int64_t ldy, int lzs_group, int epilogue, hipStream_t stream);
+
+hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
+                                const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
+                                int64_t K, int lzs_group, hipStream_t stream);
+
+// ------------------------------------------------------------ device helpers
+
+// Nibble word -> 8 OCP fp8 e4m3 bytes of (+-|c|) * 2^flag.
+// A word holds 8 sign-magnitude nibbles.  The result's low dword carries the
+// values of nibbles 0, 2, 4, 6 (bytes 0..3) and its high dword those of
+// nibbles 1, 3, 5, 7; weights and activations are decoded by this same
+// routine, so the permutation of k it introduces is the same on both MFMA
+// operands and leaves the dot product unchanged.
+// |c| * 2^flag for |c| in 1..7 is exact in e4m3 (at most 3 significant bits,
+// at most 112); flag adds to the exponent field, zero stays zero.
+__device__ __forceinline__ uint2 decode_nibbles_fp8(uint32_t w, uint32_t flag)
+{
+    // e4m3 (bias 7) of 0, 1, 2, 3 and of 4, 5, 6, 7
+    const uint32_t lo_tab = 0x44403800u + flag * 0x08080800u;
+    const uint32_t hi_tab = 0x4E4C4A48u + flag * 0x08080808u;
+    const uint32_t mag_even = w & 0x07070707u;
+    const uint32_t mag_odd = (w >> 4) & 0x07070707u;
+    uint2 r;
+    r.x = __builtin_amdgcn_perm(hi_tab, lo_tab, mag_even) | ((w << 4) & 0x80808080u);
+    r.y = __builtin_amdgcn_perm(hi_tab, lo_tab, mag_odd) | (w & 0x80808080u);
+    return r;
+}
+
+}  // namespace quartz

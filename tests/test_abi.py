@@ -1,0 +1,125 @@
+"""The C-ABI library loads, exports every symbol include/quartz.h declares,
+and rejects invalid arguments on the host before launching anything (these
+calls never reach the GPU, so they run without one)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2509_26436_amd as q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "quartz.h")
+
+OK, ENULL, ESHAPE, EUNSUP, EALIGN = 0, 1, 2, 3, 4
+A = 4096      # a fake, 16-byte aligned address: never dereferenced on these paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(quartz_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(q.library_path()):
+        pytest.skip("libquartz.so not built")
+    return q.load()
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("quartz_quantize_act", "quartz_pack_weight", "quartz_w4a4_linear"):
+        assert n in names
+    assert set(names) == set(q.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", q.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert len(q.quartz_status_string(s)) > 0
+    assert q.quartz_status_string(99) == "unknown status"
+
+
+def test_packed_weight_bytes(lib):
+    # panels of 64 columns, per (panel, group) 64 * 32 code bytes + 64 fp16 scales
+    assert q.quartz_packed_weight_bytes(320, 2880, 64) == 5 * 45 * 2176
+    assert q.quartz_packed_weight_bytes(1, 64, 64) == 2176
+    assert q.quartz_packed_weight_bytes(64, 100, 64) == 0
+    assert q.quartz_packed_weight_bytes(64, 64, 32) == 0
+
+
+def test_quantize_validation(lib):
+    f = q.quartz_quantize_act
+    assert f(A, 4, 128, 128, 32, 16, 0, A, A, A, None, None) == EUNSUP
+    assert f(A, 4, 128, 128, 64, 12, 0, A, A, A, None, None) == EUNSUP
+    assert f(A, 4, 128, 128, 64, 16, 1, A, A, A, None, None) == EUNSUP
+    assert f(A, 4, 100, 100, 64, 16, 0, A, A, A, None, None) == ESHAPE
+    assert f(A, -1, 128, 128, 64, 16, 0, A, A, A, None, None) == ESHAPE
+    assert f(A, 4, 128, 64, 64, 16, 0, A, A, A, None, None) == ESHAPE
+    assert f(None, 4, 128, 128, 64, 16, 0, A, A, A, None, None) == ENULL
+    assert f(A, 4, 128, 128, 64, 16, 0, None, A, A, None, None) == ENULL
+    assert f(A + 2, 4, 128, 128, 64, 16, 0, A, A, A, None, None) == EALIGN
+    assert f(A, 4, 128, 132, 64, 16, 0, A, A, A, None, None) == EALIGN
+    assert f(A, 4, 128, 128, 64, 16, 0, A, A, A + 8, None, None) == EALIGN
+    # nothing to do: OK without a launch (null pointers are fine then)
+    assert f(None, 0, 128, 128, 64, 16, 0, None, None, None, None, None) == OK
+
+
+def test_pack_validation(lib):
+    f = q.quartz_pack_weight
+    assert f(A, 8, 128, 16, A, None, None) == EUNSUP
+    assert f(A, 8, 96, 64, A, None, None) == ESHAPE
+    assert f(None, 8, 128, 64, A, None, None) == ENULL
+    assert f(A, 8, 128, 64, A + 4, None, None) == EALIGN
+    assert f(None, 0, 128, 64, None, None, None) == OK
+
+
+def test_linear_validation(lib):
+    f = q.quartz_w4a4_linear
+    args = dict(codes=A, flags=A, scales=A, zeros=None, w=A, bias=None, y=A)
+
+    def call(M=8, N=8, K=128, ldy=8, gs=64, lzs=16, epi=0, **over):
+        a = dict(args, **over)
+        return f(a["codes"], a["flags"], a["scales"], a["zeros"], a["w"], a["bias"], a["y"],
+                 M, N, K, ldy, gs, lzs, epi, None)
+    assert call(gs=128) == EUNSUP
+    assert call(lzs=4) == EUNSUP
+    assert call(epi=7) == EUNSUP
+    assert call(K=96) == ESHAPE
+    assert call(K=0) == ESHAPE
+    assert call(ldy=4) == ESHAPE
+    assert call(M=-3) == ESHAPE
+    assert call(codes=None) == ENULL
+    assert call(y=None) == ENULL
+    assert call(w=A + 1) == EALIGN
+    assert call(bias=A + 2) == EALIGN
+    assert call(M=0) == OK
+    assert call(N=0) == OK
+
+
+def test_debug_entry_validation(lib):
+    assert q.quartz_unpack_weight(A, 8, 100, 64, A, None) == ESHAPE
+    assert q.quartz_unpack_weight(None, 8, 128, 64, A, None) == ENULL
+    assert q.quartz_w4a4_gemm_i32(A, A, A, None, 8, 8, 128, 64, 16, None) == ENULL
+    assert q.quartz_w4a4_gemm_i32(A, A, A, A, 8, 8, 128, 64, 5, None) == EUNSUP
+    assert q.quartz_w4a4_gemm_i32(A, A, A, A, 0, 8, 128, 64, 16, None) == OK
+
+
+def test_product_path_does_not_touch_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2509_26436_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in text.lower(), fn
