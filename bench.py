@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Throughput of the QuaRTZ W4A4 linear hot path on one MI355X.
+
+Workload (default): the four linear layers of a FLUX.1-schnell-like joint
+transformer block at 4096 image + 512 text tokens (M = 4608): QKV 3072->9216,
+out 3072->3072, MLP fc1 3072->12288 and fc2 12288->3072, seeded synthetic
+bf16 activations / weights / bias (workloads.py), LZS subgroup G_s = 16.
+
+One step = one pass of the whole hot path over the block: for every layer,
+the weight pre-pack (RTN int4 + fp16 group scales), the activation quantizer
+(Stage 1 + LZS) and the W4A4 GEMM (fp8 MFMA, per-group dequant, bias).  All
+inputs are resident in HBM before the timed region.
+
+Prints ONE JSON line (stdout).  value = GEMM tera-ops (2 M N K summed over the
+layers) per second of whole steps.  roofline = the GEMM kernel (the dominant
+one): algorithmic ops / its average launch duration, from HIP events recorded
+on the launch stream inside the timed steps, against the fp8 dense MFMA peak.
+cpu_baseline = the CPU oracle on a bounded sample of the same workload (all
+weights, the first --cpu-rows rows of every layer), on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
+PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload config index (workloads.py)")
+    ap.add_argument("--lzs-group", type=int, default=16)
+    ap.add_argument("--cpu-rows", type=int, default=768,
+                    help="rows per layer in the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def layer_bytes(L, gs):
+    quant = L.M * L.K * (2 + 0.5 + 1.0 / gs + 2.0 / 64)
+    pack = L.N * L.K * (2 + 0.5 + 2.0 / 64 + 2.0 / 64)
+    gemm = (L.M * L.K * (0.5 + 1.0 / gs + 2.0 / 64) + L.N * L.K * (0.5 + 2.0 / 64)
+            + 2 * L.N + 2 * L.M * L.N)
+    return quant, pack, gemm
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the per-GPU share would be benchmarked as its own shape); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2509_26436_amd as q
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    cfg = W.CONFIGS[args.config]
+    gs = args.lzs_group
+    layers = list(cfg.layers)
+    if any(L.x_kind == "pipeline" for L in layers):
+        log("config with a pipelined input is not a bench workload")
+        sys.exit(2)
+
+    # ---------------- inputs, resident in HBM
+    t0 = time.time()
+    host = []
+    dev_in = []
+    for li, L in enumerate(layers):
+        xb = W.make_x(cfg.index, li)
+        wb = W.make_w(cfg.index, li)
+        bb = W.make_bias(cfg.index, li)
+        host.append((xb, wb, bb))
+        to = lambda a: torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        dev_in.append((to(xb), to(wb), to(bb)))
+        log(f"layer {L.name}: M={L.M} K={L.K} N={L.N} generated")
+    log(f"inputs ready in {time.time() - t0:.1f}s")
+
+    # outputs preallocated once (the step allocates nothing new)
+    outs = []
+    for (x, w, b), L in zip(dev_in, layers):
+        qa = q.quantize_act(x, lzs_group=gs)
+        pw = q.pack_weight(w)
+        y = torch.empty((L.M, L.N), dtype=torch.bfloat16, device=dev)
+        outs.append((qa, pw, y))
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        for li, ((x, w, b), (qa, pw, y), L) in enumerate(zip(dev_in, outs, layers)):
+            ev = events[li] if events is not None else None
+            if ev: ev[0].record(stream)
+            q.quartz_pack_weight(q._ptr(w), L.N, L.K, 64, q._ptr(pw.data), q._ptr(pw.scales),
+                                 q._stream_handle())
+            if ev: ev[1].record(stream)
+            q.quantize_act(x, lzs_group=gs, out=qa)
+            if ev: ev[2].record(stream)
+            q.w4a4_linear(qa, pw, b, L.epilogue, out=y)
+            if ev: ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev_all = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+              for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for s in range(args.steps):
+        step(ev_all[s])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+
+    # per-kernel durations from the events of the timed steps
+    t_pack = np.zeros(len(layers))
+    t_quant = np.zeros(len(layers))
+    t_gemm = np.zeros(len(layers))
+    for s in range(args.steps):
+        for li in range(len(layers)):
+            e = ev_all[s][li]
+            t_pack[li] += e[0].elapsed_time(e[1])
+            t_quant[li] += e[1].elapsed_time(e[2])
+            t_gemm[li] += e[2].elapsed_time(e[3])
+    t_pack /= args.steps
+    t_quant /= args.steps
+    t_gemm /= args.steps
+
+    ops = np.array([2.0 * L.M * L.N * L.K for L in layers])
+    qbytes = np.array([layer_bytes(L, gs)[0] for L in layers])
+    pbytes = np.array([layer_bytes(L, gs)[1] for L in layers])
+    gbytes = np.array([layer_bytes(L, gs)[2] for L in layers])
+    value = ops.sum() / (ms_per_step * 1e-3) / 1e12
+    gemm_tflops = ops.sum() / (t_gemm.sum() * 1e-3) / 1e12
+    quant_gbps = qbytes.sum() / (t_quant.sum() * 1e-3) / 1e9
+    pack_gbps = pbytes.sum() / (t_pack.sum() * 1e-3) / 1e9
+
+    per_layer = []
+    for li, L in enumerate(layers):
+        per_layer.append({
+            "layer": L.name, "M": L.M, "K": L.K, "N": L.N,
+            "gemm_us": round(t_gemm[li] * 1e3, 2),
+            "gemm_tflops": round(ops[li] / (t_gemm[li] * 1e-3) / 1e12, 1),
+            "quantize_us": round(t_quant[li] * 1e3, 2),
+            "quantize_gbps": round(qbytes[li] / (t_quant[li] * 1e-3) / 1e9, 1),
+            "pack_us": round(t_pack[li] * 1e3, 2),
+            "pack_gbps": round(pbytes[li] / (t_pack[li] * 1e-3) / 1e9, 1),
+        })
+
+    # ---------------- CPU oracle on a bounded sample (rank 0, N = 1 only)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = args.cpu_rows
+        t_c = time.perf_counter()
+        sample_ops = 0.0
+        for li, L in enumerate(layers):
+            xb, wb, bb = host[li]
+            wq, sw = oracle.quantize_weight(wb)
+            a = oracle.quantize_act(xb[:rows], lzs_group=gs)
+            oracle.linear_f64(a, wq, sw, bb, epilogue=L.epilogue)
+            sample_ops += 2.0 * rows * L.N * L.K
+        t_c = time.perf_counter() - t_c
+        cpu = {"value": round(sample_ops / t_c / 1e12, 6), "unit": "TOPS",
+               "cores": oracle.num_threads(), "kind": "oracle",
+               "sample": (f"weight pack of all {len(layers)} layers + quantize and linear of the "
+                          f"first {rows} of {layers[0].M} rows of every layer; "
+                          f"{t_c:.1f}s of CPU time")}
+        log(f"cpu oracle sample: {t_c:.1f}s")
+
+    result = {
+        "metric": "W4A4 linear TOPS + quantize GB/s at FLUX-shaped layers (fraction of roofline)",
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8_e4m3",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "layers": [f"{L.name} M={L.M} K={L.K} N={L.N}" for L in layers],
+            "group_size": 64, "lzs_group": gs,
+            "step": "pack_weight + quantize_act + w4a4_linear per layer",
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_FP8_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4), "traffic": None,
+        },
+        "quantize_roofline": {
+            "bound": "hbm", "achieved": round(quant_gbps, 1), "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s", "frac": round(quant_gbps / PEAK_HBM_GBPS, 4),
+        },
+        "pack_gbps": round(pack_gbps, 1),
+        "per_layer": per_layer,
+        "wall_s_timed": round(wall, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -76,6 +76,8 @@ def _load():
     lib.qo_linear_f64_sampled.argtypes = [P, P, P, P, P, P, I64, I32, I32, I32,
                                           P, P, I64, P, P]
     lib.qo_linear_f64_sampled.restype = I32
+    lib.qo_num_threads.argtypes = []
+    lib.qo_num_threads.restype = I32
     _lib = lib
     return lib
 
@@ -89,6 +91,11 @@ def _c(a, dtype):
 
 
 # ------------------------------------------------------------------ scalars
+
+def num_threads() -> int:
+    """Threads the oracle's parallel loops use (OpenMP)."""
+    return int(_load().qo_num_threads())
+
 
 def bf16_to_f32(bits: int) -> float:
     return float(_load().qo_bf16_to_f32(int(bits)))

@@ -446,3 +446,16 @@ int qo_linear_f64_sampled(const int8_t* c, const uint8_t* flags, const uint16_t*
                           rows[i], cols[i], absum ? &absum[i] : NULL);
     return QO_OK;
 }
+
+/* Number of threads the OpenMP loops above use. */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int qo_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -77,12 +77,13 @@ def rng(config: int, layer: int, tensor: int) -> np.random.Generator:
 
 def to_bf16_bits(a) -> np.ndarray:
     """float64/float32 array -> bf16 bit patterns (float32 first, then RNE)."""
-    f = np.ascontiguousarray(a, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    # round to nearest even on the 16 dropped bits
-    lsb = (u >> 16) & 1
-    u = (u + 0x7FFF + lsb) >> 16
-    return u.astype(np.uint16)
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    # round to nearest even on the 16 dropped bits (no overflow for finite values)
+    r = (u >> 16) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b) -> np.ndarray:
@@ -90,7 +91,17 @@ def bf16_bits_to_f32(b) -> np.ndarray:
 
 
 def _gelu_tanh_np(z):
-    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+    """0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))), evaluated in place."""
+    t = z * z
+    t *= z
+    t *= 0.044715
+    t += z
+    t *= np.sqrt(2.0 / np.pi)
+    np.tanh(t, out=t)
+    t += 1.0
+    t *= z
+    t *= 0.5
+    return t
 
 
 def _outlier_cols(config: int, layer: int, K: int, frac: float,
@@ -121,12 +132,15 @@ def make_x(config: int, layer_index: int, rows: int | None = None) -> np.ndarray
         g3 = rng(config, layer_index, 3)
         cols = _outlier_cols(config, layer_index, K, 0.01, g3)
         z[:, cols] *= g3.uniform(1.0, 50.0, size=cols.size)
-        x = np.maximum(_gelu_tanh_np(z), -0.17)
+        x = _gelu_tanh_np(z)
+        np.maximum(x, -0.17, out=x)
     elif kind == "t3_0.05_out0.2pct_x100":
-        x = 0.05 * g.standard_t(3.0, size=(M, K))
+        x = g.standard_t(3.0, size=(M, K))
+        x *= 0.05
         x[:, _outlier_cols(config, layer_index, K, 0.002)] *= 100.0
     elif kind == "post_gelu_t3":
-        z = 0.05 * g.standard_t(3.0, size=(M, K))
+        z = g.standard_t(3.0, size=(M, K))
+        z *= 0.05
         z[:, _outlier_cols(config, layer_index, K, 0.002)] *= 100.0
         x = _gelu_tanh_np(z)
     elif kind == "pipeline":
