@@ -63,16 +63,19 @@ enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
  *   x_bf16  bf16 [M][ldx], row-major, ldx >= K.
  *   M, K    rows (tokens) and reduction size; K % 64 == 0.
  *   mode    QUARTZ_MODE_SYMMETRIC (s = max|x| / 127 per 64-group, zero point 0).
- * Outputs (row-major, contiguous):
- *   codes   u8  [M][K/2]  4-bit codes c in [-7, 7], sign-magnitude nibbles
- *                         (bit 3 = sign, bits 0..2 = |c|; c = 0 is stored as 0).
- *                         Per row, elements 8j..8j+7 form the little-endian
- *                         32-bit word j; element 8j+i is nibble (i/2) + 4*(i%2)
- *                         of that word (even elements in the low half-word).
- *   flags   u8  [M][K/lzs_group]  FLAG in 0..4 of each subgroup.
- *   scales  u16 [M][K/64]  fp16 scale s of each group: fp16(max|x| / 127),
+ * Outputs, K-group-major (all rows of 64-group 0, then all rows of group 1, ...),
+ * so that one group of a tile of rows is one contiguous run for the GEMM:
+ *   codes   u8  [K/64][M][32]   4-bit codes c in [-7, 7] of the 64 elements of
+ *                         (group, row), sign-magnitude nibbles (bit 3 = sign,
+ *                         bits 0..2 = |c|; c = 0 is stored as 0).  Elements
+ *                         8j..8j+7 of the group form the little-endian 32-bit
+ *                         word j of its 32 bytes; element 8j+i is nibble
+ *                         (i/2) + 4*(i%2) of that word (even elements in the
+ *                         low half-word).
+ *   flags   u8  [K/64][M][64/lzs_group]  FLAG in 0..4 of each subgroup.
+ *   scales  u16 [K/64][M]   fp16 scale s of each (group, row): fp16(max|x| / 127),
  *                         round-to-nearest-even, saturating at 65504.
- *   zeros   i8  [M][K/64] or NULL; the symmetric mode writes 0.
+ *   zeros   i8  [K/64][M] or NULL; the symmetric mode writes 0.
  * The decoded activation is x~ = s * c * 2^FLAG.
  * M = 0 returns QUARTZ_OK without launching.
  */

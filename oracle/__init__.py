@@ -152,8 +152,24 @@ class ActQuant:
 
     @property
     def codes(self) -> np.ndarray:
-        """Packed nibbles in the library's storage layout, uint8 [M][K/2]."""
+        """Packed nibbles in the library's storage layout, uint8 [K/64][M][32]."""
         return pack_codes(self.c)
+
+    @property
+    def abi_flags(self) -> np.ndarray:
+        """Flags in the library's K-group-major layout, uint8 [K/64][M][64/lzs_group]."""
+        M, S = self.flags.shape
+        per = 64 // self.lzs_group
+        return np.ascontiguousarray(self.flags.reshape(M, S // per, per).transpose(1, 0, 2))
+
+    @property
+    def abi_scales(self) -> np.ndarray:
+        """Scales in the library's K-group-major layout, uint16 [K/64][M]."""
+        return np.ascontiguousarray(self.scales.T)
+
+    @property
+    def abi_zeros(self) -> np.ndarray:
+        return np.ascontiguousarray(self.zeros.T)
 
     def decoded(self) -> np.ndarray:
         """d = c * 2^FLAG as int32 [M][K]."""
@@ -181,16 +197,17 @@ def quantize_act(x_bits: np.ndarray, lzs_group: int = 16, group: int = 64,
 
 
 def pack_codes(c: np.ndarray) -> np.ndarray:
+    """int8 values [M][K] -> packed nibbles uint8 [K/64][M][32]."""
     c = _c(c, np.int8)
     M, K = c.shape
-    out = np.empty((M, K // 2), np.uint8)
+    out = np.empty((K // 64, M, 32), np.uint8)
     _load().qo_pack_codes(_ptr(c), M, K, _ptr(out))
     return out
 
 
-def unpack_codes(codes: np.ndarray, K: int) -> np.ndarray:
+def unpack_codes(codes: np.ndarray, M: int, K: int) -> np.ndarray:
+    """packed nibbles uint8 [K/64][M][32] -> int8 values [M][K]."""
     codes = _c(codes, np.uint8)
-    M = codes.shape[0]
     out = np.empty((M, K), np.int8)
     _load().qo_unpack_codes(_ptr(codes), M, K, _ptr(out))
     return out

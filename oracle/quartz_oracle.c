@@ -272,26 +272,31 @@ int qo_quantize_act(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
 /*
  * Storage layout of the 4-bit codes (the library's documented format):
  * each code is a sign-magnitude nibble, bit 3 = sign, bits 0..2 = |c|, and
- * c = 0 is always stored as 0.  Per row, elements 8j..8j+7 form the
- * little-endian 32-bit word j; element 8j+i sits in nibble (i/2) + 4*(i%2),
- * i.e. even elements fill the low half-word and odd elements the high one.
+ * c = 0 is always stored as 0.  The 32 bytes of (64-group g, row m) sit at
+ * byte (g * M + m) * 32 (K-group-major).  Within them, elements 8j..8j+7 of
+ * the group form the little-endian 32-bit word j; element 8j+i sits in nibble
+ * (i/2) + 4*(i%2), i.e. even elements fill the low half-word and odd elements
+ * the high one.
  */
 void qo_pack_codes(const int8_t* c, int64_t M, int64_t K, uint8_t* codes)
 {
+    const int64_t G = K / 64;
     for (int64_t m = 0; m < M; ++m) {
-        for (int64_t j = 0; j < K / 8; ++j) {
-            uint32_t word = 0;
-            for (int i = 0; i < 8; ++i) {
-                int v = c[m * K + 8 * j + i];
-                uint32_t nib = (uint32_t)(v < 0 ? 8 + (-v) : v);
-                int pos = (i / 2) + 4 * (i % 2);
-                word |= nib << (4 * pos);
+        for (int64_t g = 0; g < G; ++g) {
+            uint8_t* out = codes + (g * M + m) * 32;
+            for (int j = 0; j < 8; ++j) {
+                uint32_t word = 0;
+                for (int i = 0; i < 8; ++i) {
+                    int v = c[m * K + g * 64 + 8 * j + i];
+                    uint32_t nib = (uint32_t)(v < 0 ? 8 + (-v) : v);
+                    int pos = (i / 2) + 4 * (i % 2);
+                    word |= nib << (4 * pos);
+                }
+                out[4 * j + 0] = (uint8_t)(word & 0xff);
+                out[4 * j + 1] = (uint8_t)((word >> 8) & 0xff);
+                out[4 * j + 2] = (uint8_t)((word >> 16) & 0xff);
+                out[4 * j + 3] = (uint8_t)((word >> 24) & 0xff);
             }
-            uint8_t* out = codes + m * (K / 2) + 4 * j;
-            out[0] = (uint8_t)(word & 0xff);
-            out[1] = (uint8_t)((word >> 8) & 0xff);
-            out[2] = (uint8_t)((word >> 16) & 0xff);
-            out[3] = (uint8_t)((word >> 24) & 0xff);
         }
     }
 }
@@ -299,16 +304,19 @@ void qo_pack_codes(const int8_t* c, int64_t M, int64_t K, uint8_t* codes)
 /* Inverse of qo_pack_codes (nibble 8 = "-0" decodes to 0). */
 void qo_unpack_codes(const uint8_t* codes, int64_t M, int64_t K, int8_t* c)
 {
+    const int64_t G = K / 64;
     for (int64_t m = 0; m < M; ++m) {
-        for (int64_t j = 0; j < K / 8; ++j) {
-            const uint8_t* in = codes + m * (K / 2) + 4 * j;
-            uint32_t word = (uint32_t)in[0] | ((uint32_t)in[1] << 8) |
-                            ((uint32_t)in[2] << 16) | ((uint32_t)in[3] << 24);
-            for (int i = 0; i < 8; ++i) {
-                int pos = (i / 2) + 4 * (i % 2);
-                uint32_t nib = (word >> (4 * pos)) & 0xf;
-                int mag = (int)(nib & 7);
-                c[m * K + 8 * j + i] = (int8_t)((nib & 8) ? -mag : mag);
+        for (int64_t g = 0; g < G; ++g) {
+            const uint8_t* in = codes + (g * M + m) * 32;
+            for (int j = 0; j < 8; ++j) {
+                uint32_t word = (uint32_t)in[4 * j] | ((uint32_t)in[4 * j + 1] << 8) |
+                                ((uint32_t)in[4 * j + 2] << 16) | ((uint32_t)in[4 * j + 3] << 24);
+                for (int i = 0; i < 8; ++i) {
+                    int pos = (i / 2) + 4 * (i % 2);
+                    uint32_t nib = (word >> (4 * pos)) & 0xf;
+                    int mag = (int)(nib & 7);
+                    c[m * K + g * 64 + 8 * j + i] = (int8_t)((nib & 8) ? -mag : mag);
+                }
             }
         }
     }

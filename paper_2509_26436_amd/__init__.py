@@ -142,10 +142,11 @@ def _check(status: int, what: str):
 
 @dataclass
 class QuantizedAct:
-    codes: "object"     # uint8 [M, K/2]
-    flags: "object"     # uint8 [M, K/lzs_group]
-    scales: "object"    # int16 [M, K/64] (fp16 bit patterns)
-    zeros: "object"     # int8 [M, K/64] or None
+    """Quantizer outputs, K-group-major (see include/quartz.h)."""
+    codes: "object"     # uint8 [K/64, M, 32]
+    flags: "object"     # uint8 [K/64, M, 64/lzs_group]
+    scales: "object"    # int16 [K/64, M] (fp16 bit patterns)
+    zeros: "object"     # int8 [K/64, M] or None
     M: int
     K: int
     lzs_group: int
@@ -169,11 +170,12 @@ def quantize_act(x, lzs_group: int = 16, with_zeros: bool = False, stream=None,
     ldx = x.stride(0)
     if out is None:
         dev = x.device
+        G = K // GROUP
         out = QuantizedAct(
-            codes=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
-            flags=torch.empty((M, K // lzs_group), dtype=torch.uint8, device=dev),
-            scales=torch.empty((M, K // GROUP), dtype=torch.int16, device=dev),
-            zeros=torch.empty((M, K // GROUP), dtype=torch.int8, device=dev) if with_zeros else None,
+            codes=torch.empty((G, M, 32), dtype=torch.uint8, device=dev),
+            flags=torch.empty((G, M, GROUP // lzs_group), dtype=torch.uint8, device=dev),
+            scales=torch.empty((G, M), dtype=torch.int16, device=dev),
+            zeros=torch.empty((G, M), dtype=torch.int8, device=dev) if with_zeros else None,
             M=M, K=K, lzs_group=lzs_group)
     st = quartz_quantize_act(_ptr(x), M, K, ldx, GROUP, lzs_group, MODE_SYMMETRIC,
                              _ptr(out.codes), _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),

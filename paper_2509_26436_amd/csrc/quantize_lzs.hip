@@ -2,9 +2,11 @@
 // (Eq. 2 leading-zero suppression + right shift, Section 3) in one pass.
 //
 // One 64-element group is handled by a team of 8 lanes, each lane owning 8
-// consecutive bf16 values (one 16-byte load).  A wave covers 32 consecutive
-// groups (4 rounds of 8 teams), so every load instruction of a wave reads
-// 1 KiB of contiguous activations when rows are contiguous (ldx == K).
+// consecutive bf16 values (one 16-byte load).  A wave covers 8 consecutive rows
+// (one per team) and 4 consecutive groups (4 rounds): every load instruction
+// reads one full 128-byte line per row, and since the outputs are stored
+// K-group-major (codes [K/64][M][32], flags [K/64][M][64/G_s], scales
+// [K/64][M]) every code store of a wave writes 256 contiguous bytes.
 //
 // Per group:  alpha = max|x| (exact, 8-lane DPP max)
 //             s = fp16_rne_sat(alpha / 127), r = 1/s (IEEE fp32 divisions)
@@ -64,40 +66,28 @@ __device__ __forceinline__ uint32_t f16_bits_rne_sat(float s)
     return b;
 }
 
-template <int GS, bool CONTIG>
+template <int GS>
 __global__ __launch_bounds__(256) void quantize_act_kernel(
-    const uint16_t* __restrict__ x, int64_t total_groups, int64_t groups_per_row, int64_t ldx,
+    const uint16_t* __restrict__ x, int64_t M, int64_t G, int64_t ldx, int64_t quads,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ flags, uint16_t* __restrict__ scales,
     int8_t* __restrict__ zeros)
 {
+    constexpr int FB = 64 / GS;     // flag bytes per (row, group)
     const int lane = threadIdx.x & 63;
     const int team = lane >> 3;
     const int u = lane & 7;
-    const int64_t wave_base = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 32;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t row = (w / quads) * 8 + team;
+    const int64_t g0 = (w % quads) * 4;
+    const bool row_ok = row < M;
+    const uint16_t* xr = x + (row_ok ? row : 0) * ldx + u * 8;
 
     uint4 v[4];
-    int64_t gid[4];
-    int64_t row = 0, col = 0;
-    if constexpr (!CONTIG) {
-        const int64_t g0 = wave_base + team;
-        row = g0 / groups_per_row;
-        col = g0 - row * groups_per_row;
-    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        gid[j] = wave_base + 8 * j + team;
-        const uint16_t* p;
-        if constexpr (CONTIG) {
-            p = x + gid[j] * 64 + u * 8;
-        } else {
-            p = x + row * ldx + col * 64 + u * 8;
-            col += 8;
-            while (col >= groups_per_row) {
-                col -= groups_per_row;
-                ++row;
-            }
-        }
-        v[j] = gid[j] < total_groups ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+        const int64_t g = g0 + j;
+        v[j] = (row_ok && g < G) ? *reinterpret_cast<const uint4*>(xr + g * 64)
+                                 : make_uint4(0, 0, 0, 0);
     }
 
 #pragma unroll
@@ -144,25 +134,26 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(
         // keep a sign only where the magnitude is non-zero: t + 7 sets bit 3 iff t >= 1
         const uint32_t word = T | (S & (T + 0x77777777u));
 
-        if (gid[j] < total_groups) {
-            const int64_t g = gid[j];
-            reinterpret_cast<uint32_t*>(codes)[g * 8 + u] = word;
+        const int64_t g = g0 + j;
+        if (row_ok && g < G) {
+            const int64_t rg = g * M + row;          // (group, row) in K-group-major order
+            reinterpret_cast<uint32_t*>(codes)[rg * 8 + u] = word;
             if constexpr (GS == 8) {
-                flags[g * 8 + u] = (uint8_t)fl;
+                flags[rg * FB + u] = (uint8_t)fl;
             } else if constexpr (GS == 16) {
                 if ((u & 1) == 0)
-                    flags[g * 4 + (u >> 1)] = (uint8_t)fl;
+                    flags[rg * FB + (u >> 1)] = (uint8_t)fl;
             } else if constexpr (GS == 32) {
                 if ((u & 3) == 0)
-                    flags[g * 2 + (u >> 2)] = (uint8_t)fl;
+                    flags[rg * FB + (u >> 2)] = (uint8_t)fl;
             } else {
                 if (u == 0)
-                    flags[g] = (uint8_t)fl;
+                    flags[rg] = (uint8_t)fl;
             }
             if (u == 0) {
-                scales[g] = (uint16_t)s16;
+                scales[rg] = (uint16_t)s16;
                 if (zeros)
-                    zeros[g] = 0;
+                    zeros[rg] = 0;
             }
         }
     }
@@ -172,15 +163,12 @@ template <int GS>
 hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
                      uint8_t* flags, uint16_t* scales, int8_t* zeros, hipStream_t stream)
 {
-    const int64_t gpr = K / 64;
-    const int64_t total = M * gpr;
-    const int64_t blocks = (total + 127) / 128;
-    if (ldx == K)
-        quantize_act_kernel<GS, true><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-            x, total, gpr, ldx, codes, flags, scales, zeros);
-    else
-        quantize_act_kernel<GS, false><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
-            x, total, gpr, ldx, codes, flags, scales, zeros);
+    const int64_t G = K / 64;
+    const int64_t quads = (G + 3) / 4;
+    const int64_t waves = (M + 7) / 8 * quads;
+    const int64_t blocks = (waves + 3) / 4;
+    quantize_act_kernel<GS><<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(
+        x, M, G, ldx, quads, codes, flags, scales, zeros);
     return hipGetLastError();
 }
 

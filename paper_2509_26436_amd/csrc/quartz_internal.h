@@ -53,17 +53,37 @@ hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
 // routine, so the permutation of k it introduces is the same on both MFMA
 // operands and leaves the dot product unchanged.
 // |c| * 2^flag for |c| in 1..7 is exact in e4m3 (at most 3 significant bits,
-// at most 112); flag adds to the exponent field, zero stays zero.
-__device__ __forceinline__ uint2 decode_nibbles_fp8(uint32_t w, uint32_t flag)
+// at most 112): the magnitudes index an 8-entry byte table (v_perm_b32)
+// whose non-zero entries carry the exponent bias plus flag.
+struct Fp8Table {
+    uint32_t lo;   // e4m3 of 0, 1, 2, 3 (times 2^flag)
+    uint32_t hi;   // e4m3 of 4, 5, 6, 7 (times 2^flag)
+};
+
+constexpr uint32_t kTabLo = 0x44403800u;
+constexpr uint32_t kTabHi = 0x4E4C4A48u;
+
+// Table for flag byte i (0..3) of `flags8`, a word whose bytes hold 8 * FLAG:
+// the byte is replicated with v_perm_b32 (selector 0x0C yields 0x00, which
+// keeps the entry of magnitude 0 at zero) and added to the exponent fields.
+template <int I>
+__device__ __forceinline__ Fp8Table fp8_table(uint32_t flags8)
 {
-    // e4m3 (bias 7) of 0, 1, 2, 3 and of 4, 5, 6, 7
-    const uint32_t lo_tab = 0x44403800u + flag * 0x08080800u;
-    const uint32_t hi_tab = 0x4E4C4A48u + flag * 0x08080808u;
+    constexpr uint32_t rep = 0x01010101u * I;
+    constexpr uint32_t rep_lo = (0x01010100u * I) | 0x0Cu;
+    Fp8Table t;
+    t.lo = kTabLo + __builtin_amdgcn_perm(0u, flags8, rep_lo);
+    t.hi = kTabHi + __builtin_amdgcn_perm(0u, flags8, rep);
+    return t;
+}
+
+__device__ __forceinline__ uint2 decode_nibbles_fp8(uint32_t w, Fp8Table t)
+{
     const uint32_t mag_even = w & 0x07070707u;
     const uint32_t mag_odd = (w >> 4) & 0x07070707u;
     uint2 r;
-    r.x = __builtin_amdgcn_perm(hi_tab, lo_tab, mag_even) | ((w << 4) & 0x80808080u);
-    r.y = __builtin_amdgcn_perm(hi_tab, lo_tab, mag_odd) | (w & 0x80808080u);
+    r.x = __builtin_amdgcn_perm(t.hi, t.lo, mag_even) | ((w << 4) & 0x80808080u);
+    r.y = __builtin_amdgcn_perm(t.hi, t.lo, mag_odd) | (w & 0x80808080u);
     return r;
 }
 

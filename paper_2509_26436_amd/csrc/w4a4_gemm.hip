@@ -4,13 +4,20 @@
 // activations (codes + per-subgroup FLAG + fp16 scale) and packed 4-bit
 // weights (codes + fp16 scale) from global memory, decodes them in registers
 // to OCP fp8 e4m3 operands -- activations as c * 2^FLAG in [-112, 112],
-// weights as wq in [-7, 7], both exact in e4m3 -- and writes them to LDS.
-// Each wave then runs v_mfma_f32_32x32x64_f8f6f4 over the whole group, which
-// yields the exact integer group product P_g (all partial sums are integers
-// below 2^24), and folds it into fp32 accumulators with the two group scales:
-//   acc += P_g * (s_a[m,g] * s_w[n,g])      (s_a * s_w is exact in fp32).
+// weights as wq in [-7, 7], both exact in e4m3 -- and writes them to LDS
+// (double-buffered: group g+1 is fetched from global memory while group g is
+// multiplied).  Each wave then runs v_mfma_f32_32x32x64_f8f6f4 over the whole
+// group, which yields the exact integer group product P_g (every partial sum
+// is an integer below 2^24), and folds it into fp32 accumulators with the two
+// group scales:
+//   acc += P_g * (s_a[m,g] * s_w[n,g]).
+// The 32 x 32 tile of scale products s_a (x) s_w is itself produced by one
+// fp16 MFMA with a single non-zero k (fp16 x fp16 is exact in fp32), so the
+// per-group dequantization costs one FMA per output element.
 // The epilogue adds the bias, applies the optional GELU (tanh form) and
 // stores bf16 (round to nearest even).
+#include <type_traits>
+
 #include "quartz_internal.h"
 
 namespace quartz {
@@ -18,16 +25,8 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-constexpr int BM = 128;
-constexpr int BN = 128;
-constexpr int kThreads = 256;
-constexpr int kRowBytes = 64;   // one decoded fp8 row of a group in LDS
-
-__device__ __forceinline__ float f16_to_f32(uint16_t h)
-{
-    return (float)__builtin_bit_cast(_Float16, h);
-}
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float v)
 {
@@ -42,41 +41,129 @@ __device__ __forceinline__ float gelu_tanh(float v)
     return 0.5f * v * (1.0f + tanhf(k * (v + 0.044715f * v * v * v)));
 }
 
-// Flags of the 32 elements [32 h, 32 h + 32) of group g of row m: the flag of
-// 8-element word i (0..3) of that half.
-template <int GS>
-__device__ __forceinline__ void load_flags(const uint8_t* __restrict__ flags, int64_t m, int64_t K,
-                                           int g, int h, uint32_t fl[4])
+// ------------------------------------------------------------------ layout
+// Block tile BM x BN = 256 x 128, 8 waves as 4 (M) x 2 (N), wave tile 64 x 64
+// = 2 x 2 MFMA tiles of 32 x 32.  Two waves share each SIMD, so one wave's
+// VALU work (decode, dequantization) overlaps the other's MFMAs.
+constexpr int BM = 256;
+constexpr int BN = 128;
+constexpr int kWaves = 8;
+constexpr int kThreadsPerBlock = 64 * kWaves;
+constexpr int WAVES_N = 2;
+constexpr int WM = 64;
+constexpr int WN = 64;
+constexpr int TM = WM / 32;
+constexpr int TN = WN / 32;
+constexpr int kDepth = 3;      // groups held in the register prefetch ring
+
+// 16-byte chunk c of decoded fp8 row r lives at chunk c ^ f(r) with
+//   f(r) = (r1 ^ r2) | (r2 ^ r3) << 1      (r_i = bit i of r).
+// Fragment reads (16 consecutive rows, one chunk) and decode writes (8 rows,
+// both halves) then touch distinct 16-byte bank groups within every 128-byte
+// and every 256-byte window, whether the LDS serves 8 or 16 lanes per cycle.
+__device__ __forceinline__ int swz(int r, int c)
 {
-    const uint8_t* row = flags + m * (K / GS);
-    if constexpr (GS == 8) {
-        const uint32_t f4 = *reinterpret_cast<const uint32_t*>(row + g * 8 + h * 4);
-        for (int i = 0; i < 4; ++i)
-            fl[i] = (f4 >> (8 * i)) & 0xFFu;
-    } else if constexpr (GS == 16) {
-        const uint32_t f2 = *reinterpret_cast<const uint16_t*>(row + g * 4 + h * 2);
-        fl[0] = fl[1] = f2 & 0xFFu;
-        fl[2] = fl[3] = f2 >> 8;
-    } else if constexpr (GS == 32) {
-        const uint32_t f1 = row[g * 2 + h];
-        fl[0] = fl[1] = fl[2] = fl[3] = f1;
-    } else {
-        const uint32_t f1 = row[g];
-        fl[0] = fl[1] = fl[2] = fl[3] = f1;
-    }
+    const int f = (((r >> 1) ^ (r >> 2)) & 1) | ((((r >> 2) ^ (r >> 3)) & 1) << 1);
+    return r * 64 + ((c ^ f) << 4);
 }
 
+__device__ __forceinline__ v8i load_frag(const uint8_t* lds, int r, int khalf)
+{
+    const uint4 lo = *reinterpret_cast<const uint4*>(lds + swz(r, 2 * khalf));
+    const uint4 hi = *reinterpret_cast<const uint4*>(lds + swz(r, 2 * khalf + 1));
+    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z,
+               (int)hi.w};
+}
+
+// Workgroup barrier ordering LDS only: global loads still in flight (the
+// prefetch ring) are not drained; their registers are waited on at first use.
+__device__ __forceinline__ void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Raw flag bytes of the 32 elements [32 h, 32 h + 32) of one (group, row),
+// whose 64 / GS flag bytes start at `p` (loaded as is: expanding them right
+// after the load would make the prefetch wait for it).
+// (kept in a 16-bit type where 16 bits suffice, so that the zero extension
+// happens when the ring slot is decoded, not right after the load).
+template <int GS>
+using FlagRaw = typename std::conditional<GS == 8, uint32_t, uint16_t>::type;
+
+template <int GS>
+__device__ __forceinline__ FlagRaw<GS> load_flags_raw(const uint8_t* __restrict__ p, int h)
+{
+    if constexpr (GS == 8)
+        return *reinterpret_cast<const uint32_t*>(p + h * 4);
+    else if constexpr (GS == 16)
+        return *reinterpret_cast<const uint16_t*>(p + h * 2);
+    else if constexpr (GS == 32)
+        return p[h];
+    else
+        return p[0];
+}
+
+// Raw flags -> 8 * FLAG of each 8-element word i (0..3) of the half, one per byte.
+template <int GS>
+__device__ __forceinline__ uint32_t expand_flags8(uint32_t raw)
+{
+    uint32_t f;
+    if constexpr (GS == 8)
+        f = raw;
+    else if constexpr (GS == 16)
+        f = __builtin_amdgcn_perm(0u, raw, 0x01010000u);
+    else
+        f = __builtin_amdgcn_perm(0u, raw, 0x00000000u);
+    return f << 3;    // FLAG <= 4, so 8 * FLAG stays inside its byte
+}
+
+// Half (16 nibbles, words 2H and 2H+1) of one activation row-half -> 16 fp8
+// bytes = chunk 2h + H of the decoded row.
+template <int GS, int H>
+__device__ __forceinline__ void decode_act_half(uint8_t* row_base, int h, uint32_t w0, uint32_t w1,
+                                                uint32_t flags8, int r)
+{
+    const Fp8Table t0 = fp8_table<2 * H>(flags8);
+    const Fp8Table t1 = GS == 8 ? fp8_table<2 * H + 1>(flags8) : t0;
+    const uint2 d0 = decode_nibbles_fp8(w0, t0);
+    const uint2 d1 = decode_nibbles_fp8(w1, t1);
+    *reinterpret_cast<uint4*>(row_base + swz(r, 2 * h + H)) = make_uint4(d0.x, d0.y, d1.x, d1.y);
+}
+
+// Quarter (words 2q and 2q+1) of one weight column -> 16 fp8 bytes = chunk q
+// of the decoded column (no shift on weights).
+__device__ __forceinline__ void decode_weight_quarter(uint8_t* row_base, int q, uint32_t w0,
+                                                      uint32_t w1, int r)
+{
+    const Fp8Table t{kTabLo, kTabHi};
+    const uint2 d0 = decode_nibbles_fp8(w0, t);
+    const uint2 d1 = decode_nibbles_fp8(w1, t);
+    *reinterpret_cast<uint4*>(row_base + swz(r, q)) = make_uint4(d0.x, d0.y, d1.x, d1.y);
+}
+
+// Staging roles: thread t decodes A row t/2, half t%2 (16 code bytes) and
+// B column t/4, quarter t%4 (8 code bytes); threads < BM carry s_a of row t
+// and BM <= t < BM + BN s_w of column t - BM.  Every thread issues the same
+// four loads per group (the rest load a scale they do not use), so the
+// compiler can count them and wait only for the group being decoded.  Rows
+// past M and columns past the padded N read a clamped, valid row / column:
+// they only feed outputs that are never stored, so the main loop needs no
+// bounds checks.
 template <int GS, bool I32OUT>
-__global__ __launch_bounds__(kThreads) void w4a4_gemm_kernel(
+__global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t As[BM * kRowBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[BN * kRowBytes];
-    __shared__ float sa_s[BM];
-    __shared__ float sw_s[BN];
+    __shared__ __attribute__((aligned(16))) uint8_t As[2][BM * 64];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][BN * 64];
+    // group scales as fp16 bits; entries BM (BN) stay 0: the upper half-wave's
+    // k = 8 operand slot of the outer-product MFMA reads them
+    __shared__ uint16_t sas[2][BM + 8];
+    __shared__ uint16_t sws[2][BN + 8];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -84,137 +171,194 @@ __global__ __launch_bounds__(kThreads) void w4a4_gemm_kernel(
     const int64_t m0 = (int64_t)blockIdx.y * BM;
     const int64_t n0 = (int64_t)blockIdx.x * BN;
     const int G = (int)(K / 64);
-    const int64_t panels = (N + kPanel - 1) / kPanel;
+    const int64_t padded_n = (N + kPanel - 1) / kPanel * kPanel;
 
-    // staging role: row / column (tid / 2) and half of the group (tid % 2)
-    const int sr = tid >> 1;
-    const int sh = tid & 1;
-    const int64_t am = m0 + sr;
-    const int64_t bn = n0 + sr;
-    const bool a_ok = am < M;
-    const bool b_ok = bn < panels * kPanel;
-    const uint8_t* a_codes = codes + am * (K / 2) + sh * 16;
-    const uint8_t* b_base = w_packed + (bn / kPanel) * G * kChunkBytes;
-    const int b_col = (int)(bn % kPanel);
+    static_assert(2 * BM == kThreadsPerBlock && 4 * BN == kThreadsPerBlock, "staging roles");
+    const int sr = tid >> 1;          // A row
+    const int sh = tid & 1;           // A half
+    const int bc = tid >> 2;          // B column
+    const int bq = tid & 3;           // B quarter
+    // activations are K-group-major: group g of row m at (g * M + m)
+    const int64_t am = min(m0 + sr, M - 1);
+    const uint8_t* a_code_ptr = codes + am * 32 + sh * 16;
+    const uint8_t* a_flag_ptr = flags + am * (64 / GS);
+    const int64_t a_code_stride = M * 32;
+    const int64_t a_flag_stride = M * (64 / GS);
+    const int64_t bn = min(n0 + bc, padded_n - 1);
+    const uint8_t* b_code_ptr = w_packed + (bn / kPanel) * G * kChunkBytes + (bn % kPanel) * 32 +
+                                bq * 8;
+    const bool sa_role = tid < BM;
+    const bool sw_role = tid >= BM && tid < BM + BN;
+    // scale source: s_a of a row (K-group-major, stride M per group) or s_w of
+    // a column (inside the packed chunk, stride kChunkBytes per group)
+    const int64_t sam = min(m0 + (tid & (BM - 1)), M - 1);
+    const int64_t swn = min(n0 + (tid & (BN - 1)), padded_n - 1);
+    const uint8_t* s_ptr = sw_role ? w_packed + (swn / kPanel) * G * kChunkBytes +
+                                         kChunkCodeBytes + (swn % kPanel) * 2
+                                   : reinterpret_cast<const uint8_t*>(scales + sam);
+    const int64_t s_stride = sw_role ? (int64_t)kChunkBytes : M * 2;
 
-    // compute role: 2 x 2 waves, each 64 x 64 = 2 x 2 MFMA tiles of 32 x 32
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
-
-    v16f acc[2][2];
+    struct Raw {
+        uint4 a;
+        uint2 b;
+        FlagRaw<GS> f;
+        uint16_t s;
+    };
+    auto fetch = [&](Raw& r, int g) {
+        r.a = *reinterpret_cast<const uint4*>(a_code_ptr + g * a_code_stride);
+        r.f = load_flags_raw<GS>(a_flag_ptr + g * a_flag_stride, sh);
+        r.b = *reinterpret_cast<const uint2*>(b_code_ptr + (int64_t)g * kChunkBytes);
+        r.s = *reinterpret_cast<const uint16_t*>(s_ptr + g * s_stride);
+    };
+    // ---- compute roles
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
+    const int l32 = lane & 31;
+    const int khalf = lane >> 5;
+    int sa_idx[TM], sw_idx[TN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
+        sa_idx[i] = khalf ? BM : wm * WM + i * 32 + l32;
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
+        sw_idx[j] = khalf ? BN : wn * WN + j * 32 + l32;
+
+    v16f acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 acc[i][j][r] = 0.0f;
 
-    for (int g = 0; g < G; ++g) {
-        // ---- stage A: 32 codes of row am -> fp8 in LDS
-        {
-            uint4 c4 = make_uint4(0, 0, 0, 0);
-            uint32_t fl[4] = {0, 0, 0, 0};
-            float sa = 0.0f;
-            if (a_ok) {
-                c4 = *reinterpret_cast<const uint4*>(a_codes + g * 32);
-                load_flags<GS>(flags, am, K, g, sh, fl);
-                sa = f16_to_f32(scales[am * G + g]);
-            }
-            const uint2 d0 = decode_nibbles_fp8(c4.x, fl[0]);
-            const uint2 d1 = decode_nibbles_fp8(c4.y, fl[1]);
-            const uint2 d2 = decode_nibbles_fp8(c4.z, fl[2]);
-            const uint2 d3 = decode_nibbles_fp8(c4.w, fl[3]);
-            uint4* dst = reinterpret_cast<uint4*>(As + sr * kRowBytes + sh * 32);
-            dst[0] = make_uint4(d0.x, d0.y, d1.x, d1.y);
-            dst[1] = make_uint4(d2.x, d2.y, d3.x, d3.y);
-            if (sh == 0)
-                sa_s[sr] = sa;
+    // Decode of the next group, cut into four slices so that each slice's VALU
+    // work is issued while the matrix unit runs one tile's MFMAs.
+    auto stage_slice = [&](const Raw& r, int buf, int slice) {
+        switch (slice) {
+        case 0:
+            decode_act_half<GS, 0>(As[buf], sh, r.a.x, r.a.y, expand_flags8<GS>((uint32_t)r.f), sr);
+            break;
+        case 1:
+            decode_act_half<GS, 1>(As[buf], sh, r.a.z, r.a.w, expand_flags8<GS>((uint32_t)r.f), sr);
+            break;
+        case 2:
+            decode_weight_quarter(Bs[buf], bq, r.b.x, r.b.y, bc);
+            break;
+        default:
+            if (sa_role)
+                sas[buf][tid] = r.s;
+            else if (sw_role)
+                sws[buf][tid - BM] = r.s;
+            break;
         }
-        // ---- stage B: 32 weight codes of column bn -> fp8 in LDS
-        {
-            uint4 c4 = make_uint4(0, 0, 0, 0);
-            float sw = 0.0f;
-            if (b_ok) {
-                const uint8_t* chunk = b_base + (int64_t)g * kChunkBytes;
-                c4 = *reinterpret_cast<const uint4*>(chunk + b_col * 32 + sh * 16);
-                sw = f16_to_f32(reinterpret_cast<const uint16_t*>(chunk + kChunkCodeBytes)[b_col]);
-            }
-            const uint2 d0 = decode_nibbles_fp8(c4.x, 0);
-            const uint2 d1 = decode_nibbles_fp8(c4.y, 0);
-            const uint2 d2 = decode_nibbles_fp8(c4.z, 0);
-            const uint2 d3 = decode_nibbles_fp8(c4.w, 0);
-            uint4* dst = reinterpret_cast<uint4*>(Bs + sr * kRowBytes + sh * 32);
-            dst[0] = make_uint4(d0.x, d0.y, d1.x, d1.y);
-            dst[1] = make_uint4(d2.x, d2.y, d3.x, d3.y);
-            if (sh == 0)
-                sw_s[sr] = sw;
-        }
-        __syncthreads();
+    };
+    auto stage = [&](const Raw& r, int buf) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            stage_slice(r, buf, q);
+    };
 
-        // ---- MFMA over the group + per-group dequantization
-        v8i a_frag[2], b_frag[2];
+    // One group: per tile, the MFMAs, then a decode slice of the next group
+    // (VALU work that runs while the matrix unit computes), then the tile's
+    // FMAs.  Scheduling barriers keep this order; the asm statement pins each
+    // tile's FMAs (without a use, LLVM sinks them to the end of the loop and
+    // keeps every tile's results live).
+    auto compute = [&](int buf, const Raw& next, bool more, int next_buf) {
+        v8i bf[TN];
+        v8h sw_op[TN];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const uint4* src = reinterpret_cast<const uint4*>(
-                As + (wm * 64 + i * 32 + (lane & 31)) * kRowBytes + (lane >> 5) * 32);
-            const uint4 lo = src[0], hi = src[1];
-            a_frag[i] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
-                            (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+        for (int j = 0; j < TN; ++j) {
+            bf[j] = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
+            sw_op[j] = v8h{};
+            if constexpr (!I32OUT)
+                sw_op[j][0] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
         }
+        constexpr int T = TM * TN;
+        static_assert(T == 4, "four decode slices per group");
+        const v16f zero = {};
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const uint4* src = reinterpret_cast<const uint4*>(
-                Bs + (wn * 64 + j * 32 + (lane & 31)) * kRowBytes + (lane >> 5) * 32);
-            const uint4 lo = src[0], hi = src[1];
-            b_frag[j] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
-                            (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-        }
+        for (int i = 0; i < TM; ++i) {
+            const v8i af = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
+            // fp16 operand of the scale outer product: only k = 0 is non-zero
+            v8h sa_op = v8h{};
+            if constexpr (!I32OUT)
+                sa_op[0] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            float sa_r[16];
-            if constexpr (!I32OUT) {
+            for (int j = 0; j < TN; ++j) {
+                const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf[j], zero, 0,
+                                                                               0, 0, 0, 0, 0);
+                v16f sc;
+                if constexpr (!I32OUT)
+                    sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op[j], zero, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                if (more)
+                    stage_slice(next, next_buf, i * TN + j);
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    sa_r[r] = sa_s[wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)];
-            }
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                v16f zero;
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    zero[r] = 0.0f;
-                const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                    a_frag[i], b_frag[j], zero, 0, 0, 0, 0, 0, 0);
-                if constexpr (I32OUT) {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
+                for (int r = 0; r < 16; ++r) {
+                    if constexpr (I32OUT)
                         acc[i][j][r] += p[r];
-                } else {
-                    const float sw = sw_s[wn * 64 + j * 32 + (lane & 31)];
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        acc[i][j][r] = fmaf(p[r], sa_r[r] * sw, acc[i][j][r]);
+                    else
+                        acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
                 }
+                asm volatile("" : "+v"(acc[i][j]));
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
-        __syncthreads();
+    };
+
+    // ---- pipeline: register ring of kDepth groups, fp8 LDS double buffer
+    if (tid < 8) {
+        sas[tid & 1][BM + (tid >> 1)] = 0;
+        sws[tid & 1][BN + (tid >> 1)] = 0;
+    }
+    Raw ring[kDepth];
+#pragma unroll
+    for (int u = 0; u < kDepth; ++u)
+        fetch(ring[u], min(u, G - 1));
+    stage(ring[0], 0);
+    lds_sync();
+
+    // Main loop over full chunks of kDepth groups: straight-line code with the
+    // same loads on every path (prefetch indices past the end are clamped to
+    // the last group: a harmless reload), so the compiler waits only for the
+    // ring slot being decoded, not for the loads just issued.
+    int g0 = 0;
+    for (; g0 + kDepth <= G; g0 += kDepth) {
+#pragma unroll
+        for (int u = 0; u < kDepth; ++u) {
+            const int g = g0 + u;
+            // ring slot u held group g (staged one iteration ago): refill it
+            fetch(ring[u], min(g + kDepth, G - 1));
+            compute(g & 1, ring[(u + 1) % kDepth], true, (g + 1) & 1);
+            lds_sync();
+        }
+    }
+    // Tail: the last G % kDepth groups (already in the ring).
+#pragma unroll
+    for (int u = 0; u < kDepth - 1; ++u) {
+        const int g = g0 + u;
+        if (g < G) {
+            compute(g & 1, ring[(u + 1) % kDepth], g + 1 < G, (g + 1) & 1);
+            lds_sync();
+        }
     }
 
-    // ---- epilogue
+    // ---- epilogue: lane holds column l32 of each 32 x 32 tile, rows 8 (r/4) + 4 khalf + r%4
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int j = 0; j < TN; ++j) {
+        const int64_t col = n0 + wn * WN + j * 32 + l32;
+        if (col >= N)
+            continue;
+        float b = 0.0f;
+        if (!I32OUT && bias)
+            b = __uint_as_float((uint32_t)bias[col] << 16);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-            if (col >= N)
-                continue;
-            float b = 0.0f;
-            if (!I32OUT && bias)
-                b = __uint_as_float((uint32_t)bias[col] << 16);
+        for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int64_t row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
                 if (row >= M)
                     continue;
                 if constexpr (I32OUT) {
@@ -230,33 +374,38 @@ __global__ __launch_bounds__(kThreads) void w4a4_gemm_kernel(
     }
 }
 
+template <bool I32OUT, int GS>
+hipError_t launch_gs(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
+                     const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
+                     int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue,
+                     hipStream_t stream)
+{
+    const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
+    w4a4_gemm_kernel<GS, I32OUT><<<grid, dim3(kThreadsPerBlock), 0, stream>>>(
+        codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, epilogue);
+    return hipGetLastError();
+}
+
 template <bool I32OUT>
 hipError_t launch(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
                   const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                   int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group, int epilogue,
                   hipStream_t stream)
 {
-    const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
-    const dim3 block(kThreads);
     switch (lzs_group) {
     case 8:
-        w4a4_gemm_kernel<8, I32OUT><<<grid, block, 0, stream>>>(codes, flags, scales, w_packed,
-                                                                bias, y, yi, M, N, K, ldy, epilogue);
-        break;
+        return launch_gs<I32OUT, 8>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
+                                    epilogue, stream);
     case 16:
-        w4a4_gemm_kernel<16, I32OUT><<<grid, block, 0, stream>>>(codes, flags, scales, w_packed,
-                                                                 bias, y, yi, M, N, K, ldy, epilogue);
-        break;
+        return launch_gs<I32OUT, 16>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
+                                     epilogue, stream);
     case 32:
-        w4a4_gemm_kernel<32, I32OUT><<<grid, block, 0, stream>>>(codes, flags, scales, w_packed,
-                                                                 bias, y, yi, M, N, K, ldy, epilogue);
-        break;
+        return launch_gs<I32OUT, 32>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
+                                     epilogue, stream);
     default:
-        w4a4_gemm_kernel<64, I32OUT><<<grid, block, 0, stream>>>(codes, flags, scales, w_packed,
-                                                                 bias, y, yi, M, N, K, ldy, epilogue);
-        break;
+        return launch_gs<I32OUT, 64>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
+                                     epilogue, stream);
     }
-    return hipGetLastError();
 }
 
 }  // namespace

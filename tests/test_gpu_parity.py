@@ -38,10 +38,10 @@ def _act_parity(xb, gs, ldx_pad=0, with_zeros=True):
     torch.cuda.synchronize()
     ref = oracle.quantize_act(xb, lzs_group=gs)
     np.testing.assert_array_equal(got.codes.cpu().numpy(), ref.codes)
-    np.testing.assert_array_equal(got.flags.cpu().numpy(), ref.flags)
-    np.testing.assert_array_equal(to_host_u16(got.scales), ref.scales)
+    np.testing.assert_array_equal(got.flags.cpu().numpy(), ref.abi_flags)
+    np.testing.assert_array_equal(to_host_u16(got.scales), ref.abi_scales)
     if with_zeros:
-        np.testing.assert_array_equal(got.zeros.cpu().numpy(), ref.zeros)
+        np.testing.assert_array_equal(got.zeros.cpu().numpy(), ref.abi_zeros)
     return got, ref
 
 
@@ -102,7 +102,7 @@ def test_quantize_empty():
     q = _q()
     xd = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
     out = q.quantize_act(xd, 16)
-    assert out.codes.shape == (0, 64)
+    assert out.codes.shape == (2, 0, 32)
 
 
 @pytest.mark.parametrize("cfg,layer", LAYERS)
@@ -147,8 +147,8 @@ def _gemm_case(xb, wb, gs):
     M, K = xb.shape
     qa = q.QuantizedAct(
         codes=torch.from_numpy(a_ref.codes).cuda(),
-        flags=torch.from_numpy(a_ref.flags).cuda(),
-        scales=torch.from_numpy(a_ref.scales.view(np.int16)).cuda(),
+        flags=torch.from_numpy(a_ref.abi_flags).cuda(),
+        scales=torch.from_numpy(a_ref.abi_scales.view(np.int16)).cuda(),
         zeros=None, M=M, K=K, lzs_group=gs)
     pw = q.pack_weight(to_dev_bf16(wb))
     return qa, pw, a_ref, wq_ref, sw_ref

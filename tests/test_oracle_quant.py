@@ -194,14 +194,20 @@ def test_pack_unpack_layout():
     g = np.random.Generator(np.random.PCG64(91))
     c = g.integers(-7, 8, size=(5, 64)).astype(np.int8)
     codes = oracle.pack_codes(c)
-    assert codes.shape == (5, 32)
-    np.testing.assert_array_equal(oracle.unpack_codes(codes, 64), c)
+    assert codes.shape == (1, 5, 32)
+    np.testing.assert_array_equal(oracle.unpack_codes(codes, 5, 64), c)
+    c2 = g.integers(-7, 8, size=(3, 192)).astype(np.int8)
+    np.testing.assert_array_equal(oracle.unpack_codes(oracle.pack_codes(c2), 3, 192), c2)
     # element 8j+i -> nibble (i/2) + 4(i%2) of little-endian word j; sign-magnitude
-    c1 = np.zeros((1, 8), np.int8)
-    c1[0, 1] = -3          # odd element 1 -> nibble 4 (byte 2, low nibble): 0xB
-    c1[0, 6] = 5           # even element 6 -> nibble 3 (byte 1, high nibble): 0x5
+    c1 = np.zeros((2, 128), np.int8)
+    c1[1, 64 + 1] = -3     # row 1, group 1, odd element 1 -> nibble 4 (byte 2): 0xB
+    c1[1, 64 + 6] = 5      # even element 6 -> nibble 3 (byte 1, high nibble): 0x5
+    c1[0, 8 + 2] = 7       # row 0, group 0, word 1, element 2 -> nibble 1 of word 1
     out = oracle.pack_codes(c1)
-    assert list(out[0]) == [0x00, 0x50, 0x0B, 0x00]
+    # K-group-major: (group 1, row 1) is the fourth 32-byte block
+    assert list(out[1, 1, :4]) == [0x00, 0x50, 0x0B, 0x00]
+    assert list(out[0, 0, 4:8]) == [0x70, 0x00, 0x00, 0x00]
+    assert out.sum() == 0x50 + 0x0B + 0x70
 
 
 def test_weight_quantizer():
