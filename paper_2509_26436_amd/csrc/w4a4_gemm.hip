@@ -93,16 +93,14 @@ template <int GS>
 using FlagRaw = typename std::conditional<GS == 8, uint32_t, uint16_t>::type;
 
 template <int GS>
-__device__ __forceinline__ FlagRaw<GS> load_flags_raw(const uint8_t* __restrict__ p, int h)
+__device__ __forceinline__ FlagRaw<GS> load_flags_raw(const uint8_t* __restrict__ p)
 {
     if constexpr (GS == 8)
-        return *reinterpret_cast<const uint32_t*>(p + h * 4);
+        return *reinterpret_cast<const uint32_t*>(p);
     else if constexpr (GS == 16)
-        return *reinterpret_cast<const uint16_t*>(p + h * 2);
-    else if constexpr (GS == 32)
-        return p[h];
+        return *reinterpret_cast<const uint16_t*>(p);
     else
-        return p[0];
+        return *p;
 }
 
 // Raw flags -> 8 * FLAG of each 8-element word i (0..3) of the half, one per byte.
@@ -117,30 +115,6 @@ __device__ __forceinline__ uint32_t expand_flags8(uint32_t raw)
     else
         f = __builtin_amdgcn_perm(0u, raw, 0x00000000u);
     return f << 3;    // FLAG <= 4, so 8 * FLAG stays inside its byte
-}
-
-// Half (16 nibbles, words 2H and 2H+1) of one activation row-half -> 16 fp8
-// bytes = chunk 2h + H of the decoded row.
-template <int GS, int H>
-__device__ __forceinline__ void decode_act_half(uint8_t* row_base, int h, uint32_t w0, uint32_t w1,
-                                                uint32_t flags8, int r)
-{
-    const Fp8Table t0 = fp8_table<2 * H>(flags8);
-    const Fp8Table t1 = GS == 8 ? fp8_table<2 * H + 1>(flags8) : t0;
-    const uint2 d0 = decode_nibbles_fp8(w0, t0);
-    const uint2 d1 = decode_nibbles_fp8(w1, t1);
-    *reinterpret_cast<uint4*>(row_base + swz(r, 2 * h + H)) = make_uint4(d0.x, d0.y, d1.x, d1.y);
-}
-
-// Quarter (words 2q and 2q+1) of one weight column -> 16 fp8 bytes = chunk q
-// of the decoded column (no shift on weights).
-__device__ __forceinline__ void decode_weight_quarter(uint8_t* row_base, int q, uint32_t w0,
-                                                      uint32_t w1, int r)
-{
-    const Fp8Table t{kTabLo, kTabHi};
-    const uint2 d0 = decode_nibbles_fp8(w0, t);
-    const uint2 d1 = decode_nibbles_fp8(w1, t);
-    *reinterpret_cast<uint4*>(row_base + swz(r, q)) = make_uint4(d0.x, d0.y, d1.x, d1.y);
 }
 
 // Staging roles: thread t decodes A row t/2, half t%2 (16 code bytes) and
@@ -178,24 +152,28 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const int sh = tid & 1;           // A half
     const int bc = tid >> 2;          // B column
     const int bq = tid & 3;           // B quarter
-    // activations are K-group-major: group g of row m at (g * M + m)
+    // Global addresses = a wave-uniform base for group g (scalar registers)
+    // plus a fixed 32-bit per-lane offset.  Activations are K-group-major:
+    // group g of row m at (g * M + m).
     const int64_t am = min(m0 + sr, M - 1);
-    const uint8_t* a_code_ptr = codes + am * 32 + sh * 16;
-    const uint8_t* a_flag_ptr = flags + am * (64 / GS);
-    const int64_t a_code_stride = M * 32;
-    const int64_t a_flag_stride = M * (64 / GS);
+    const uint32_t a_code_off = (uint32_t)(am * 32 + sh * 16);
+    constexpr int kFlagHalf = GS == 64 ? 0 : 32 / GS;   // flag bytes of the first half
+    const uint32_t a_flag_off = (uint32_t)(am * (64 / GS) + sh * kFlagHalf);
     const int64_t bn = min(n0 + bc, padded_n - 1);
-    const uint8_t* b_code_ptr = w_packed + (bn / kPanel) * G * kChunkBytes + (bn % kPanel) * 32 +
-                                bq * 8;
-    const bool sa_role = tid < BM;
-    const bool sw_role = tid >= BM && tid < BM + BN;
-    // scale source: s_a of a row (K-group-major, stride M per group) or s_w of
-    // a column (inside the packed chunk, stride kChunkBytes per group)
+    const uint32_t b_code_off = (uint32_t)((bn / kPanel) * G * kChunkBytes + (bn % kPanel) * 32 +
+                                           bq * 8);
+    // scales: waves 0-3 carry s_a of row tid (K-group-major, stride M per
+    // group), waves 4-5 s_w of column tid - BM (inside the packed chunk,
+    // stride kChunkBytes per group); waves 6-7 load an s_a they do not use
+    const int uwave = __builtin_amdgcn_readfirstlane(wave);
+    const bool sa_role = uwave < 4;
+    const bool sw_role = uwave == 4 || uwave == 5;
     const int64_t sam = min(m0 + (tid & (BM - 1)), M - 1);
     const int64_t swn = min(n0 + (tid & (BN - 1)), padded_n - 1);
-    const uint8_t* s_ptr = sw_role ? w_packed + (swn / kPanel) * G * kChunkBytes +
-                                         kChunkCodeBytes + (swn % kPanel) * 2
-                                   : reinterpret_cast<const uint8_t*>(scales + sam);
+    const uint32_t s_off = sw_role ? (uint32_t)((swn / kPanel) * G * kChunkBytes + kChunkCodeBytes +
+                                                (swn % kPanel) * 2)
+                                   : (uint32_t)(sam * 2);
+    const uint8_t* s_base = sw_role ? w_packed : reinterpret_cast<const uint8_t*>(scales);
     const int64_t s_stride = sw_role ? (int64_t)kChunkBytes : M * 2;
 
     struct Raw {
@@ -205,10 +183,14 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         uint16_t s;
     };
     auto fetch = [&](Raw& r, int g) {
-        r.a = *reinterpret_cast<const uint4*>(a_code_ptr + g * a_code_stride);
-        r.f = load_flags_raw<GS>(a_flag_ptr + g * a_flag_stride, sh);
-        r.b = *reinterpret_cast<const uint2*>(b_code_ptr + (int64_t)g * kChunkBytes);
-        r.s = *reinterpret_cast<const uint16_t*>(s_ptr + g * s_stride);
+        const uint8_t* ca = codes + (int64_t)g * (M * 32);
+        const uint8_t* cf = flags + (int64_t)g * (M * (64 / GS));
+        const uint8_t* cb = w_packed + (int64_t)g * kChunkBytes;
+        const uint8_t* cs = s_base + (int64_t)g * s_stride;
+        r.a = *reinterpret_cast<const uint4*>(ca + a_code_off);
+        r.f = load_flags_raw<GS>(cf + a_flag_off);
+        r.b = *reinterpret_cast<const uint2*>(cb + b_code_off);
+        r.s = *reinterpret_cast<const uint16_t*>(cs + s_off);
     };
     // ---- compute roles
     const int wm = wave / WAVES_N;
@@ -234,29 +216,62 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
 
     // Decode of the next group, cut into four slices so that each slice's VALU
     // work is issued while the matrix unit runs one tile's MFMAs.
-    auto stage_slice = [&](const Raw& r, int buf, int slice) {
-        switch (slice) {
+    // Decode of the next group in eight pieces, two per MFMA tile: piece 2t
+    // goes between tile t's fp8 MFMA and its scale MFMA, piece 2t+1 right
+    // before its FMAs.  Tiles 0 and 1 decode the two words pairs of the
+    // activation row half, tile 2 the weight column quarter, tile 3 stores
+    // the scales.
+    uint32_t fl8 = 0;      // 8 * FLAG per activation word of this half
+    Fp8Table t_lo, t_hi;   // tables of the two words being decoded
+    uint2 d_first;         // first word of a pair, decoded
+    auto stage_piece = [&](const Raw& r, int buf, int piece) {
+        switch (piece) {
         case 0:
-            decode_act_half<GS, 0>(As[buf], sh, r.a.x, r.a.y, expand_flags8<GS>((uint32_t)r.f), sr);
+            fl8 = expand_flags8<GS>((uint32_t)r.f);
+            t_lo = fp8_table<0>(fl8);
+            t_hi = GS == 8 ? fp8_table<1>(fl8) : t_lo;
+            d_first = decode_nibbles_fp8(r.a.x, t_lo);
             break;
-        case 1:
-            decode_act_half<GS, 1>(As[buf], sh, r.a.z, r.a.w, expand_flags8<GS>((uint32_t)r.f), sr);
+        case 1: {
+            const uint2 d = decode_nibbles_fp8(r.a.y, t_hi);
+            *reinterpret_cast<uint4*>(As[buf] + swz(sr, 2 * sh)) =
+                make_uint4(d_first.x, d_first.y, d.x, d.y);
             break;
+        }
         case 2:
-            decode_weight_quarter(Bs[buf], bq, r.b.x, r.b.y, bc);
+            t_lo = GS <= 16 ? fp8_table<2>(fl8) : t_lo;
+            t_hi = GS == 8 ? fp8_table<3>(fl8) : t_lo;
+            d_first = decode_nibbles_fp8(r.a.z, t_lo);
             break;
-        default:
+        case 3: {
+            const uint2 d = decode_nibbles_fp8(r.a.w, t_hi);
+            *reinterpret_cast<uint4*>(As[buf] + swz(sr, 2 * sh + 1)) =
+                make_uint4(d_first.x, d_first.y, d.x, d.y);
+            break;
+        }
+        case 4:
+            d_first = decode_nibbles_fp8(r.b.x, Fp8Table{kTabLo, kTabHi});
+            break;
+        case 5: {
+            const uint2 d = decode_nibbles_fp8(r.b.y, Fp8Table{kTabLo, kTabHi});
+            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, bq)) =
+                make_uint4(d_first.x, d_first.y, d.x, d.y);
+            break;
+        }
+        case 6:
             if (sa_role)
                 sas[buf][tid] = r.s;
             else if (sw_role)
                 sws[buf][tid - BM] = r.s;
             break;
+        default:
+            break;
         }
     };
     auto stage = [&](const Raw& r, int buf) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            stage_slice(r, buf, q);
+        for (int q = 0; q < 8; ++q)
+            stage_piece(r, buf, q);
     };
 
     // One group: per tile, the MFMAs, then a decode slice of the next group
@@ -277,35 +292,45 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         constexpr int T = TM * TN;
         static_assert(T == 4, "four decode slices per group");
         const v16f zero = {};
+        v8i af[TM];
+        v8h sa_op[TM];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
-            const v8i af = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
+            af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
             // fp16 operand of the scale outer product: only k = 0 is non-zero
-            v8h sa_op = v8h{};
+            sa_op[i] = v8h{};
             if constexpr (!I32OUT)
-                sa_op[0] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf[j], zero, 0,
-                                                                               0, 0, 0, 0, 0);
-                v16f sc;
-                if constexpr (!I32OUT)
-                    sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op[j], zero, 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
-                if (more)
-                    stage_slice(next, next_buf, i * TN + j);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    if constexpr (I32OUT)
-                        acc[i][j][r] += p[r];
-                    else
-                        acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
-                }
-                asm volatile("" : "+v"(acc[i][j]));
-                __builtin_amdgcn_sched_barrier(0);
-            }
+                sa_op[i][0] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
         }
+        auto tile = [&](int i, int j, bool interleave) {
+            // in-order issue: VALU work between the two MFMAs keeps the wave
+            // busy while the matrix unit finishes the first one
+            const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                af[i], bf[j], zero, 0, 0, 0, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (interleave && more)
+                stage_piece(next, next_buf, 2 * (i * TN + j));
+            __builtin_amdgcn_sched_barrier(0);
+            v16f sc;
+            if constexpr (!I32OUT)
+                sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op[i], sw_op[j], zero, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (interleave && more)
+                stage_piece(next, next_buf, 2 * (i * TN + j) + 1);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                if constexpr (I32OUT)
+                    acc[i][j][r] += p[r];
+                else
+                    acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
+            }
+            asm volatile("" : "+v"(acc[i][j]));
+            __builtin_amdgcn_sched_barrier(0);
+        };
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+            tile(t / TN, t % TN, true);
     };
 
     // ---- pipeline: register ring of kDepth groups, fp8 LDS double buffer
@@ -320,28 +345,35 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     stage(ring[0], 0);
     lds_sync();
 
-    // Main loop over full chunks of kDepth groups: straight-line code with the
-    // same loads on every path (prefetch indices past the end are clamped to
-    // the last group: a harmless reload), so the compiler waits only for the
-    // ring slot being decoded, not for the loads just issued.
-    int g0 = 0;
-    for (; g0 + kDepth <= G; g0 += kDepth) {
+    // Main loop over chunks of 2 * kDepth groups (ring slot and LDS buffer are
+    // then compile-time constants in every unrolled copy): straight-line code
+    // with the same loads on every path (prefetch indices past the end are
+    // clamped to the last group: a harmless reload), so the compiler waits
+    // only for the ring slot being decoded, not for the loads just issued.
+    constexpr int kUnroll = 2 * kDepth;
+    {
+        int g0 = 0;
+        for (; g0 + kUnroll <= G; g0 += kUnroll) {
 #pragma unroll
-        for (int u = 0; u < kDepth; ++u) {
-            const int g = g0 + u;
-            // ring slot u held group g (staged one iteration ago): refill it
-            fetch(ring[u], min(g + kDepth, G - 1));
-            compute(g & 1, ring[(u + 1) % kDepth], true, (g + 1) & 1);
-            lds_sync();
+            for (int u = 0; u < kUnroll; ++u) {
+                const int g = g0 + u;
+                // ring slot u % kDepth held group g (staged one iteration ago): refill it
+                fetch(ring[u % kDepth], min(g + kDepth, G - 1));
+                compute(u & 1, ring[(u + 1) % kDepth], true, (u + 1) & 1);
+                lds_sync();
+            }
         }
-    }
-    // Tail: the last G % kDepth groups (already in the ring).
+        // Tail: the last G % kUnroll groups (their prefetches are issued above
+        // or inside this loop in the same ring order).
 #pragma unroll
-    for (int u = 0; u < kDepth - 1; ++u) {
-        const int g = g0 + u;
-        if (g < G) {
-            compute(g & 1, ring[(u + 1) % kDepth], g + 1 < G, (g + 1) & 1);
-            lds_sync();
+        for (int u = 0; u < kUnroll - 1; ++u) {
+            const int g = g0 + u;
+            if (g < G) {
+                if (g + kDepth < G)
+                    fetch(ring[u % kDepth], g + kDepth);
+                compute(u & 1, ring[(u + 1) % kDepth], g + 1 < G, (u + 1) & 1);
+                lds_sync();
+            }
         }
     }
 
