@@ -5,8 +5,19 @@
 
 namespace {
 
-constexpr int64_t kMaxK = int64_t(1) << 20;       // codes of one row stay < 512 KiB
-constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxK = int64_t(1) << 20;       // at most 16384 groups per row
+// rows x groups of one call (M x K/64 or N x K/64): 2^34 elements, 32 GiB of
+// bf16 input; keeps every grid below 2^32 threads
+constexpr int64_t kMaxRowGroups = int64_t(1) << 28;
+
+// sizes that every entry point accepts: rows >= 0, 0 <= K <= kMaxK, K % 64 == 0
+// and rows * K / 64 <= kMaxRowGroups
+bool size_ok(int64_t rows, int64_t K)
+{
+    if (rows < 0 || K < 0 || K % 64 != 0 || K > kMaxK)
+        return false;
+    return K == 0 || rows <= kMaxRowGroups / (K / 64);
+}
 
 bool aligned16(const void* p)
 {
@@ -53,8 +64,7 @@ quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int6
 {
     if (group_size != 64 || !lzs_ok(lzs_group) || mode != QUARTZ_MODE_SYMMETRIC)
         return QUARTZ_ERR_UNSUPPORTED;
-    if (M < 0 || K < 0 || K % 64 != 0 || ldx < K || K > kMaxK || M > kMaxRows ||
-        (K > 0 && M > kMaxRows / (K / 64 > 0 ? K / 64 : 1)))
+    if (!size_ok(M, K) || ldx < K)
         return QUARTZ_ERR_SHAPE;
     if (ldx % 8 != 0)
         return QUARTZ_ERR_ALIGN;       // 16-byte aligned rows for the vector loads
@@ -81,8 +91,7 @@ quartz_status quartz_pack_weight(const void* w_bf16, int64_t N, int64_t K, int32
 {
     if (group_size != 64)
         return QUARTZ_ERR_UNSUPPORTED;
-    if (N < 0 || K < 0 || K % 64 != 0 || K > kMaxK || N > kMaxRows ||
-        (K > 0 && N > kMaxRows / (K / 64 > 0 ? K / 64 : 1)))
+    if (!size_ok(N, K))
         return QUARTZ_ERR_SHAPE;
     if (N == 0 || K == 0)
         return QUARTZ_OK;
@@ -99,7 +108,7 @@ quartz_status quartz_unpack_weight(const void* w_packed, int64_t N, int64_t K,
 {
     if (group_size != 64)
         return QUARTZ_ERR_UNSUPPORTED;
-    if (N < 0 || K < 0 || K % 64 != 0 || K > kMaxK || N > kMaxRows)
+    if (!size_ok(N, K))
         return QUARTZ_ERR_SHAPE;
     if (N == 0 || K == 0)
         return QUARTZ_OK;
@@ -117,8 +126,8 @@ static quartz_status check_gemm(const uint8_t* codes, const uint8_t* flags, cons
 {
     if (group_size != 64 || !lzs_ok(lzs_group))
         return QUARTZ_ERR_UNSUPPORTED;
-    if (M < 0 || N < 0 || K <= 0 || K % 64 != 0 || K > kMaxK || M > kMaxRows || N > kMaxRows ||
-        (M + 127) / 128 > 65535)
+    if (K <= 0 || !size_ok(M, K) || !size_ok(N, K) ||
+        (M + quartz::kGemmBlockRows - 1) / quartz::kGemmBlockRows > 65535)
         return QUARTZ_ERR_SHAPE;
     if (M == 0 || N == 0)
         return QUARTZ_OK;

@@ -45,7 +45,7 @@ __device__ __forceinline__ float gelu_tanh(float v)
 // Block tile BM x BN = 256 x 128, 8 waves as 4 (M) x 2 (N), wave tile 64 x 64
 // = 2 x 2 MFMA tiles of 32 x 32.  Two waves share each SIMD, so one wave's
 // VALU work (decode, dequantization) overlaps the other's MFMAs.
-constexpr int BM = 256;
+constexpr int BM = (int)kGemmBlockRows;
 constexpr int BN = 128;
 constexpr int kWaves = 8;
 constexpr int kThreadsPerBlock = 64 * kWaves;
@@ -152,16 +152,18 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const int sh = tid & 1;           // A half
     const int bc = tid >> 2;          // B column
     const int bq = tid & 3;           // B quarter
-    // Global addresses = a wave-uniform base for group g (scalar registers)
-    // plus a fixed 32-bit per-lane offset.  Activations are K-group-major:
-    // group g of row m at (g * M + m).
+    // Global addresses = a wave-uniform base for group g and this block
+    // (scalar registers) plus a small 32-bit per-lane offset.  Activations
+    // are K-group-major: group g of row m at (g * M + m).
     const int64_t am = min(m0 + sr, M - 1);
-    const uint32_t a_code_off = (uint32_t)(am * 32 + sh * 16);
+    const uint32_t a_code_off = (uint32_t)((am - m0) * 32 + sh * 16);
     constexpr int kFlagHalf = GS == 64 ? 0 : 32 / GS;   // flag bytes of the first half
-    const uint32_t a_flag_off = (uint32_t)(am * (64 / GS) + sh * kFlagHalf);
+    const uint32_t a_flag_off = (uint32_t)((am - m0) * (64 / GS) + sh * kFlagHalf);
+    // the block's columns n0 .. n0 + BN - 1 span two 64-column panels
+    const int64_t panel0 = n0 / kPanel;
     const int64_t bn = min(n0 + bc, padded_n - 1);
-    const uint32_t b_code_off = (uint32_t)((bn / kPanel) * G * kChunkBytes + (bn % kPanel) * 32 +
-                                           bq * 8);
+    const uint32_t b_code_off = (uint32_t)((bn / kPanel - panel0) * G * kChunkBytes +
+                                           (bn % kPanel) * 32 + bq * 8);
     // scales: waves 0-3 carry s_a of row tid (K-group-major, stride M per
     // group), waves 4-5 s_w of column tid - BM (inside the packed chunk,
     // stride kChunkBytes per group); waves 6-7 load an s_a they do not use
@@ -170,10 +172,14 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const bool sw_role = uwave == 4 || uwave == 5;
     const int64_t sam = min(m0 + (tid & (BM - 1)), M - 1);
     const int64_t swn = min(n0 + (tid & (BN - 1)), padded_n - 1);
-    const uint32_t s_off = sw_role ? (uint32_t)((swn / kPanel) * G * kChunkBytes + kChunkCodeBytes +
-                                                (swn % kPanel) * 2)
-                                   : (uint32_t)(sam * 2);
-    const uint8_t* s_base = sw_role ? w_packed : reinterpret_cast<const uint8_t*>(scales);
+    const uint32_t s_off = sw_role ? (uint32_t)((swn / kPanel - panel0) * G * kChunkBytes +
+                                                kChunkCodeBytes + (swn % kPanel) * 2)
+                                   : (uint32_t)((sam - m0) * 2);
+    const uint8_t* a_blk = codes + m0 * 32;
+    const uint8_t* f_blk = flags + m0 * (64 / GS);
+    const uint8_t* b_blk = w_packed + panel0 * G * kChunkBytes;
+    const uint8_t* s_base =
+        sw_role || I32OUT ? b_blk : reinterpret_cast<const uint8_t*>(scales + m0);
     const int64_t s_stride = sw_role ? (int64_t)kChunkBytes : M * 2;
 
     struct Raw {
@@ -183,14 +189,17 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         uint16_t s;
     };
     auto fetch = [&](Raw& r, int g) {
-        const uint8_t* ca = codes + (int64_t)g * (M * 32);
-        const uint8_t* cf = flags + (int64_t)g * (M * (64 / GS));
-        const uint8_t* cb = w_packed + (int64_t)g * kChunkBytes;
+        const uint8_t* ca = a_blk + (int64_t)g * (M * 32);
+        const uint8_t* cf = f_blk + (int64_t)g * (M * (64 / GS));
+        const uint8_t* cb = b_blk + (int64_t)g * kChunkBytes;
         const uint8_t* cs = s_base + (int64_t)g * s_stride;
         r.a = *reinterpret_cast<const uint4*>(ca + a_code_off);
         r.f = load_flags_raw<GS>(cf + a_flag_off);
         r.b = *reinterpret_cast<const uint2*>(cb + b_code_off);
-        r.s = *reinterpret_cast<const uint16_t*>(cs + s_off);
+        if constexpr (!I32OUT)       // the integer path has no scales (scales == nullptr)
+            r.s = *reinterpret_cast<const uint16_t*>(cs + s_off);
+        else
+            r.s = 0;
     };
     // ---- compute roles
     const int wm = wave / WAVES_N;

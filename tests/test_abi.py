@@ -74,6 +74,10 @@ def test_quantize_validation(lib):
     assert f(A, 4, 128, 128, 64, 16, 0, A, A, A + 8, None, None) == EALIGN
     # nothing to do: OK without a launch (null pointers are fine then)
     assert f(None, 0, 128, 128, 64, 16, 0, None, None, None, None, None) == OK
+    # size limits: K <= 2^20, rows * K/64 <= 2^28
+    K = 1 << 21
+    assert f(A, 1, K, K, 64, 16, 0, A, A, A, None, None) == ESHAPE
+    assert f(A, (1 << 24) + 1, 1024, 1024, 64, 16, 0, A, A, A, None, None) == ESHAPE
 
 
 def test_pack_validation(lib):
@@ -83,6 +87,8 @@ def test_pack_validation(lib):
     assert f(None, 8, 128, 64, A, None, None) == ENULL
     assert f(A, 8, 128, 64, A + 4, None, None) == EALIGN
     assert f(None, 0, 128, 64, None, None, None) == OK
+    assert f(A, (1 << 24) + 1, 1024, 64, A, None, None) == ESHAPE
+    assert f(A, 1, 1 << 21, 64, A, None, None) == ESHAPE
 
 
 def test_linear_validation(lib):
@@ -106,6 +112,9 @@ def test_linear_validation(lib):
     assert call(bias=A + 2) == EALIGN
     assert call(M=0) == OK
     assert call(N=0) == OK
+    assert call(K=1 << 21) == ESHAPE
+    assert call(M=65535 * 256 + 1, K=64) == ESHAPE          # grid.y limit of 65535 tiles
+    assert call(N=(1 << 24) + 1, ldy=(1 << 24) + 1, K=1024) == ESHAPE
 
 
 def test_debug_entry_validation(lib):
