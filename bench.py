@@ -17,12 +17,19 @@ one): algorithmic ops / its average launch duration, from HIP events recorded
 on the launch stream inside the timed steps, against the fp8 dense MFMA peak.
 cpu_baseline = the CPU oracle on a bounded sample of the same workload (all
 weights, the first --cpu-rows rows of every layer), on this host's cores.
+roofline.traffic = HBM bytes per GEMM launch from the FETCH_SIZE / WRITE_SIZE
+counters of a profiled run, each scaled by what the counter reads for a plain
+device copy of known size (--copy-calibration); read from the committed
+summary under profiles/ and reported only while the GEMM sources still hash
+to the values recorded there (null otherwise).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,6 +39,9 @@ if ROOT not in sys.path:
 
 PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
+                for f in ("w4a4_gemm.hip", "quartz_internal.h")]
 
 
 def log(*a):
@@ -45,10 +55,51 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3, help="workload config index (workloads.py)")
     ap.add_argument("--lzs-group", type=int, default=16)
-    ap.add_argument("--cpu-rows", type=int, default=768,
+    ap.add_argument("--cpu-rows", type=int, default=1536,
                     help="rows per layer in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
+                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
+
+
+def gemm_sources_sha256() -> str:
+    h = hashlib.sha256()
+    for p in GEMM_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload: str, gs: int):
+    """HBM bytes per GEMM launch recorded in the committed counter summary, if
+    it covers this workload and the GEMM sources have not changed since."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    fields = dict(re.findall(r"^- (\w+): `([^`]*)`", text, flags=re.M))
+    try:
+        if (fields.get("gemm_sources_sha256") != gemm_sources_sha256()
+                or fields.get("workload") != workload or int(fields.get("lzs_group", -1)) != gs):
+            return None
+        return float(fields["hbm_bytes_per_gemm_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int):
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
 def layer_bytes(L, gs):
@@ -78,6 +129,9 @@ def main():
         log("bench.py needs a GPU")
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     dev = torch.device("cuda", 0)
     cfg = W.CONFIGS[args.config]
     gs = args.lzs_group
@@ -177,6 +231,8 @@ def main():
             "pack_gbps": round(pbytes[li] / (t_pack[li] * 1e-3) / 1e9, 1),
         })
 
+    traffic = recorded_traffic(cfg.name, gs)
+
     # ---------------- CPU oracle on a bounded sample (rank 0, N = 1 only)
     cpu = None
     if not args.no_cpu_baseline:
@@ -219,7 +275,10 @@ def main():
         },
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_FP8_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes": round(float(gbytes.mean())),
+            "per": f"GEMM launch, mean over the {len(layers)} layers",
         },
         "quantize_roofline": {
             "bound": "hbm", "achieved": round(quant_gbps, 1), "peak": PEAK_HBM_GBPS,
