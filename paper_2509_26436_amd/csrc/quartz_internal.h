@@ -22,8 +22,9 @@ inline int64_t packed_weight_bytes(int64_t N, int64_t K)
     return panels * (K / kGroup) * kChunkBytes;
 }
 
-// Output rows per GEMM workgroup (grid.y = ceil(M / kGemmBlockRows) <= 65535).
+// Output tile per GEMM workgroup (grid.y = ceil(M / kGemmBlockRows) <= 65535).
 constexpr int64_t kGemmBlockRows = 256;
+constexpr int64_t kGemmBlockCols = 128;
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error.  Arguments are validated by the

@@ -5,17 +5,25 @@
 // weights (codes + fp16 scale) from global memory, decodes them in registers
 // to OCP fp8 e4m3 operands -- activations as c * 2^FLAG in [-112, 112],
 // weights as wq in [-7, 7], both exact in e4m3 -- and writes them to LDS
-// (double-buffered: group g+1 is fetched from global memory while group g is
-// multiplied).  Each wave then runs v_mfma_f32_32x32x64_f8f6f4 over the whole
-// group, which yields the exact integer group product P_g (every partial sum
-// is an integer below 2^24), and folds it into fp32 accumulators with the two
-// group scales:
+// (double-buffered: group g+1 is decoded while group g is multiplied).  Each
+// wave then runs v_mfma_f32_32x32x64_f8f6f4 over the whole group, which yields
+// the exact integer group product P_g (every partial sum is an integer below
+// 2^24), and folds it into fp32 accumulators with the two group scales:
 //   acc += P_g * (s_a[m,g] * s_w[n,g]).
 // The 32 x 32 tile of scale products s_a (x) s_w is itself produced by one
 // fp16 MFMA with a single non-zero k (fp16 x fp16 is exact in fp32), so the
 // per-group dequantization costs one FMA per output element.
 // The epilogue adds the bias, applies the optional GELU (tanh form) and
 // stores bf16 (round to nearest even).
+//
+// The vector ALU is the scarce unit (one FMA per output and group, plus the
+// decode), and one wave alone cannot issue it back to back, so the work is
+// split by wave: per SIMD two "math" waves run only the MFMAs and the
+// dequantization FMAs while a third "decode" wave streams the next group in
+// (buffer loads, nibble -> fp8 decode, LDS stores).  Their instruction
+// streams are independent, so the SIMD interleaves them.  All global
+// addressing is scalar: buffer loads whose resource base advances by one
+// group per iteration.
 #include <type_traits>
 
 #include "quartz_internal.h"
@@ -26,7 +34,17 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
 
+// Buffer resource word 3 for raw (untyped, stride 0) loads on gfx9: a load at
+// an offset >= num_records returns zero instead of touching memory.
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             kRsrcWord3);
+}
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float v)
 {
@@ -42,25 +60,27 @@ __device__ __forceinline__ float gelu_tanh(float v)
 }
 
 // ------------------------------------------------------------------ layout
-// Block tile BM x BN = 256 x 128, 8 waves as 4 (M) x 2 (N), wave tile 64 x 64
-// = 2 x 2 MFMA tiles of 32 x 32.  Two waves share each SIMD, so one wave's
-// VALU work (decode, dequantization) overlaps the other's MFMAs.
+// Block tile BM x BN = 256 x 128.  12 waves: waves 0-7 are math waves as
+// 4 (M) x 2 (N), wave tile 64 x 64 = 2 x 2 MFMA tiles of 32 x 32; waves 8-11
+// are decode waves.  Waves are placed on the 4 SIMDs round robin, so each
+// SIMD holds two math waves and one decode wave.
 constexpr int BM = (int)kGemmBlockRows;
-constexpr int BN = 128;
-constexpr int kWaves = 8;
-constexpr int kThreadsPerBlock = 64 * kWaves;
+constexpr int BN = (int)kGemmBlockCols;
+constexpr int kMathWaves = 8;
+constexpr int kDecodeWaves = 4;
+constexpr int kThreadsPerBlock = 64 * (kMathWaves + kDecodeWaves);
+constexpr int kDecodeThreads = 64 * kDecodeWaves;
 constexpr int WAVES_N = 2;
 constexpr int WM = 64;
 constexpr int WN = 64;
 constexpr int TM = WM / 32;
 constexpr int TN = WN / 32;
-constexpr int kDepth = 3;      // groups held in the register prefetch ring
+constexpr int kPanelsPerBlock = BN / kPanel;
 
 // 16-byte chunk c of decoded fp8 row r lives at chunk c ^ f(r) with
 //   f(r) = (r1 ^ r2) | (r2 ^ r3) << 1      (r_i = bit i of r).
-// Fragment reads (16 consecutive rows, one chunk) and decode writes (8 rows,
-// both halves) then touch distinct 16-byte bank groups within every 128-byte
-// and every 256-byte window, whether the LDS serves 8 or 16 lanes per cycle.
+// Fragment reads (16 consecutive rows, one chunk) then touch distinct
+// 16-byte bank groups within every 128-byte and every 256-byte window.
 __device__ __forceinline__ int swz(int r, int c)
 {
     const int f = (((r >> 1) ^ (r >> 2)) & 1) | ((((r >> 2) ^ (r >> 3)) & 1) << 1);
@@ -84,47 +104,52 @@ __device__ __forceinline__ void lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Raw flag bytes of the 32 elements [32 h, 32 h + 32) of one (group, row),
-// whose 64 / GS flag bytes start at `p` (loaded as is: expanding them right
-// after the load would make the prefetch wait for it).
-// (kept in a 16-bit type where 16 bits suffice, so that the zero extension
-// happens when the ring slot is decoded, not right after the load).
+// The 64 / GS flag bytes of one (group, row), loaded as is; expanded to
+// 8 * FLAG per 8-element word (words 0-3 in `lo`, 4-7 in `hi`, one per byte)
+// only when the group is decoded, so the prefetch never waits for them.
 template <int GS>
-using FlagRaw = typename std::conditional<GS == 8, uint32_t, uint16_t>::type;
+using FlagRaw = typename std::conditional<GS == 8, uint2,
+                typename std::conditional<GS == 16, uint32_t, uint16_t>::type>::type;
 
 template <int GS>
-__device__ __forceinline__ FlagRaw<GS> load_flags_raw(const uint8_t* __restrict__ p)
+__device__ __forceinline__ FlagRaw<GS> load_flags_raw(Rsrc r, uint32_t off)
 {
     if constexpr (GS == 8)
-        return *reinterpret_cast<const uint32_t*>(p);
+        return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
     else if constexpr (GS == 16)
-        return *reinterpret_cast<const uint16_t*>(p);
+        return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+    else if constexpr (GS == 32)
+        return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
     else
-        return *p;
+        return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
 }
 
-// Raw flags -> 8 * FLAG of each 8-element word i (0..3) of the half, one per byte.
 template <int GS>
-__device__ __forceinline__ uint32_t expand_flags8(uint32_t raw)
+__device__ __forceinline__ uint2 expand_flags8(FlagRaw<GS> raw)
 {
-    uint32_t f;
-    if constexpr (GS == 8)
+    uint2 f;
+    if constexpr (GS == 8) {
         f = raw;
-    else if constexpr (GS == 16)
-        f = __builtin_amdgcn_perm(0u, raw, 0x01010000u);
-    else
-        f = __builtin_amdgcn_perm(0u, raw, 0x00000000u);
-    return f << 3;    // FLAG <= 4, so 8 * FLAG stays inside its byte
+    } else if constexpr (GS == 16) {
+        f.x = __builtin_amdgcn_perm(0u, raw, 0x01010000u);
+        f.y = __builtin_amdgcn_perm(0u, raw, 0x03030202u);
+    } else if constexpr (GS == 32) {
+        f.x = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x00000000u);
+        f.y = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x01010101u);
+    } else {
+        f.x = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x00000000u);
+        f.y = f.x;
+    }
+    f.x <<= 3;      // FLAG <= 4, so 8 * FLAG stays inside its byte
+    f.y <<= 3;
+    return f;
 }
 
-// Staging roles: thread t decodes A row t/2, half t%2 (16 code bytes) and
-// B column t/4, quarter t%4 (8 code bytes); threads < BM carry s_a of row t
-// and BM <= t < BM + BN s_w of column t - BM.  Every thread issues the same
-// four loads per group (the rest load a scale they do not use), so the
-// compiler can count them and wait only for the group being decoded.  Rows
-// past M and columns past the padded N read a clamped, valid row / column:
-// they only feed outputs that are never stored, so the main loop needs no
-// bounds checks.
+// Decode roles (decode thread d = tid - 512, 0..255): A row d (32 code bytes,
+// the row's 64 / G_s flags, s_a) and B column d/2, half d%2 (16 code bytes);
+// threads d < 128 also carry s_w of column d.  Rows past M and columns past
+// the packed panels fall outside the buffer ranges and read as zero: they
+// only feed outputs that are never stored, so nothing needs a bounds check.
 template <int GS, bool I32OUT>
 __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
@@ -139,71 +164,103 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     __shared__ uint16_t sas[2][BM + 8];
     __shared__ uint16_t sws[2][BN + 8];
 
+    constexpr int FB = 64 / GS;                           // flag bytes per (group, row)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int64_t m0 = (int64_t)blockIdx.y * BM;
     const int64_t n0 = (int64_t)blockIdx.x * BN;
     const int G = (int)(K / 64);
-    const int64_t padded_n = (N + kPanel - 1) / kPanel * kPanel;
-
-    static_assert(2 * BM == kThreadsPerBlock && 4 * BN == kThreadsPerBlock, "staging roles");
-    const int sr = tid >> 1;          // A row
-    const int sh = tid & 1;           // A half
-    const int bc = tid >> 2;          // B column
-    const int bq = tid & 3;           // B quarter
-    // Global addresses = a wave-uniform base for group g and this block
-    // (scalar registers) plus a small 32-bit per-lane offset.  Activations
-    // are K-group-major: group g of row m at (g * M + m).
-    const int64_t am = min(m0 + sr, M - 1);
-    const uint32_t a_code_off = (uint32_t)((am - m0) * 32 + sh * 16);
-    constexpr int kFlagHalf = GS == 64 ? 0 : 32 / GS;   // flag bytes of the first half
-    const uint32_t a_flag_off = (uint32_t)((am - m0) * (64 / GS) + sh * kFlagHalf);
-    // the block's columns n0 .. n0 + BN - 1 span two 64-column panels
-    const int64_t panel0 = n0 / kPanel;
-    const int64_t bn = min(n0 + bc, padded_n - 1);
-    const uint32_t b_code_off = (uint32_t)((bn / kPanel - panel0) * G * kChunkBytes +
-                                           (bn % kPanel) * 32 + bq * 8);
-    // scales: waves 0-3 carry s_a of row tid (K-group-major, stride M per
-    // group), waves 4-5 s_w of column tid - BM (inside the packed chunk,
-    // stride kChunkBytes per group); waves 6-7 load an s_a they do not use
     const int uwave = __builtin_amdgcn_readfirstlane(wave);
-    const bool sa_role = uwave < 4;
-    const bool sw_role = uwave == 4 || uwave == 5;
-    const int64_t sam = min(m0 + (tid & (BM - 1)), M - 1);
-    const int64_t swn = min(n0 + (tid & (BN - 1)), padded_n - 1);
-    const uint32_t s_off = sw_role ? (uint32_t)((swn / kPanel - panel0) * G * kChunkBytes +
-                                                kChunkCodeBytes + (swn % kPanel) * 2)
-                                   : (uint32_t)((sam - m0) * 2);
-    const uint8_t* a_blk = codes + m0 * 32;
-    const uint8_t* f_blk = flags + m0 * (64 / GS);
-    const uint8_t* b_blk = w_packed + panel0 * G * kChunkBytes;
-    const uint8_t* s_base =
-        sw_role || I32OUT ? b_blk : reinterpret_cast<const uint8_t*>(scales + m0);
-    const int64_t s_stride = sw_role ? (int64_t)kChunkBytes : M * 2;
+    const bool decoder = uwave >= kMathWaves;
+
+    // ------------------------------------------------------ decode waves
+    static_assert(kDecodeThreads == BM && kDecodeThreads == 2 * BN, "decode roles");
+    const int d = tid - kMathWaves * 64;          // decode thread index (math waves: < 0)
+    const int dr = d & (BM - 1);                  // A row
+    const int bc = (d >> 1) & (BN - 1);           // B column
+    const int bh = d & 1;                         // B half
+    const int swc = d & (BN - 1);                 // column whose s_w this thread loads
+    const int64_t panels = (N + kPanel - 1) / kPanel;
+    const int64_t panel0 = n0 / kPanel;
+    const int64_t rows = min(M - m0, (int64_t)BM);
+    const uint32_t a_bytes = (uint32_t)(rows * 32);
+    const uint32_t f_bytes = (uint32_t)(rows * FB);
+    const uint32_t s_bytes = (uint32_t)(rows * 2);
+    const int64_t blk_panels = min(panels - panel0, (int64_t)kPanelsPerBlock);
+    const uint32_t b_bytes = (uint32_t)((blk_panels - 1) * G * kChunkBytes + kChunkBytes);
+    const uint32_t a_off = (uint32_t)(dr * 32);
+    const uint32_t f_off = (uint32_t)(dr * FB);
+    const uint32_t b_off = (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * 16);
+    const uint32_t sw_off =
+        (uint32_t)((swc / kPanel) * G * kChunkBytes + kChunkCodeBytes + (swc % kPanel) * 2);
 
     struct Raw {
-        uint4 a;
-        uint2 b;
+        uint4 a0, a1;
+        uint4 b;
         FlagRaw<GS> f;
-        uint16_t s;
+        uint16_t sa, sw;
     };
     auto fetch = [&](Raw& r, int g) {
-        const uint8_t* ca = a_blk + (int64_t)g * (M * 32);
-        const uint8_t* cf = f_blk + (int64_t)g * (M * (64 / GS));
-        const uint8_t* cb = b_blk + (int64_t)g * kChunkBytes;
-        const uint8_t* cs = s_base + (int64_t)g * s_stride;
-        r.a = *reinterpret_cast<const uint4*>(ca + a_code_off);
-        r.f = load_flags_raw<GS>(cf + a_flag_off);
-        r.b = *reinterpret_cast<const uint2*>(cb + b_code_off);
-        if constexpr (!I32OUT)       // the integer path has no scales (scales == nullptr)
-            r.s = *reinterpret_cast<const uint16_t*>(cs + s_off);
-        else
-            r.s = 0;
+        const Rsrc ra = make_rsrc(codes + ((int64_t)g * M + m0) * 32, a_bytes);
+        const Rsrc rf = make_rsrc(flags + ((int64_t)g * M + m0) * FB, f_bytes);
+        const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
+        r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off, 0, 0));
+        r.a1 = __builtin_bit_cast(uint4,
+                                  __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
+        r.f = load_flags_raw<GS>(rf, f_off);
+        r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+        if constexpr (!I32OUT) {       // the integer path has no scales (scales == nullptr)
+            const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
+            r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
+            r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
+        } else {
+            r.sa = 0;
+            r.sw = 0;
+        }
     };
-    // ---- compute roles
-    const int wm = wave / WAVES_N;
-    const int wn = wave % WAVES_N;
+    // decode one group into LDS buffer `buf`
+    auto stage = [&](const Raw& r, int buf) {
+        const uint2 fl8 = expand_flags8<GS>(r.f);
+        const uint32_t a[8] = {r.a0.x, r.a0.y, r.a0.z, r.a0.w, r.a1.x, r.a1.y, r.a1.z, r.a1.w};
+        constexpr int kWordsPerFlag = GS / 8;
+        Fp8Table t = fp8_table<0>(fl8.x);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            uint2 w[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int wi = 2 * c + h;           // word index 0..7
+                if (wi % kWordsPerFlag == 0 && wi > 0) {
+                    const uint32_t f = wi < 4 ? fl8.x : fl8.y;
+                    switch (wi & 3) {
+                    case 0: t = fp8_table<0>(f); break;
+                    case 1: t = fp8_table<1>(f); break;
+                    case 2: t = fp8_table<2>(f); break;
+                    default: t = fp8_table<3>(f); break;
+                    }
+                }
+                w[h] = decode_nibbles_fp8(a[wi], t);
+            }
+            *reinterpret_cast<uint4*>(As[buf] + swz(dr, c)) = make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
+        }
+        const Fp8Table tw{kTabLo, kTabHi};
+        const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
+        const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
+        const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
+        const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
+        *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
+        *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
+        if constexpr (!I32OUT) {
+            sas[buf][dr] = r.sa;
+            if (d < BN)
+                sws[buf][swc] = r.sw;
+        }
+    };
+
+    // -------------------------------------------------------- math waves
+    const int wm = (wave & (kMathWaves - 1)) / WAVES_N;
+    const int wn = (wave & (kMathWaves - 1)) % WAVES_N;
     const int l32 = lane & 31;
     const int khalf = lane >> 5;
     int sa_idx[TM], sw_idx[TN];
@@ -223,166 +280,95 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             for (int r = 0; r < 16; ++r)
                 acc[i][j][r] = 0.0f;
 
-    // Decode of the next group, cut into four slices so that each slice's VALU
-    // work is issued while the matrix unit runs one tile's MFMAs.
-    // Decode of the next group in eight pieces, two per MFMA tile: piece 2t
-    // goes between tile t's fp8 MFMA and its scale MFMA, piece 2t+1 right
-    // before its FMAs.  Tiles 0 and 1 decode the two words pairs of the
-    // activation row half, tile 2 the weight column quarter, tile 3 stores
-    // the scales.
-    uint32_t fl8 = 0;      // 8 * FLAG per activation word of this half
-    Fp8Table t_lo, t_hi;   // tables of the two words being decoded
-    uint2 d_first;         // first word of a pair, decoded
-    auto stage_piece = [&](const Raw& r, int buf, int piece) {
-        switch (piece) {
-        case 0:
-            fl8 = expand_flags8<GS>((uint32_t)r.f);
-            t_lo = fp8_table<0>(fl8);
-            t_hi = GS == 8 ? fp8_table<1>(fl8) : t_lo;
-            d_first = decode_nibbles_fp8(r.a.x, t_lo);
-            break;
-        case 1: {
-            const uint2 d = decode_nibbles_fp8(r.a.y, t_hi);
-            *reinterpret_cast<uint4*>(As[buf] + swz(sr, 2 * sh)) =
-                make_uint4(d_first.x, d_first.y, d.x, d.y);
-            break;
-        }
-        case 2:
-            t_lo = GS <= 16 ? fp8_table<2>(fl8) : t_lo;
-            t_hi = GS == 8 ? fp8_table<3>(fl8) : t_lo;
-            d_first = decode_nibbles_fp8(r.a.z, t_lo);
-            break;
-        case 3: {
-            const uint2 d = decode_nibbles_fp8(r.a.w, t_hi);
-            *reinterpret_cast<uint4*>(As[buf] + swz(sr, 2 * sh + 1)) =
-                make_uint4(d_first.x, d_first.y, d.x, d.y);
-            break;
-        }
-        case 4:
-            d_first = decode_nibbles_fp8(r.b.x, Fp8Table{kTabLo, kTabHi});
-            break;
-        case 5: {
-            const uint2 d = decode_nibbles_fp8(r.b.y, Fp8Table{kTabLo, kTabHi});
-            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, bq)) =
-                make_uint4(d_first.x, d_first.y, d.x, d.y);
-            break;
-        }
-        case 6:
-            if (sa_role)
-                sas[buf][tid] = r.s;
-            else if (sw_role)
-                sws[buf][tid - BM] = r.s;
-            break;
-        default:
-            break;
-        }
-    };
-    auto stage = [&](const Raw& r, int buf) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-            stage_piece(r, buf, q);
-    };
-
-    // One group: per tile, the MFMAs, then a decode slice of the next group
-    // (VALU work that runs while the matrix unit computes), then the tile's
-    // FMAs.  Scheduling barriers keep this order; the asm statement pins each
-    // tile's FMAs (without a use, LLVM sinks them to the end of the loop and
-    // keeps every tile's results live).
-    auto compute = [&](int buf, const Raw& next, bool more, int next_buf) {
-        v8i bf[TN];
-        v8h sw_op[TN];
+    // One group: per tile the fp8 MFMA, the scale MFMA and the FMAs; the two
+    // math waves of a SIMD interleave, so one's FMAs run under the other's
+    // MFMAs.  The asm statement pins each tile's FMAs (without a use, LLVM
+    // sinks them to the end of the loop and keeps every tile's results live).
+    auto compute = [&](int buf) {
+        v8i bf[TN], af[TM];
+        _Float16 sw_h[TN], sa_h[TM];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             bf[j] = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
-            sw_op[j] = v8h{};
             if constexpr (!I32OUT)
-                sw_op[j][0] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
+                sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
         }
-        constexpr int T = TM * TN;
-        static_assert(T == 4, "four decode slices per group");
-        const v16f zero = {};
-        v8i af[TM];
-        v8h sa_op[TM];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
-            // fp16 operand of the scale outer product: only k = 0 is non-zero
-            sa_op[i] = v8h{};
             if constexpr (!I32OUT)
-                sa_op[i][0] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
+                sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
         }
-        auto tile = [&](int i, int j, bool interleave) {
-            // in-order issue: VALU work between the two MFMAs keeps the wave
-            // busy while the matrix unit finishes the first one
+        const v16f zero = {};
+#pragma unroll
+        for (int t = 0; t < TM * TN; ++t) {
+            const int i = t / TN, j = t % TN;
             const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                 af[i], bf[j], zero, 0, 0, 0, 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (interleave && more)
-                stage_piece(next, next_buf, 2 * (i * TN + j));
-            __builtin_amdgcn_sched_barrier(0);
-            v16f sc;
-            if constexpr (!I32OUT)
-                sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op[i], sw_op[j], zero, 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (interleave && more)
-                stage_piece(next, next_buf, 2 * (i * TN + j) + 1);
-            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (I32OUT) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                if constexpr (I32OUT)
+                for (int r = 0; r < 16; ++r)
                     acc[i][j][r] += p[r];
-                else
+            } else {
+                // fp16 operands of the scale outer product: only k = 0 is non-zero
+                v8h sa_op = {}, sw_op = {};
+                sa_op[0] = sa_h[i];
+                sw_op[0] = sw_h[j];
+                const v16f sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
                     acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
             }
             asm volatile("" : "+v"(acc[i][j]));
-            __builtin_amdgcn_sched_barrier(0);
-        };
-#pragma unroll
-        for (int t = 0; t < T; ++t)
-            tile(t / TN, t % TN, true);
+        }
     };
 
-    // ---- pipeline: register ring of kDepth groups, fp8 LDS double buffer
-    if (tid < 8) {
-        sas[tid & 1][BM + (tid >> 1)] = 0;
-        sws[tid & 1][BN + (tid >> 1)] = 0;
-    }
-    Raw ring[kDepth];
-#pragma unroll
-    for (int u = 0; u < kDepth; ++u)
-        fetch(ring[u], min(u, G - 1));
-    stage(ring[0], 0);
-    lds_sync();
-
-    // Main loop over chunks of 2 * kDepth groups (ring slot and LDS buffer are
-    // then compile-time constants in every unrolled copy): straight-line code
-    // with the same loads on every path (prefetch indices past the end are
-    // clamped to the last group: a harmless reload), so the compiler waits
-    // only for the ring slot being decoded, not for the loads just issued.
-    constexpr int kUnroll = 2 * kDepth;
-    {
-        int g0 = 0;
-        for (; g0 + kUnroll <= G; g0 += kUnroll) {
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int g = g0 + u;
-                // ring slot u % kDepth held group g (staged one iteration ago): refill it
-                fetch(ring[u % kDepth], min(g + kDepth, G - 1));
-                compute(u & 1, ring[(u + 1) % kDepth], true, (u + 1) & 1);
-                lds_sync();
-            }
+    // ---- pipeline: decode waves keep a register ring of two groups in flight
+    // and write the fp8 LDS double buffer one group ahead of the math waves.
+    // The two roles run separate loops with the same barriers (one before
+    // the first group and one after each), so their registers never overlap
+    // in liveness.
+    if (decoder) {
+        Raw ring[2];
+        if (d < 8) {
+            sas[d & 1][BM + (d >> 1)] = 0;
+            sws[d & 1][BN + (d >> 1)] = 0;
         }
-        // Tail: the last G % kUnroll groups (their prefetches are issued above
-        // or inside this loop in the same ring order).
-#pragma unroll
-        for (int u = 0; u < kUnroll - 1; ++u) {
-            const int g = g0 + u;
-            if (g < G) {
-                if (g + kDepth < G)
-                    fetch(ring[u % kDepth], g + kDepth);
-                compute(u & 1, ring[(u + 1) % kDepth], g + 1 < G, (u + 1) & 1);
-                lds_sync();
-            }
+        fetch(ring[0], 0);
+        fetch(ring[1], min(1, G - 1));
+        stage(ring[0], 0);
+        fetch(ring[0], min(2, G - 1));
+        lds_sync();
+        // Iteration g: decode group g + 1 (ring slot (g + 1) & 1) into buffer
+        // (g + 1) & 1 and refill that slot with group g + 3.  Straight-line
+        // code with clamped prefetch indices (a harmless reload at the end),
+        // so the compiler waits only for the slot being decoded.
+        auto dstep = [&](int u, int g) {
+            stage(ring[(u + 1) & 1], (u + 1) & 1);
+            fetch(ring[(u + 1) & 1], min(g + 3, G - 1));
+            lds_sync();
+        };
+        int g = 0;
+        for (; g + 2 <= G; g += 2) {
+            dstep(0, g);
+            dstep(1, g + 1);
+        }
+        if (g < G)
+            dstep(0, g);
+        return;
+    }
+    lds_sync();
+    {
+        int g = 0;
+        for (; g + 2 <= G; g += 2) {
+            compute(0);
+            lds_sync();
+            compute(1);
+            lds_sync();
+        }
+        if (g < G) {
+            compute(0);
+            lds_sync();
         }
     }
 
