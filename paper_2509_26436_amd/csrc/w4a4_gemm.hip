@@ -76,6 +76,7 @@ constexpr int WN = 64;
 constexpr int TM = WM / 32;
 constexpr int TN = WN / 32;
 constexpr int kPanelsPerBlock = BN / kPanel;
+constexpr int kStages = 3;
 
 // 16-byte chunk c of decoded fp8 row r lives at chunk c ^ f(r) with
 //   f(r) = (r1 ^ r2) | (r2 ^ r3) << 1      (r_i = bit i of r).
@@ -157,12 +158,15 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t As[2][BM * 64];
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][BN * 64];
+    // three LDS stages: group g + 2 is decoded into one while the math waves
+    // read the operands of group g + 1 from another (and multiply group g
+    // from registers)
+    __shared__ __attribute__((aligned(16))) uint8_t As[kStages][BM * 64];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[kStages][BN * 64];
     // group scales as fp16 bits; entries BM (BN) stay 0: the upper half-wave's
     // k = 8 operand slot of the outer-product MFMA reads them
-    __shared__ uint16_t sas[2][BM + 8];
-    __shared__ uint16_t sws[2][BN + 8];
+    __shared__ uint16_t sas[kStages][BM + 8];
+    __shared__ uint16_t sws[kStages][BN + 8];
 
     constexpr int FB = 64 / GS;                           // flag bytes per (group, row)
     const int tid = threadIdx.x;
@@ -280,95 +284,133 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             for (int r = 0; r < 16; ++r)
                 acc[i][j][r] = 0.0f;
 
-    // One group: per tile the fp8 MFMA, the scale MFMA and the FMAs; the two
-    // math waves of a SIMD interleave, so one's FMAs run under the other's
-    // MFMAs.  The asm statement pins each tile's FMAs (without a use, LLVM
-    // sinks them to the end of the loop and keeps every tile's results live).
-    auto compute = [&](int buf) {
-        v8i bf[TN], af[TM];
-        _Float16 sw_h[TN], sa_h[TM];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            bf[j] = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
-            if constexpr (!I32OUT)
-                sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
-            if constexpr (!I32OUT)
-                sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
-        }
+    // Operands of the group being multiplied, held in registers; each one is
+    // refilled with the next group's (from LDS stage nb) right after its last
+    // use, so the LDS reads overlap the MFMAs instead of stalling the next
+    // group's first MFMA.
+    v8i bf[TN], af[TM];
+    _Float16 sw_h[TN], sa_h[TM];
+    auto load_a = [&](int i, int buf) {
+        af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
+        if constexpr (!I32OUT)
+            sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
+    };
+    auto load_b = [&](int j, int buf) {
+        bf[j] = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
+        if constexpr (!I32OUT)
+            sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
+    };
+
+    // One group: per tile (order (0,0) (0,1) (1,0) (1,1)) the fp8 MFMA, the
+    // scale MFMA, the prefetch of operands whose last use this was, and the
+    // FMAs; the two math waves of a SIMD interleave, so one's FMAs run under
+    // the other's MFMAs.  The asm statement pins each tile's FMAs (without a
+    // use, LLVM sinks them to the end of the loop and keeps every tile's
+    // results live).
+    static_assert(TM == 2 && TN == 2, "prefetch order assumes 2 x 2 tiles");
+    auto compute = [&](int nb) {
         const v16f zero = {};
 #pragma unroll
         for (int t = 0; t < TM * TN; ++t) {
             const int i = t / TN, j = t % TN;
             const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                 af[i], bf[j], zero, 0, 0, 0, 0, 0, 0);
-            if constexpr (I32OUT) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    acc[i][j][r] += p[r];
-            } else {
+            v16f sc;
+            if constexpr (!I32OUT) {
                 // fp16 operands of the scale outer product: only k = 0 is non-zero
                 v8h sa_op = {}, sw_op = {};
                 sa_op[0] = sa_h[i];
                 sw_op[0] = sw_h[j];
-                const v16f sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+                sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (t == 1)
+                load_a(0, nb);
+            if (t == 2)
+                load_b(0, nb);
+            if (t == 3) {
+                load_a(1, nb);
+                load_b(1, nb);
+            }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
+            for (int r = 0; r < 16; ++r) {
+                if constexpr (I32OUT)
+                    acc[i][j][r] += p[r];
+                else
                     acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
             }
             asm volatile("" : "+v"(acc[i][j]));
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
+    // The math waves' barrier: their own outstanding LDS reads (the prefetch)
+    // may cross it, since the stage they read is not rewritten until two
+    // barriers later; the memory clobber keeps the compiler from moving LDS
+    // accesses across it.
+    auto math_barrier = [] { asm volatile("s_barrier" ::: "memory"); };
 
     // ---- pipeline: decode waves keep a register ring of two groups in flight
-    // and write the fp8 LDS double buffer one group ahead of the math waves.
-    // The two roles run separate loops with the same barriers (one before
-    // the first group and one after each), so their registers never overlap
-    // in liveness.
+    // and decode two groups ahead of the math waves.  The two roles run
+    // separate loops with the same barriers (one before the first group and
+    // one after each), so their registers never overlap in liveness.
     if (decoder) {
         Raw ring[2];
-        if (d < 8) {
-            sas[d & 1][BM + (d >> 1)] = 0;
-            sws[d & 1][BN + (d >> 1)] = 0;
+        if (d < 8 * kStages) {
+            sas[d >> 3][BM + (d & 7)] = 0;
+            sws[d >> 3][BN + (d & 7)] = 0;
         }
         fetch(ring[0], 0);
         fetch(ring[1], min(1, G - 1));
         stage(ring[0], 0);
         fetch(ring[0], min(2, G - 1));
+        stage(ring[1], 1);
+        fetch(ring[1], min(3, G - 1));
         lds_sync();
-        // Iteration g: decode group g + 1 (ring slot (g + 1) & 1) into buffer
-        // (g + 1) & 1 and refill that slot with group g + 3.  Straight-line
-        // code with clamped prefetch indices (a harmless reload at the end),
+        // Iteration g: decode group g + 2 (ring slot g % 2) into stage
+        // (g + 2) % 3 and refill the slot with group g + 4.  Straight-line
+        // code with clamped prefetch indices (harmless reloads at the end),
         // so the compiler waits only for the slot being decoded.
         auto dstep = [&](int u, int g) {
-            stage(ring[(u + 1) & 1], (u + 1) & 1);
-            fetch(ring[(u + 1) & 1], min(g + 3, G - 1));
+            stage(ring[u & 1], (u + 2) % kStages);
+            fetch(ring[u & 1], min(g + 4, G - 1));
             lds_sync();
         };
+        constexpr int kU = 2 * kStages;
         int g = 0;
-        for (; g + 2 <= G; g += 2) {
-            dstep(0, g);
-            dstep(1, g + 1);
+        for (; g + kU <= G; g += kU) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+                dstep(u, g + u);
         }
-        if (g < G)
-            dstep(0, g);
+#pragma unroll
+        for (int u = 0; u < kU - 1; ++u)
+            if (g + u < G)
+                dstep(u, g + u);
         return;
     }
     lds_sync();
+    load_a(0, 0);
+    load_a(1, 0);
+    load_b(0, 0);
+    load_b(1, 0);
     {
+        // iteration g multiplies group g and prefetches group g + 1 from
+        // stage (g + 1) % 3 (at the last group: a harmless read of a stale stage)
         int g = 0;
-        for (; g + 2 <= G; g += 2) {
-            compute(0);
-            lds_sync();
-            compute(1);
-            lds_sync();
+        for (; g + kStages <= G; g += kStages) {
+#pragma unroll
+            for (int u = 0; u < kStages; ++u) {
+                compute((u + 1) % kStages);
+                math_barrier();
+            }
         }
-        if (g < G) {
-            compute(0);
-            lds_sync();
+#pragma unroll
+        for (int u = 0; u < kStages - 1; ++u) {
+            if (g + u < G) {
+                compute((u + 1) % kStages);
+                math_barrier();
+            }
         }
     }
 
