@@ -60,7 +60,7 @@ enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
  * Activation quantizer: Stage 1 (Eq. 1) and Stage 2 (Eq. 2 + right shift) in
  * one pass over x.
  *
- *   x_bf16  bf16 [M][ldx], row-major, ldx >= K.
+ *   x_bf16  bf16 [M][ldx], row-major, K <= ldx <= 2^24, ldx % 8 == 0.
  *   M, K    rows (tokens) and reduction size; K % 64 == 0.
  *   mode    QUARTZ_MODE_SYMMETRIC (s = max|x| / 127 per 64-group, zero point 0).
  * Outputs, K-group-major (all rows of 64-group 0, then all rows of group 1, ...),

@@ -9,6 +9,8 @@ constexpr int64_t kMaxK = int64_t(1) << 20;       // at most 16384 groups per ro
 // rows x groups of one call (M x K/64 or N x K/64): 2^34 elements, 32 GiB of
 // bf16 input; keeps every grid below 2^32 threads
 constexpr int64_t kMaxRowGroups = int64_t(1) << 28;
+// leading dimension of the activations (elements): 8 rows of it stay below 2^32 bytes
+constexpr int64_t kMaxLd = int64_t(1) << 24;
 
 // sizes that every entry point accepts: rows >= 0, 0 <= K <= kMaxK, K % 64 == 0
 // and rows * K / 64 <= kMaxRowGroups
@@ -64,7 +66,7 @@ quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int6
 {
     if (group_size != 64 || !lzs_ok(lzs_group) || mode != QUARTZ_MODE_SYMMETRIC)
         return QUARTZ_ERR_UNSUPPORTED;
-    if (!size_ok(M, K) || ldx < K)
+    if (!size_ok(M, K) || ldx < K || ldx > kMaxLd)
         return QUARTZ_ERR_SHAPE;
     if (ldx % 8 != 0)
         return QUARTZ_ERR_ALIGN;       // 16-byte aligned rows for the vector loads
