@@ -356,6 +356,9 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // one after each), so their registers never overlap in liveness.
     if (decoder) {
         Raw ring[2];
+        // the decode of each group is on the critical path of the next ones:
+        // give these waves issue priority over the math waves
+        __builtin_amdgcn_s_setprio(2);
         if (d < 8 * kStages) {
             sas[d >> 3][BM + (d & 7)] = 0;
             sws[d >> 3][BN + (d & 7)] = 0;
