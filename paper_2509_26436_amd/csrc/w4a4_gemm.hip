@@ -288,7 +288,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // refilled with the next group's (from LDS stage nb) right after its last
     // use, so the LDS reads overlap the MFMAs instead of stalling the next
     // group's first MFMA.
-    v8i bf[TN], af[TM];
+    // a single weight-fragment register set: column 0 (prefetched) for tiles
+    // (0,0) (1,0), then column 1, read from the current stage once column 0's
+    // last product is issued
+    v8i bf, af[TM];
     _Float16 sw_h[TN], sa_h[TM];
     auto load_a = [&](int i, int buf) {
         af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
@@ -296,51 +299,84 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
     };
     auto load_b = [&](int j, int buf) {
-        bf[j] = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
+        bf = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
         if constexpr (!I32OUT)
             sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
     };
 
-    // One group: per tile (order (0,0) (0,1) (1,0) (1,1)) the fp8 MFMA, the
-    // scale MFMA, the prefetch of operands whose last use this was, and the
-    // FMAs; the two math waves of a SIMD interleave, so one's FMAs run under
-    // the other's MFMAs.  The asm statement pins each tile's FMAs (without a
-    // use, LLVM sinks them to the end of the loop and keeps every tile's
-    // results live).
+    // One group, tiles in the order (0,0) (1,0) (0,1) (1,1).  The fp8 product
+    // of each tile is issued one step ahead: step t issues the scale MFMA of
+    // tile t, the fp8 MFMA of tile t + 1 and then the FMAs of tile t, which
+    // therefore wait only for the short scale MFMA while the matrix unit
+    // works on the next product.  The first product of a group is issued
+    // right after the barrier, and the last tile's FMAs follow it (its
+    // results stay live across the barrier).  Operands are prefetched for
+    // the next group after their last use.  The asm statement pins each
+    // tile's FMAs (without a use, LLVM sinks them to the end of the loop).
     static_assert(TM == 2 && TN == 2, "prefetch order assumes 2 x 2 tiles");
-    auto compute = [&](int nb) {
-        const v16f zero = {};
+    v16f p_next, p_last, s_last;       // product of the next tile; last tile's P and S
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        p_last[r] = 0.0f;              // the "last tile" before the first group adds 0
+        s_last[r] = 0.0f;
+    }
+    const v16f zero = {};
+    auto fma_tile = [&](int i, int j, const v16f& p, const v16f& sc) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            if constexpr (I32OUT)
+                acc[i][j][r] += p[r];
+            else
+                acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
+        }
+        asm volatile("" : "+v"(acc[i][j]));
+    };
+    auto scale_tile = [&](int i, int j) {
+        v16f sc = zero;
+        if constexpr (!I32OUT) {
+            // fp16 operands of the scale outer product: only k = 0 is non-zero
+            v8h sa_op = {}, sw_op = {};
+            sa_op[0] = sa_h[i];
+            sw_op[0] = sw_h[j];
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+        }
+        return sc;
+    };
+    auto compute = [&](int cb, int nb) {
+        // product of tile 0, then the last tile of the previous group
+        p_next = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[0], bf, zero, 0, 0, 0, 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        fma_tile(TM - 1, TN - 1, p_last, s_last);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int t = 0; t < TM * TN; ++t) {
-            const int i = t / TN, j = t % TN;
-            const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                af[i], bf[j], zero, 0, 0, 0, 0, 0, 0);
-            v16f sc;
-            if constexpr (!I32OUT) {
-                // fp16 operands of the scale outer product: only k = 0 is non-zero
-                v8h sa_op = {}, sw_op = {};
-                sa_op[0] = sa_h[i];
-                sw_op[0] = sw_h[j];
-                sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+            const int i = t % TM, j = t / TM;
+            const v16f p = p_next;
+            const v16f sc = scale_tile(i, j);
+            if (t + 1 < TM * TN) {
+                const int i1 = (t + 1) % TM;
+                p_next = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i1], bf, zero, 0, 0,
+                                                                          0, 0, 0, 0);
             }
             __builtin_amdgcn_sched_barrier(0);
-            if (t == 1)
+            // refills after the last use of each operand: af[i] by the product of
+            // tile (i,1) (issued one step ahead), sa_h[i] by the scale of tile
+            // (i,1), bf / sw_h[0] by column 0's products and scales
+            if (t == 0)
+                load_b(1, cb);          // column 1 of this group (column 0's products are issued)
+            if (t == 2) {
                 load_a(0, nb);
-            if (t == 2)
-                load_b(0, nb);
-            if (t == 3) {
+                load_b(0, nb);          // column 0 of the next group
+            }
+            if (t == 3)
                 load_a(1, nb);
-                load_b(1, nb);
-            }
             __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                if constexpr (I32OUT)
-                    acc[i][j][r] += p[r];
-                else
-                    acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
+            if (t + 1 < TM * TN) {
+                fma_tile(i, j, p, sc);
+            } else {
+                p_last = p;
+                s_last = sc;
             }
-            asm volatile("" : "+v"(acc[i][j]));
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -396,7 +432,6 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     load_a(0, 0);
     load_a(1, 0);
     load_b(0, 0);
-    load_b(1, 0);
     {
         // iteration g multiplies group g and prefetches group g + 1 from
         // stage (g + 1) % 3 (at the last group: a harmless read of a stale stage)
@@ -404,18 +439,20 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         for (; g + kStages <= G; g += kStages) {
 #pragma unroll
             for (int u = 0; u < kStages; ++u) {
-                compute((u + 1) % kStages);
+                compute(u % kStages, (u + 1) % kStages);
                 math_barrier();
             }
         }
 #pragma unroll
         for (int u = 0; u < kStages - 1; ++u) {
             if (g + u < G) {
-                compute((u + 1) % kStages);
+                compute(u % kStages, (u + 1) % kStages);
                 math_barrier();
             }
         }
     }
+
+    fma_tile(TM - 1, TN - 1, p_last, s_last);
 
     // ---- epilogue: lane holds column l32 of each 32 x 32 tile, rows 8 (r/4) + 4 khalf + r%4
 #pragma unroll
