@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=1536,
                     help="rows per layer in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-batched-mlp", action="store_true",
+                    help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -108,6 +110,58 @@ def layer_bytes(L, gs):
     gemm = (L.M * L.K * (0.5 + 1.0 / gs + 2.0 / 64) + L.N * L.K * (0.5 + 2.0 / 64)
             + 2 * L.N + 2 * L.M * L.N)
     return quant, pack, gemm
+
+
+def batched_mlp(q, W, torch, np, gs, reps=5):
+    """The batched FLUX MLP at M = 18432 (4 images x 4608 tokens) as one pipeline:
+    quantize x -> fc1 3072->12288 with the GELU epilogue -> quantize -> fc2
+    12288->3072.  Per layer: mean quantize and GEMM time over `reps` passes
+    (HIP events on the launch stream), and the end-to-end time against the
+    sum of the two roofline times (quantize bytes at 8 TB/s + GEMM ops at the
+    fp8 dense peak)."""
+    dev = torch.device("cuda", 0)
+    cfg = W.CONFIGS[4]
+    L1, L2 = cfg.layers
+    to = lambda a: torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+    x1 = to(W.make_x(4, 0))
+    w1, b1 = to(W.make_w(4, 0)), to(W.make_bias(4, 0))
+    w2, b2 = to(W.make_w(4, 1)), to(W.make_bias(4, 1))
+    pw1, pw2 = q.pack_weight(w1), q.pack_weight(w2)
+    qa1 = q.quantize_act(x1, lzs_group=gs)
+    y1 = q.w4a4_linear(qa1, pw1, b1, 1)
+    qa2 = q.quantize_act(y1, lzs_group=gs)
+    y2 = q.w4a4_linear(qa2, pw2, b2, 0)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    t = np.zeros(4)
+    for it in range(reps + 2):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        ev[0].record(stream)
+        q.quantize_act(x1, lzs_group=gs, out=qa1)
+        ev[1].record(stream)
+        q.w4a4_linear(qa1, pw1, b1, 1, out=y1)
+        ev[2].record(stream)
+        q.quantize_act(y1, lzs_group=gs, out=qa2)
+        ev[3].record(stream)
+        q.w4a4_linear(qa2, pw2, b2, 0, out=y2)
+        ev[4].record(stream)
+        torch.cuda.synchronize()
+        if it >= 2:
+            t += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(4)])
+    t = t / reps * 1e3        # us
+    out = []
+    for li, L in enumerate((L1, L2)):
+        qb, _, _ = layer_bytes(L, gs)
+        ops = 2.0 * L.M * L.N * L.K
+        tq, tg = t[2 * li], t[2 * li + 1]
+        roof = qb / (PEAK_HBM_GBPS * 1e3) + ops / (PEAK_FP8_TFLOPS * 1e6)      # us
+        out.append({"layer": L.name, "M": L.M, "K": L.K, "N": L.N,
+                    "quantize_us": round(tq, 2), "quantize_gbps": round(qb / (tq * 1e3), 1),
+                    "gemm_us": round(tg, 2), "gemm_tflops": round(ops / (tg * 1e6), 1),
+                    "end_to_end_us": round(tq + tg, 2), "roofline_us": round(roof, 2),
+                    "frac": round(roof / (tq + tg), 4)})
+    return {"workload": cfg.name, "lzs_group": gs,
+            "step": "quantize + fc1 (GELU) + quantize + fc2", "per_layer": out}
 
 
 def main():
@@ -233,6 +287,14 @@ def main():
 
     traffic = recorded_traffic(cfg.name, gs)
 
+    mlp = None
+    if not args.no_batched_mlp:
+        del outs, dev_in
+        torch.cuda.empty_cache()
+        t_m = time.time()
+        mlp = batched_mlp(q, W, torch, np, gs)
+        log(f"batched MLP pipeline measured in {time.time() - t_m:.1f}s")
+
     # ---------------- CPU oracle on a bounded sample (rank 0, N = 1 only)
     cpu = None
     if not args.no_cpu_baseline:
@@ -286,6 +348,7 @@ def main():
         },
         "pack_gbps": round(pack_gbps, 1),
         "per_layer": per_layer,
+        "batched_mlp": mlp,
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
