@@ -463,29 +463,63 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
 
     fma_tile(TM - 1, TN - 1, p_last, s_last);
 
-    // ---- epilogue: lane holds column l32 of each 32 x 32 tile, rows 8 (r/4) + 4 khalf + r%4
+    // ---- epilogue.  Lane l holds column l % 32 of each 32 x 32 tile, rows
+    // 8 (r/4) + 4 khalf + r%4 of register r.
+    if constexpr (I32OUT) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int64_t col = n0 + wn * WN + j * 32 + l32;
-        if (col >= N)
-            continue;
-        float b = 0.0f;
-        if (!I32OUT && bias)
-            b = __uint_as_float((uint32_t)bias[col] << 16);
+        for (int j = 0; j < TN; ++j) {
+            const int64_t col = n0 + wn * WN + j * 32 + l32;
+            if (col >= N)
+                continue;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                    if (row < M)
+                        yi[row * N + col] = (int32_t)acc[i][j][r];
+                }
+            }
+        }
+    } else {
+        // bias and activation per element, then one lane-half swap between the
+        // two column tiles: afterwards lane l holds column l of the wave's 64
+        // columns for one row (tile 0's rows in the first register, tile 1's
+        // khalf = 1 rows in the second), so every store covers a full 128-byte
+        // row segment; the pair is rounded to bf16 (RNE) by one conversion
+        static_assert(TN == 2, "the swap pairs the two column tiles");
+        float b[TN] = {0.0f, 0.0f};
+        if (bias) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t c = n0 + wn * WN + j * 32 + l32;
+                b[j] = c < N ? __uint_as_float((uint32_t)bias[c] << 16) : 0.0f;
+            }
+        }
+        const int64_t col = n0 + wn * WN + lane;
+        typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+        typedef float f2 __attribute__((ext_vector_type(2)));
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
-                if (row >= M)
-                    continue;
-                if constexpr (I32OUT) {
-                    yi[row * N + col] = (int32_t)acc[i][j][r];
-                } else {
-                    float v = acc[i][j][r] + b;
-                    if constexpr (GELU)
-                        v = gelu_tanh(v);
-                    y[row * ldy + col] = f32_to_bf16_rne(v);
+                float v0 = acc[i][0][r] + b[0];
+                float v1 = acc[i][1][r] + b[1];
+                if constexpr (GELU) {
+                    v0 = gelu_tanh(v0);
+                    v1 = gelu_tanh(v1);
+                }
+                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
+                                                                 __float_as_uint(v1), false, false);
+                const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
+                const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
+                const int64_t row0 = m0 + wm * WM + i * 32 + 8 * (r >> 2) + (r & 3);
+                const int64_t row1 = row0 + 4;
+                if (col < N) {
+                    if (row0 < M)
+                        y[row0 * ldy + col] = (uint16_t)pk;
+                    if (row1 < M)
+                        y[row1 * ldy + col] = (uint16_t)(pk >> 16);
                 }
             }
         }
