@@ -3,7 +3,7 @@
 //
 // One 64-element group is handled by a team of 8 lanes, each lane owning 8
 // consecutive bf16 values (one 16-byte load).  A work item is 8 consecutive
-// rows (one per team) x 4 consecutive groups: every load instruction reads
+// rows (one per team) x 2 consecutive groups: every load instruction reads
 // one full 128-byte line per row, and since the outputs are stored
 // K-group-major (codes [K/64][M][32], flags [K/64][M][64/G_s], scales
 // [K/64][M]) every code store of a wave writes 256 contiguous bytes.  Waves
@@ -40,7 +40,7 @@ constexpr uint32_t kMagicBits = 0x4B400000u;
 constexpr float kInv127 = 1.0f / 127.0f;       // fp32(1/127)
 constexpr int kRsrcWord3 = 0x00020000;         // raw buffer, out-of-range reads zero
 constexpr int kNonTemporal = 2;                // cache policy: x is streamed once
-constexpr int kGroupsPerItem = 4;
+constexpr int kGroupsPerItem = 2;
 constexpr int kWavesPerBlock = 4;
 
 // DPP controls (gfx9 encoding).
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
 
     struct Item {
         int64_t row0, g0;
-        int rows, ng;       // valid rows (<= 8) and groups (<= 4)
+        int rows, ng;       // valid rows (<= 8) and groups (<= kGroupsPerItem)
     };
     auto item_of = [&](uint32_t it) {
         Item t;
@@ -244,8 +244,8 @@ hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8
     const int64_t G = K / 64;
     const int64_t quads = (G + kGroupsPerItem - 1) / kGroupsPerItem;
     const int64_t items = (M + 7) / 8 * quads;
-    // up to 24 waves per CU on 256 CUs, each walking the items with a grid stride
-    const int64_t max_blocks = 256 * 24 / kWavesPerBlock;
+    // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
+    const int64_t max_blocks = 256 * 32 / kWavesPerBlock;
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock, max_blocks);
     quantize_act_kernel<GS><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
         x, M, G, ldx, quads, items, codes, flags, scales, zeros);
