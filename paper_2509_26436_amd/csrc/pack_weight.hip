@@ -37,29 +37,24 @@ __device__ __forceinline__ uint32_t f16_bits_rne_sat(float s)
     return b;
 }
 
-// grid covers panels * 64 columns x G groups; one team per (column, group)
-__global__ __launch_bounds__(256) void pack_weight_kernel(
-    const uint16_t* __restrict__ w, int64_t N, int64_t K, int64_t padded_cols,
-    uint8_t* __restrict__ w_packed, uint16_t* __restrict__ w_scales)
-{
-    const int lane = threadIdx.x & 63;
-    const int u = lane & 7;
-    const int64_t G = K / 64;
-    const int64_t team = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
-    const int64_t total = padded_cols * G;
-    const bool live = team < total;
-    // team -> (panel, group, column in panel); consecutive teams walk the
-    // columns of one (panel, group) chunk so the chunk is written contiguously
-    const int64_t cpan = team % kPanel;
-    const int64_t pg = team / kPanel;
-    const int64_t g = pg % G;
-    const int64_t panel = pg / G;
-    const int64_t n = panel * kPanel + cpan;
-    const bool real = live && n < N;
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;     // raw buffer, out-of-range reads zero
+constexpr int kNonTemporal = 2;            // cache policy: w is streamed once
+constexpr int kWavesPerBlock = 4;
+constexpr int kGroupsPerItem = 2;
 
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (real)
-        v = *reinterpret_cast<const uint4*>(w + n * K + g * 64 + u * 8);
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             kRsrcWord3);
+}
+
+// One column-group of one lane: 8 bf16 weights -> the nibble word; the team's
+// fp16 scale.  r = 1/s is one Newton step on the hardware reciprocal, equal to
+// the IEEE quotient for every finite fp16 s; the scale itself keeps the IEEE
+// division (fp16(beta * fp32(1/7)) differs from fp16(beta / 7) for a few beta).
+__device__ __forceinline__ void pack_group(uint4 v, uint32_t& word, uint32_t& s16)
+{
     const uint32_t d[4] = {v.x, v.y, v.z, v.w};
     float f[8];
 #pragma unroll
@@ -67,18 +62,20 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(
         f[2 * p] = __uint_as_float(d[p] << 16);
         f[2 * p + 1] = __uint_as_float(d[p] & 0xFFFF0000u);
     }
-    float amax = 0.0f;
+    float amax = fabsf(f[0]);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 1; i < 8; ++i)
         amax = fmaxf(amax, fabsf(f[i]));
     uint32_t ab = __float_as_uint(amax);
     ab = max(ab, dpp_xor1(ab));
     ab = max(ab, dpp_xor2(ab));
     ab = max(ab, dpp_half_mirror(ab));
     const float beta = __uint_as_float(ab);
-    const uint32_t s16 = f16_bits_rne_sat(beta / 7.0f);
+    s16 = f16_bits_rne_sat(beta / 7.0f);
     const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)s16);
-    const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+    const float r0 = __builtin_amdgcn_rcpf(s);
+    const float e = __builtin_fmaf(-s, r0, 1.0f);
+    const float r = s16 == 0 ? 0.0f : __builtin_fmaf(r0, e, r0);
 
     uint32_t T = 0;
 #pragma unroll
@@ -91,16 +88,97 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(
 #pragma unroll
     for (int p = 0; p < 4; ++p)
         S |= (d[p] & 0x80008000u) >> (12 - 4 * p);
-    const uint32_t word = T | (S & (T + 0x77777777u));
+    word = T | (S & (T + 0x77777777u));
+}
 
-    if (live) {
-        uint8_t* chunk = w_packed + (panel * G + g) * kChunkBytes;
-        reinterpret_cast<uint32_t*>(chunk + cpan * 32)[u] = word;
-        if (u == 0) {
-            reinterpret_cast<uint16_t*>(chunk + kChunkCodeBytes)[cpan] = (uint16_t)s16;
-            if (real && w_scales)
-                w_scales[n * G + g] = (uint16_t)s16;
+// A work item is 8 consecutive columns of one panel (one team of 8 lanes per
+// column, each lane 8 weights) x kGroupsPerItem groups.  Waves walk the items
+// with a grid stride and load the next item before packing the current one.
+// Columns past N read as zero (outside the buffer range) and pack to zero
+// codes and scales, as the padded panel layout requires.
+__global__ __launch_bounds__(64 * kWavesPerBlock) void pack_weight_kernel(
+    const uint16_t* __restrict__ w, int64_t N, int64_t K, int64_t panels,
+    uint8_t* __restrict__ w_packed, uint16_t* __restrict__ w_scales)
+{
+    const int lane = threadIdx.x & 63;
+    const int team = lane >> 3;            // column within the item
+    const int u = lane & 7;
+    const int64_t G = K / 64;
+    // item indices are wave-uniform and below 2^31 (N * K / 64 <= 2^28)
+    const uint32_t gpairs = (uint32_t)((G + kGroupsPerItem - 1) / kGroupsPerItem);
+    const uint32_t nitems = (uint32_t)(panels * (kPanel / 8)) * gpairs;
+    const uint32_t stride = gridDim.x * kWavesPerBlock;
+    const uint32_t w_off = (uint32_t)((team * K + u * 8) * 2);
+
+    struct Item {
+        int64_t panel, n0, g0;   // first column n0 = panel * 64 + 8 c8
+        int c8, ng;
+    };
+    auto item_of = [&](uint32_t it) {
+        Item t;
+        const uint32_t pc = it / gpairs;           // (panel, 8-column block)
+        t.g0 = (int64_t)(it % gpairs) * kGroupsPerItem;
+        t.panel = pc / (kPanel / 8);
+        t.c8 = (int)(pc % (kPanel / 8));
+        t.n0 = t.panel * kPanel + t.c8 * 8;
+        t.ng = (int)min(G - t.g0, (int64_t)kGroupsPerItem);
+        return t;
+    };
+    auto load = [&](const Item& t, uint4 (&v)[kGroupsPerItem]) {
+        // bytes from the item's base to the end of its last real column's K weights
+        const int64_t cols = min(N - t.n0, (int64_t)8);
+        const uint32_t bytes =
+            cols > 0 ? (uint32_t)(((cols - 1) * K + (G - t.g0) * 64) * 2) : 0u;
+        const Rsrc rw = make_rsrc(w + (cols > 0 ? t.n0 * K + t.g0 * 64 : 0), bytes);
+#pragma unroll
+        for (int j = 0; j < kGroupsPerItem; ++j)
+            v[j] = j < t.ng ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                          rw, (int)(w_off + j * 128), 0, kNonTemporal))
+                            : make_uint4(0, 0, 0, 0);
+    };
+    auto work = [&](const Item& t, const uint4 (&v)[kGroupsPerItem]) {
+        const int cpan = t.c8 * 8 + team;
+        const int64_t n = t.n0 + team;
+#pragma unroll
+        for (int j = 0; j < kGroupsPerItem; ++j) {
+            if (j >= t.ng)
+                break;
+            uint32_t word, s16;
+            pack_group(v[j], word, s16);
+            const int64_t g = t.g0 + j;
+            uint8_t* chunk = w_packed + (t.panel * G + g) * kChunkBytes;
+            reinterpret_cast<uint32_t*>(chunk + cpan * 32)[u] = word;
+            if (u == 0) {
+                reinterpret_cast<uint16_t*>(chunk + kChunkCodeBytes)[cpan] = (uint16_t)s16;
+                if (n < N && w_scales)
+                    w_scales[n * G + g] = (uint16_t)s16;
+            }
         }
+    };
+
+    uint4 va[kGroupsPerItem], vb[kGroupsPerItem];
+    uint32_t it = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (it >= nitems)
+        return;
+    Item ta = item_of(it), tb = ta;
+    load(ta, va);
+    while (true) {
+        const uint32_t nb = it + stride;
+        if (nb < nitems) {
+            tb = item_of(nb);
+            load(tb, vb);
+        }
+        work(ta, va);
+        if (nb >= nitems)
+            break;
+        it = nb + stride;
+        if (it < nitems) {
+            ta = item_of(it);
+            load(ta, va);
+        }
+        work(tb, vb);
+        if (it >= nitems)
+            break;
     }
 }
 
@@ -136,11 +214,14 @@ __global__ __launch_bounds__(256) void unpack_weight_kernel(
 hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
                               uint16_t* w_scales, hipStream_t stream)
 {
-    const int64_t padded = (N + kPanel - 1) / kPanel * kPanel;
-    const int64_t teams = padded * (K / 64);
-    const int64_t blocks = (teams * 8 + 255) / 256;
-    pack_weight_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(w, N, K, padded, w_packed,
-                                                                          w_scales);
+    const int64_t panels = (N + kPanel - 1) / kPanel;
+    const int64_t gpairs = (K / 64 + kGroupsPerItem - 1) / kGroupsPerItem;
+    const int64_t items = panels * (kPanel / 8) * gpairs;
+    // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
+    const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock,
+                               (int64_t)(256 * 32 / kWavesPerBlock));
+    pack_weight_kernel<<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
+        w, N, K, panels, w_packed, w_scales);
     return hipGetLastError();
 }
 
