@@ -315,9 +315,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
 
     // One group, tiles in the order (0,0) (1,0) (0,1) (1,1).  The fp8 product
     // of each tile is issued one step ahead: step t issues the scale MFMA of
-    // tile t, the fp8 MFMA of tile t + 1 and then the FMAs of tile t, which
-    // therefore wait only for the short scale MFMA while the matrix unit
-    // works on the next product.  The first product of a group is issued
+    // tile t, then the FMAs of tile t (which wait only for the short scale
+    // MFMA) with the fp8 MFMA of tile t + 1 issued between their two halves,
+    // so the matrix unit works on the next product meanwhile and the other
+    // math wave's MFMAs can slot in between.  The first product of a group is issued
     // right after the barrier, and the last tile's FMAs follow it (its
     // results stay live across the barrier).  Operands are prefetched for
     // the next group after their last use.  The asm statement pins each
@@ -347,26 +348,51 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             v8h sa_op = {}, sw_op = {};
             sa_op[0] = sa_h[i];
             sw_op[0] = sw_h[j];
+            __builtin_amdgcn_s_setprio(3);
             sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+            __builtin_amdgcn_s_setprio(0);
         }
         return sc;
     };
+    // MFMA issue runs at raised wave priority (above the decode waves): the
+    // matrix unit is the resource to keep fed, and a math wave whose MFMA is
+    // held back also holds back the FMAs behind it.
+    auto mfma_p = [&](int i) {
+        __builtin_amdgcn_s_setprio(3);
+        const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf, zero, 0, 0, 0, 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+        return p;
+    };
+    auto fma_rows = [&](int i, int j, const v16f& p, const v16f& sc, int r0) {
+#pragma unroll
+        for (int r = r0; r < r0 + 8; ++r) {
+            if constexpr (I32OUT)
+                acc[i][j][r] += p[r];
+            else
+                acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
+        }
+        asm volatile("" : "+v"(acc[i][j]));
+    };
     auto compute = [&](int cb, int nb) {
         // product of tile 0, then the last tile of the previous group
-        p_next = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[0], bf, zero, 0, 0, 0, 0, 0, 0);
+        p_next = mfma_p(0);
         __builtin_amdgcn_sched_barrier(0);
         fma_tile(TM - 1, TN - 1, p_last, s_last);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int t = 0; t < TM * TN; ++t) {
+            // step t: scale MFMA of tile t, half of tile t's FMAs, fp8 MFMA of
+            // tile t + 1, operand refills, the other half of the FMAs (so a
+            // wave never issues two MFMAs back to back)
             const int i = t % TM, j = t / TM;
             const v16f p = p_next;
             const v16f sc = scale_tile(i, j);
-            if (t + 1 < TM * TN) {
-                const int i1 = (t + 1) % TM;
-                p_next = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i1], bf, zero, 0, 0,
-                                                                          0, 0, 0, 0);
-            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (t + 1 < TM * TN)
+                fma_rows(i, j, p, sc, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (t + 1 < TM * TN)
+                p_next = mfma_p((t + 1) % TM);
             __builtin_amdgcn_sched_barrier(0);
             // refills after the last use of each operand: af[i] by the product of
             // tile (i,1) (issued one step ahead), sa_h[i] by the scale of tile
@@ -381,7 +407,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 load_a(1, nb);
             __builtin_amdgcn_sched_barrier(0);
             if (t + 1 < TM * TN) {
-                fma_tile(i, j, p, sc);
+                fma_rows(i, j, p, sc, 8);
             } else {
                 p_last = p;
                 s_last = sc;
