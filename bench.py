@@ -41,7 +41,7 @@ PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
-                for f in ("w4a4_gemm.hip", "quartz_internal.h")]
+                for f in ("w4a4_gemm.hip", "gemm_schedule.h", "quartz_internal.h")]
 
 
 def log(*a):
@@ -128,9 +128,11 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
     w2, b2 = to(W.make_w(4, 1)), to(W.make_bias(4, 1))
     pw1, pw2 = q.pack_weight(w1), q.pack_weight(w2)
     qa1 = q.quantize_act(x1, lzs_group=gs)
-    y1 = q.w4a4_linear(qa1, pw1, b1, 1)
+    ws1 = q.gemm_workspace(L1.M, L1.N, L1.K, dev)
+    ws2 = q.gemm_workspace(L2.M, L2.N, L2.K, dev)
+    y1 = q.w4a4_linear(qa1, pw1, b1, 1, workspace=ws1)
     qa2 = q.quantize_act(y1, lzs_group=gs)
-    y2 = q.w4a4_linear(qa2, pw2, b2, 0)
+    y2 = q.w4a4_linear(qa2, pw2, b2, 0, workspace=ws2)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     t = np.zeros(4)
@@ -139,11 +141,11 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
         ev[0].record(stream)
         q.quantize_act(x1, lzs_group=gs, out=qa1)
         ev[1].record(stream)
-        q.w4a4_linear(qa1, pw1, b1, 1, out=y1)
+        q.w4a4_linear(qa1, pw1, b1, 1, out=y1, workspace=ws1)
         ev[2].record(stream)
         q.quantize_act(y1, lzs_group=gs, out=qa2)
         ev[3].record(stream)
-        q.w4a4_linear(qa2, pw2, b2, 0, out=y2)
+        q.w4a4_linear(qa2, pw2, b2, 0, out=y2, workspace=ws2)
         ev[4].record(stream)
         torch.cuda.synchronize()
         if it >= 2:
@@ -208,19 +210,22 @@ def main():
         log(f"layer {L.name}: M={L.M} K={L.K} N={L.N} generated")
     log(f"inputs ready in {time.time() - t0:.1f}s")
 
-    # outputs preallocated once (the step allocates nothing new)
+    # outputs and GEMM workspaces preallocated once (the step allocates nothing new)
     outs = []
+    workspaces = []
     for (x, w, b), L in zip(dev_in, layers):
         qa = q.quantize_act(x, lzs_group=gs)
         pw = q.pack_weight(w)
         y = torch.empty((L.M, L.N), dtype=torch.bfloat16, device=dev)
         outs.append((qa, pw, y))
+        workspaces.append(q.gemm_workspace(L.M, L.N, L.K, dev))
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
 
     def step(events=None):
-        for li, ((x, w, b), (qa, pw, y), L) in enumerate(zip(dev_in, outs, layers)):
+        for li, ((x, w, b), (qa, pw, y), ws, L) in enumerate(zip(dev_in, outs, workspaces,
+                                                                 layers)):
             ev = events[li] if events is not None else None
             if ev: ev[0].record(stream)
             q.quartz_pack_weight(q._ptr(w), L.N, L.K, 64, q._ptr(pw.data), q._ptr(pw.scales),
@@ -228,7 +233,7 @@ def main():
             if ev: ev[1].record(stream)
             q.quantize_act(x, lzs_group=gs, out=qa)
             if ev: ev[2].record(stream)
-            q.w4a4_linear(qa, pw, b, L.epilogue, out=y)
+            q.w4a4_linear(qa, pw, b, L.epilogue, out=y, workspace=ws)
             if ev: ev[3].record(stream)
 
     for _ in range(args.warmup):
@@ -305,7 +310,7 @@ def main():
 
     mlp = None
     if not args.no_batched_mlp:
-        del outs, dev_in
+        del outs, dev_in, workspaces
         torch.cuda.empty_cache()
         t_m = time.time()
         mlp = batched_mlp(q, W, torch, np, gs)
@@ -349,7 +354,7 @@ def main():
             "workload": cfg.name,
             "layers": [f"{L.name} M={L.M} K={L.K} N={L.N}" for L in layers],
             "group_size": 64, "lzs_group": gs,
-            "step": "pack_weight + quantize_act + w4a4_linear per layer",
+            "step": "pack_weight + quantize_act + w4a4_linear (workspace entry point) per layer",
         },
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_FP8_TFLOPS,

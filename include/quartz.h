@@ -50,7 +50,8 @@ typedef enum quartz_status {
     QUARTZ_ERR_SHAPE = 2,       /* negative size, K % 64 != 0, ld too small, too large */
     QUARTZ_ERR_UNSUPPORTED = 3, /* group_size, lzs_group, mode or epilogue not supported */
     QUARTZ_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
-    QUARTZ_ERR_HIP = 5          /* the kernel launch failed */
+    QUARTZ_ERR_HIP = 5,         /* the kernel launch failed */
+    QUARTZ_ERR_WORKSPACE = 6    /* workspace smaller than the size query asks for */
 } quartz_status;
 
 enum { QUARTZ_MODE_SYMMETRIC = 0 };
@@ -115,9 +116,12 @@ quartz_status quartz_pack_weight(const void* w_bf16, int64_t N, int64_t K, int32
  *                                 symmetric mode never needs it).
  *   w_packed    output of quartz_pack_weight for N, K.
  *   bias_bf16   bf16 [N] or NULL.
- *   y_bf16      bf16 [M][ldy], ldy >= N.
+ *   y_bf16      bf16 [M][ldy], N <= ldy <= 2^24.
  *   epilogue    QUARTZ_EPI_NONE or QUARTZ_EPI_GELU_TANH.
- * M = 0 or N = 0 returns QUARTZ_OK without launching.
+ * M = 0 or N = 0 returns QUARTZ_OK without launching.  The output has at most
+ * 2^31 - 1 tiles of 256 x 128 (QUARTZ_ERR_SHAPE otherwise).
+ * The kernel is persistent: one workgroup per compute unit walks its share of
+ * the output tiles as one continuous pipeline (Section 4.4 fixes no order).
  */
 quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                                  const uint16_t* scales, const int8_t* zeros,
@@ -125,6 +129,40 @@ quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                                  int64_t M, int64_t N, int64_t K, int64_t ldy,
                                  int32_t group_size, int32_t lzs_group, int32_t epilogue,
                                  hipStream_t stream);
+
+/*
+ * The same W4A4 linear layer with a caller-provided workspace, which lets the
+ * GEMM balance its work over the whole device: when the output tiles do not
+ * fill a whole number of rounds of one workgroup per compute unit, the grid
+ * becomes persistent and the tiles of the last rounds are cut along K
+ * (stream-K); a tile shared by several workgroups gets their fp32 partial
+ * sums added in a fixed order by the last one to finish, so results are
+ * deterministic.  The values are those of quartz_w4a4_linear up to the fp32
+ * summation order over groups (Section 4.4 fixes no order).
+ *
+ *   workspace        device memory, 16-byte aligned, at least
+ *                    quartz_w4a4_linear_workspace_bytes(M, N, K, 64) bytes,
+ *                    or NULL (then this is exactly quartz_w4a4_linear).
+ *                    Its first use must find it zero-filled; every call leaves
+ *                    it ready for the next one.  Calls that use one workspace
+ *                    must not overlap in time (one stream, or synchronized).
+ *   workspace_bytes  its size; a smaller size than the query gives returns
+ *                    QUARTZ_ERR_WORKSPACE and launches nothing.
+ * The other arguments are those of quartz_w4a4_linear.  The library does not
+ * keep the workspace between calls; the caller owns it.
+ *
+ * quartz_w4a4_linear_workspace_bytes: the size for this M, N, K on the
+ * current device (it depends on its number of compute units); 0 when the
+ * tiles fill whole rounds (then NULL may be passed) or the sizes are invalid.
+ */
+size_t quartz_w4a4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t group_size);
+
+quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
+                                    const uint16_t* scales, const int8_t* zeros,
+                                    const void* w_packed, const void* bias_bf16, void* y_bf16,
+                                    int64_t M, int64_t N, int64_t K, int64_t ldy,
+                                    int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Test / inspection helpers.
@@ -141,6 +179,26 @@ quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                    const void* w_packed, int32_t* acc_out, int64_t M, int64_t N,
                                    int64_t K, int32_t group_size, int32_t lzs_group,
                                    hipStream_t stream);
+
+/*
+ * quartz_w4a4_linear_schedule (host only, needs no GPU): the GEMM work
+ * schedule for a persistent grid of at most `blocks` workgroups (the entry
+ * points use the device's compute-unit count), with (split = 1, as
+ * quartz_w4a4_linear_ws) or without (split = 0, as quartz_w4a4_linear) tiles
+ * cut along K.
+ *   schedule  host int32[10]: tiles_n, groups, split, blocks, whole tiles of
+ *             workgroup 0, sk_first, sk_tiles, sk_blocks, sk_q, sk_r.
+ *   segments  host int32[capacity][10], one row per (workgroup, segment):
+ *             workgroup, segment index, tile, g0, g1 (groups [g0, g1)),
+ *             split-tile index or -1, slot or -1, first and last workgroup
+ *             sharing the tile (or -1), and the slot the finishing workgroup
+ *             reads for this workgroup's share (or -1).
+ * Returns the number of segments (rows past `capacity` are not written), -1
+ * for invalid arguments, -2 if the schedule is inconsistent (a library bug).
+ */
+int64_t quartz_w4a4_linear_schedule(int64_t M, int64_t N, int64_t K, int32_t blocks,
+                                    int32_t split, int32_t* schedule, int32_t* segments,
+                                    int64_t capacity);
 
 /* Static, NUL-terminated description of a status code (host memory). */
 const char* quartz_status_string(quartz_status s);

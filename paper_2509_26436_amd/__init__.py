@@ -18,10 +18,11 @@ from dataclasses import dataclass
 __all__ = [
     "QuartzError", "library_path", "load",
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
-    "quartz_w4a4_linear", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
+    "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
+    "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_status_string", "QuantizedAct", "PackedWeight",
-    "quantize_act", "pack_weight", "w4a4_linear", "unpack_weight", "w4a4_gemm_i32",
-    "EXPORTED_SYMBOLS",
+    "quantize_act", "pack_weight", "w4a4_linear", "gemm_workspace", "linear_schedule",
+    "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -35,7 +36,8 @@ GROUP = 64
 
 EXPORTED_SYMBOLS = (
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
-    "quartz_w4a4_linear", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
+    "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
+    "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_status_string",
 )
 
@@ -72,6 +74,13 @@ def load() -> ctypes.CDLL:
     lib.quartz_pack_weight.restype = I32
     lib.quartz_w4a4_linear.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32, P]
     lib.quartz_w4a4_linear.restype = I32
+    lib.quartz_w4a4_linear_workspace_bytes.argtypes = [I64, I64, I64, I32]
+    lib.quartz_w4a4_linear_workspace_bytes.restype = SZ
+    lib.quartz_w4a4_linear_ws.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32,
+                                          P, SZ, P]
+    lib.quartz_w4a4_linear_ws.restype = I32
+    lib.quartz_w4a4_linear_schedule.argtypes = [I64, I64, I64, I32, I32, P, P, I64]
+    lib.quartz_w4a4_linear_schedule.restype = I64
     lib.quartz_unpack_weight.argtypes = [P, I64, I64, I32, P, P]
     lib.quartz_unpack_weight.restype = I32
     lib.quartz_w4a4_gemm_i32.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P]
@@ -106,6 +115,23 @@ def quartz_w4a4_linear(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, 
                        group_size, lzs_group, epilogue, stream) -> int:
     return load().quartz_w4a4_linear(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, ldy,
                                      group_size, lzs_group, epilogue, stream)
+
+
+def quartz_w4a4_linear_workspace_bytes(M, N, K, group_size=GROUP) -> int:
+    return int(load().quartz_w4a4_linear_workspace_bytes(M, N, K, group_size))
+
+
+def quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, ldy,
+                          group_size, lzs_group, epilogue, workspace, workspace_bytes,
+                          stream) -> int:
+    return load().quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, K,
+                                        ldy, group_size, lzs_group, epilogue, workspace,
+                                        workspace_bytes, stream)
+
+
+def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
+    return int(load().quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments,
+                                                  capacity))
 
 
 def quartz_unpack_weight(w_packed, N, K, group_size, wq, stream) -> int:
@@ -198,9 +224,18 @@ def pack_weight(w, with_scales: bool = True, stream=None) -> PackedWeight:
     return PackedWeight(data=data, scales=scales, N=N, K=K)
 
 
+def gemm_workspace(M: int, N: int, K: int, device):
+    """Zero-filled uint8 workspace for ``w4a4_linear(..., workspace=...)`` on ``device`` (the
+    current device's size query), or None when this shape needs none."""
+    torch = _torch()
+    nbytes = quartz_w4a4_linear_workspace_bytes(M, N, K, GROUP)
+    return torch.zeros((nbytes,), dtype=torch.uint8, device=device) if nbytes else None
+
+
 def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI_NONE,
-                out=None, stream=None):
-    """Returns y bf16 [M, N] (or writes ``out``, a bf16 [M, >=N] view with unit column stride)."""
+                out=None, stream=None, workspace=None):
+    """Returns y bf16 [M, N] (or writes ``out``, a bf16 [M, >=N] view with unit column stride).
+    With ``workspace`` (from ``gemm_workspace``) the call is quartz_w4a4_linear_ws."""
     torch = _torch()
     if a.K != w.K:
         raise ValueError("K mismatch between activations and weights")
@@ -209,11 +244,40 @@ def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI
     if out is None:
         out = torch.empty((a.M, w.N), dtype=torch.bfloat16, device=a.codes.device)
     ldy = out.stride(0)
-    st = quartz_w4a4_linear(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
-                            _ptr(w.data), _ptr(bias), _ptr(out), a.M, w.N, a.K, ldy, GROUP,
-                            a.lzs_group, epilogue, _stream_handle(stream))
-    _check(st, "quartz_w4a4_linear")
+    if workspace is None:
+        st = quartz_w4a4_linear(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                                _ptr(w.data), _ptr(bias), _ptr(out), a.M, w.N, a.K, ldy, GROUP,
+                                a.lzs_group, epilogue, _stream_handle(stream))
+        _check(st, "quartz_w4a4_linear")
+    else:
+        st = quartz_w4a4_linear_ws(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                                   _ptr(w.data), _ptr(bias), _ptr(out), a.M, w.N, a.K, ldy,
+                                   GROUP, a.lzs_group, epilogue, _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream_handle(stream))
+        _check(st, "quartz_w4a4_linear_ws")
     return out
+
+
+SCHEDULE_FIELDS = ("tiles_n", "groups", "split", "blocks", "dp_tiles_b0", "sk_first",
+                   "sk_tiles", "sk_blocks", "sk_q", "sk_r")
+SEGMENT_FIELDS = ("block", "index", "tile", "g0", "g1", "sk_tile", "slot", "b_first", "b_last",
+                  "finisher_slot")
+
+
+def linear_schedule(M: int, N: int, K: int, blocks: int, split: bool = True):
+    """Host-side GEMM work schedule for a persistent grid of at most ``blocks``
+    workgroups: (dict of SCHEDULE_FIELDS, int32 numpy array [segments, len(SEGMENT_FIELDS)])."""
+    import numpy as np
+    sched = np.zeros(len(SCHEDULE_FIELDS), dtype=np.int32)
+    n = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), sched.ctypes.data, None, 0)
+    if n < 0:
+        raise ValueError(f"schedule error {n}")
+    seg = np.zeros((max(n, 1), len(SEGMENT_FIELDS)), dtype=np.int32)
+    n2 = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), sched.ctypes.data,
+                                     seg.ctypes.data, n)
+    assert n2 == n
+    return dict(zip(SCHEDULE_FIELDS, (int(v) for v in sched))), seg[:n]
 
 
 def unpack_weight(w: PackedWeight, stream=None):

@@ -9,7 +9,8 @@ constexpr int64_t kMaxK = int64_t(1) << 20;       // at most 16384 groups per ro
 // rows x groups of one call (M x K/64 or N x K/64): 2^34 elements, 32 GiB of
 // bf16 input; keeps every grid below 2^32 threads
 constexpr int64_t kMaxRowGroups = int64_t(1) << 28;
-// leading dimension of the activations (elements): 8 rows of it stay below 2^32 bytes
+// leading dimension of the activations and of the output (elements): 64 bf16
+// rows of it stay below 2^31 bytes (one buffer range per wave of output rows)
 constexpr int64_t kMaxLd = int64_t(1) << 24;
 
 // sizes that every entry point accepts: rows >= 0, 0 <= K <= kMaxK, K % 64 == 0
@@ -55,6 +56,8 @@ const char* quartz_status_string(quartz_status s)
         return "a pointer is not 16-byte aligned";
     case QUARTZ_ERR_HIP:
         return "HIP kernel launch failed";
+    case QUARTZ_ERR_WORKSPACE:
+        return "workspace smaller than quartz_w4a4_linear_workspace_bytes";
     }
     return "unknown status";
 }
@@ -129,7 +132,9 @@ static quartz_status check_gemm(const uint8_t* codes, const uint8_t* flags, cons
     if (group_size != 64 || !lzs_ok(lzs_group))
         return QUARTZ_ERR_UNSUPPORTED;
     if (K <= 0 || !size_ok(M, K) || !size_ok(N, K) ||
-        (M + quartz::kGemmBlockRows - 1) / quartz::kGemmBlockRows > 65535)
+        ((M + quartz::kGemmBlockRows - 1) / quartz::kGemmBlockRows) *
+                ((N + quartz::kGemmBlockCols - 1) / quartz::kGemmBlockCols) >
+            quartz::kMaxGemmTiles)
         return QUARTZ_ERR_SHAPE;
     if (M == 0 || N == 0)
         return QUARTZ_OK;
@@ -140,6 +145,39 @@ static quartz_status check_gemm(const uint8_t* codes, const uint8_t* flags, cons
     return QUARTZ_OK;
 }
 
+static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
+                                 const uint16_t* scales, const void* w_packed,
+                                 const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
+                                 int64_t K, int64_t ldy, int32_t group_size, int32_t lzs_group,
+                                 int32_t epilogue, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream)
+{
+    if (epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH)
+        return QUARTZ_ERR_UNSUPPORTED;
+    quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, group_size, lzs_group);
+    if (st != QUARTZ_OK)
+        return st;
+    if (ldy < N || ldy > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (M == 0 || N == 0)
+        return QUARTZ_OK;
+    if (!scales || !y_bf16)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(scales) || !aligned16(y_bf16) || (bias_bf16 && !aligned16(bias_bf16)) ||
+        (workspace && !aligned16(workspace)))
+        return QUARTZ_ERR_ALIGN;
+    const quartz::GemmSchedule sch =
+        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+    if (sch.blocks <= 0)
+        return QUARTZ_ERR_HIP;          // no usable device
+    if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    return from_hip(quartz::launch_w4a4_linear(
+        codes, flags, scales, static_cast<const uint8_t*>(w_packed),
+        static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
+        lzs_group, epilogue, sch, workspace, stream));
+}
+
 quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                                  const uint16_t* scales, const int8_t* zeros,
                                  const void* w_packed, const void* bias_bf16, void* y_bf16,
@@ -148,23 +186,80 @@ quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                                  hipStream_t stream)
 {
     (void)zeros;   // the symmetric mode has zero points 0 by construction
-    if (epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH)
-        return QUARTZ_ERR_UNSUPPORTED;
-    quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, group_size, lzs_group);
-    if (st != QUARTZ_OK)
-        return st;
-    if (ldy < N)
-        return QUARTZ_ERR_SHAPE;
-    if (M == 0 || N == 0)
-        return QUARTZ_OK;
-    if (!scales || !y_bf16)
-        return QUARTZ_ERR_NULL;
-    if (!aligned16(scales) || !aligned16(y_bf16) || (bias_bf16 && !aligned16(bias_bf16)))
-        return QUARTZ_ERR_ALIGN;
-    return from_hip(quartz::launch_w4a4_linear(
-        codes, flags, scales, static_cast<const uint8_t*>(w_packed),
-        static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
-        lzs_group, epilogue, stream));
+    return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
+                       group_size, lzs_group, epilogue, nullptr, 0, stream);
+}
+
+size_t quartz_w4a4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t group_size)
+{
+    if (group_size != 64 || M <= 0 || N <= 0 || K <= 0 || !size_ok(M, K) || !size_ok(N, K))
+        return 0;
+    return quartz::gemm_workspace_bytes(
+        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), true));
+}
+
+quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
+                                    const uint16_t* scales, const int8_t* zeros,
+                                    const void* w_packed, const void* bias_bf16, void* y_bf16,
+                                    int64_t M, int64_t N, int64_t K, int64_t ldy,
+                                    int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    (void)zeros;
+    return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
+                       group_size, lzs_group, epilogue, workspace, workspace_bytes, stream);
+}
+
+int64_t quartz_w4a4_linear_schedule(int64_t M, int64_t N, int64_t K, int32_t blocks,
+                                    int32_t split, int32_t* schedule, int32_t* segments,
+                                    int64_t capacity)
+{
+    if (M <= 0 || N <= 0 || K <= 0 || !size_ok(M, K) || !size_ok(N, K) || blocks <= 0 ||
+        !schedule || capacity < 0 || (capacity > 0 && !segments))
+        return -1;
+    const quartz::GemmSchedule s = quartz::gemm_schedule(M, N, K, blocks, split != 0);
+    if (s.blocks <= 0)
+        return -1;
+    const int32_t fields[10] = {s.tiles_n, s.groups, s.sk_tiles > 0 ? 1 : 0, s.blocks,
+                                quartz::dp_count(s, 0), s.sk_first, s.sk_tiles, s.sk_blocks,
+                                s.sk_q, s.sk_r};
+    for (int i = 0; i < 10; ++i)
+        schedule[i] = fields[i];
+    int64_t n = 0;
+    for (int32_t b = 0; b < s.blocks; ++b) {
+        quartz::GemmSegment sg;
+        int32_t steps = 0;
+        for (int32_t j = 0; quartz::gemm_segment(s, b, j, sg); ++j, ++n) {
+            steps += sg.g1 - sg.g0;
+            if (n >= capacity)
+                continue;
+            int32_t b_first = -1, b_last = -1, other_slot = -1;
+            if (sg.sk_tile >= 0) {
+                quartz::sk_contributors(s, sg.sk_tile, b_first, b_last);
+                other_slot = quartz::sk_slot(s, b, sg.sk_tile);
+            }
+            const int32_t row[10] = {b, j, sg.tile, sg.g0, sg.g1, sg.sk_tile, sg.slot, b_first,
+                                     b_last, other_slot};
+            for (int i = 0; i < 10; ++i)
+                segments[n * 10 + i] = row[i];
+        }
+        // the kernel walks the same segments incrementally
+        quartz::GemmCursor c;
+        int32_t jc = 0, padded = 0;
+        for (bool ok = quartz::cursor_begin(s, b, c); ok; ok = quartz::cursor_next(s, b, c), ++jc) {
+            quartz::GemmSegment ref;
+            if (!quartz::gemm_segment(s, b, jc, ref) || ref.tile != c.sg.tile || ref.g0 != c.sg.g0 ||
+                ref.g1 != c.sg.g1 || ref.sk_tile != c.sg.sk_tile || ref.slot != c.sg.slot ||
+                c.j != jc || (int64_t)c.tm * s.tiles_n + c.tn != c.sg.tile)
+                return -2;
+            padded += quartz::padded_steps(c.sg.g1 - c.sg.g0);
+        }
+        quartz::GemmSegment extra;
+        if (quartz::gemm_segment(s, b, jc, extra) || padded != quartz::gemm_steps(s, b) ||
+            padded < steps)
+            return -2;
+    }
+    return n;
 }
 
 quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,

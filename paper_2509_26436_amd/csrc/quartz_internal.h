@@ -3,7 +3,10 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
+
+#include "gemm_schedule.h"
 
 namespace quartz {
 
@@ -22,8 +25,11 @@ inline int64_t packed_weight_bytes(int64_t N, int64_t K)
     return panels * (K / kGroup) * kChunkBytes;
 }
 
-// Output tile per GEMM workgroup (grid.y = ceil(M / kGemmBlockRows) <= 65535).
+// Output tile per GEMM workgroup, and the most tiles one GEMM may have (the
+// schedule indexes them with 32-bit integers; an output that large would not
+// fit in device memory anyway).
 constexpr int64_t kGemmBlockRows = 256;
+constexpr int64_t kMaxGemmTiles = (int64_t(1) << 31) - 1;
 constexpr int64_t kGemmBlockCols = 128;
 
 // ---------------------------------------------------------------- launchers
@@ -39,10 +45,23 @@ hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* 
 hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, int8_t* wq,
                                 hipStream_t stream);
 
+// Work schedule of the GEMM for a persistent grid of at most `blocks`
+// workgroups (split: tiles of the last rounds may be cut along K, which needs
+// a workspace; s.blocks == 0 when there is nothing to launch or blocks <= 0),
+// its workspace size (0 when no tile is split) and the persistent grid size
+// of the current device (CUs x resident workgroups per CU; 0 if there is no
+// device).
+GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split);
+size_t gemm_workspace_bytes(const GemmSchedule& s);
+int gemm_resident_blocks();
+
+// `workspace`: gemm_workspace_bytes(sch) bytes whose counter part is zero
+// (left zero again by the launch); unused unless sch.persistent.
 hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                               const uint16_t* scales, const uint8_t* w_packed,
                               const uint16_t* bias, uint16_t* y, int64_t M, int64_t N, int64_t K,
-                              int64_t ldy, int lzs_group, int epilogue, hipStream_t stream);
+                              int64_t ldy, int lzs_group, int epilogue, const GemmSchedule& sch,
+                              void* workspace, hipStream_t stream);
 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,

@@ -24,8 +24,11 @@
 // streams are independent, so the SIMD interleaves them.  All global
 // addressing is scalar: buffer loads whose resource base advances by one
 // group per iteration.
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
 
+#include "gemm_schedule.h"
 #include "quartz_internal.h"
 
 namespace quartz {
@@ -44,13 +47,6 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes)
 {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                              kRsrcWord3);
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float v)
-{
-    uint32_t u = __float_as_uint(v);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
 }
 
 // GELU, tanh form: 0.5 v (1 + tanh(u)) with u = sqrt(2/pi) (v + 0.044715 v^3).
@@ -160,12 +156,19 @@ __device__ __forceinline__ uint2 expand_flags8(FlagRaw<GS> raw)
 // threads d < 128 also carry s_w of column d.  Rows past M and columns past
 // the packed panels fall outside the buffer ranges and read as zero: they
 // only feed outputs that are never stored, so nothing needs a bounds check.
-template <int GS, bool I32OUT, bool GELU>
+//
+// Persistent workgroups: each one walks its segments (gemm_schedule.h) as a
+// single pipeline.  The decode waves fetch and decode across segment
+// boundaries without a break, so while the math waves write one tile's
+// output the next tile's first groups are already being staged.  SPLIT
+// instantiations carry the partial-sum code of shared tiles.
+template <int GS, bool I32OUT, bool GELU, bool SPLIT>
 __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
-    int64_t M, int64_t N, int64_t K, int64_t ldy)
+    int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
+    uint32_t* __restrict__ counters, float* __restrict__ slots)
 {
     // three LDS stages: group g + 2 is decoded into one while the math waves
     // read the operands of group g + 1 from another (and multiply group g
@@ -179,119 +182,211 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
 
     constexpr int FB = 64 / GS;                           // flag bytes per (group, row)
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t m0 = (int64_t)blockIdx.y * BM;
-    const int64_t n0 = (int64_t)blockIdx.x * BN;
-    const int G = (int)(K / 64);
     const int uwave = __builtin_amdgcn_readfirstlane(wave);
     const bool decoder = uwave >= kMathWaves;
 
-    // ------------------------------------------------------ decode waves
-    static_assert(kDecodeThreads == BM && kDecodeThreads == 2 * BN, "decode roles");
-    const int d = tid - kMathWaves * 64;          // decode thread index (math waves: < 0)
-    const int dr = d & (BM - 1);                  // A row
-    const int bc = (d >> 1) & (BN - 1);           // B column
-    const int bh = d & 1;                         // B half
-    const int swc = d & (BN - 1);                 // column whose s_w this thread loads
-    const int64_t panels = (N + kPanel - 1) / kPanel;
-    const int64_t panel0 = n0 / kPanel;
-    const int64_t rows = min(M - m0, (int64_t)BM);
-    const uint32_t a_bytes = (uint32_t)(rows * 32);
-    const uint32_t f_bytes = (uint32_t)(rows * FB);
-    const uint32_t s_bytes = (uint32_t)(rows * 2);
-    const int64_t blk_panels = min(panels - panel0, (int64_t)kPanelsPerBlock);
-    const uint32_t b_bytes = (uint32_t)((blk_panels - 1) * G * kChunkBytes + kChunkBytes);
-    const uint32_t a_off = (uint32_t)(dr * 32);
-    const uint32_t f_off = (uint32_t)(dr * FB);
-    const uint32_t b_off = (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * 16);
-    const uint32_t sw_off =
-        (uint32_t)((swc / kPanel) * G * kChunkBytes + kChunkCodeBytes + (swc % kPanel) * 2);
+    // Values that must not stay live across the loops pass through opaque
+    // copies where they are used: the schedule (so the compiler re-derives
+    // the reciprocals of its divisors per segment, a few scalar instructions,
+    // instead of hoisting them into registers) and the thread index (so
+    // per-lane indices are recomputed after each tile's output code instead
+    // of occupying registers the main loop needs).
+    auto fresh_schedule = [&] {
+        GemmSchedule s = sch;
+        asm volatile("" : "+s"(s.tiles_n), "+s"(s.groups), "+s"(s.blocks), "+s"(s.sk_first),
+                          "+s"(s.sk_q), "+s"(s.sk_r), "+s"(s.sk_blocks), "+s"(s.sk_tiles));
+        return s;
+    };
+    auto fresh_tid = [&] {
+        int t = tid;
+        asm volatile("" : "+v"(t));
+        return t;
+    };
 
-    struct Raw {
-        uint4 a0, a1;
-        uint4 b;
-        FlagRaw<GS> f;
-        uint16_t sa, sw;
-    };
-    auto fetch = [&](Raw& r, int g) {
-        const Rsrc ra = make_rsrc(codes + ((int64_t)g * M + m0) * 32, a_bytes);
-        const Rsrc rf = make_rsrc(flags + ((int64_t)g * M + m0) * FB, f_bytes);
-        const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
-        r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off, 0, 0));
-        r.a1 = __builtin_bit_cast(uint4,
-                                  __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
-        r.f = load_flags_raw<GS>(rf, f_off);
-        r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
-        if constexpr (!I32OUT) {       // the integer path has no scales (scales == nullptr)
-            const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
-            r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
-            r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
-        } else {
-            r.sa = 0;
-            r.sw = 0;
-        }
-    };
-    // decode one group into LDS buffer `buf`
-    auto stage = [&](const Raw& r, int buf) {
-        const uint2 fl8 = expand_flags8<GS>(r.f);
-        const uint32_t a[8] = {r.a0.x, r.a0.y, r.a0.z, r.a0.w, r.a1.x, r.a1.y, r.a1.z, r.a1.w};
-        constexpr int kWordsPerFlag = GS / 8;
-        Fp8Table t = fp8_table<0>(fl8.x);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            uint2 w[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int wi = 2 * c + h;           // word index 0..7
-                if (wi % kWordsPerFlag == 0 && wi > 0) {
-                    const uint32_t f = wi < 4 ? fl8.x : fl8.y;
-                    switch (wi & 3) {
-                    case 0: t = fp8_table<0>(f); break;
-                    case 1: t = fp8_table<1>(f); break;
-                    case 2: t = fp8_table<2>(f); break;
-                    default: t = fp8_table<3>(f); break;
-                    }
-                }
-                w[h] = decode_nibbles_fp8(a[wi], t);
+    // ------------------------------------------------------ decode waves
+    if (decoder) {
+        static_assert(kDecodeThreads == BM && kDecodeThreads == 2 * BN, "decode roles");
+        const int d = tid - kMathWaves * 64;      // decode thread index
+        const int dr = d & (BM - 1);              // A row
+        const int bc = (d >> 1) & (BN - 1);       // B column
+        const int bh = d & 1;                     // B half
+        const int swc = d & (BN - 1);             // column whose s_w this thread loads
+        const int G = (int)(K / 64);
+        const int64_t panels = (N + kPanel - 1) / kPanel;
+        const uint32_t a_off = (uint32_t)(dr * 32);
+        const uint32_t f_off = (uint32_t)(dr * FB);
+        const uint32_t b_off = (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * 16);
+        const uint32_t sw_off =
+            (uint32_t)((swc / kPanel) * G * kChunkBytes + kChunkCodeBytes + (swc % kPanel) * 2);
+
+        // fetch cursor: segment fc, step fg of it (steps past its groups are
+        // no-ops), and the buffer ranges of its tile
+        const int32_t blk = (int32_t)blockIdx.x;
+        GemmCursor fc;
+        int fg = 0, fend = 0;
+        bool fdone = false;
+        int64_t m0 = 0, panel0 = 0;
+        uint32_t a_bytes = 0, f_bytes = 0, s_bytes = 0, b_bytes = 0;
+        auto set_ranges = [&] {
+            m0 = (int64_t)fc.tm * BM;
+            panel0 = (int64_t)fc.tn * (BN / kPanel);
+            const int64_t rows = min(M - m0, (int64_t)BM);
+            a_bytes = (uint32_t)(rows * 32);
+            f_bytes = (uint32_t)(rows * FB);
+            s_bytes = (uint32_t)(rows * 2);
+            const int64_t blk_panels = min(panels - panel0, (int64_t)kPanelsPerBlock);
+            b_bytes = (uint32_t)((blk_panels - 1) * G * kChunkBytes + kChunkBytes);
+        };
+        if (!cursor_begin(fresh_schedule(), blk, fc))
+            return;
+        fg = fc.sg.g0;
+        fend = fc.sg.g0 + padded_steps(fc.sg.g1 - fc.sg.g0);
+        set_ranges();
+
+        struct Raw {
+            uint4 a0, a1;
+            uint4 b;
+            FlagRaw<GS> f;
+            uint16_t sa, sw;
+        };
+        // fetch the cursor's group into r, then advance the cursor by one step.
+        // A no-op step (and any step past the end) reloads the segment's last
+        // group: every step issues the same loads, so the compiler can wait
+        // for exactly the ring slot being decoded (a conditional load would
+        // make it wait for all of them), and staging the copy is harmless
+        // since the stage a step writes is never read by another step.
+        auto fetch_next = [&](Raw& r) {
+            const int g = min(fg, fc.sg.g1 - 1);
+            const Rsrc ra = make_rsrc(codes + ((int64_t)g * M + m0) * 32, a_bytes);
+            const Rsrc rf = make_rsrc(flags + ((int64_t)g * M + m0) * FB, f_bytes);
+            const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
+            r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off, 0, 0));
+            r.a1 = __builtin_bit_cast(uint4,
+                                      __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
+            r.f = load_flags_raw<GS>(rf, f_off);
+            r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+            if constexpr (!I32OUT) {   // the integer path has no scales (scales == nullptr)
+                const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
+                r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
+                r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
+            } else {
+                r.sa = 0;
+                r.sw = 0;
             }
-            *reinterpret_cast<uint4*>(As[buf] + swz(dr, c)) = make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
+            if (!fdone && ++fg == fend) {
+                if (cursor_next(fresh_schedule(), blk, fc)) {
+                    fg = fc.sg.g0;
+                    fend = fc.sg.g0 + padded_steps(fc.sg.g1 - fc.sg.g0);
+                    set_ranges();
+                } else {
+                    fdone = true;
+                }
+            }
+        };
+        // decode one group into LDS buffer `buf`
+        auto stage = [&](const Raw& r, int buf) {
+            const uint2 fl8 = expand_flags8<GS>(r.f);
+            const uint32_t a[8] = {r.a0.x, r.a0.y, r.a0.z, r.a0.w, r.a1.x, r.a1.y, r.a1.z, r.a1.w};
+            constexpr int kWordsPerFlag = GS / 8;
+            Fp8Table t = fp8_table<0>(fl8.x);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                uint2 w[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int wi = 2 * c + h;           // word index 0..7
+                    if (wi % kWordsPerFlag == 0 && wi > 0) {
+                        const uint32_t f = wi < 4 ? fl8.x : fl8.y;
+                        switch (wi & 3) {
+                        case 0: t = fp8_table<0>(f); break;
+                        case 1: t = fp8_table<1>(f); break;
+                        case 2: t = fp8_table<2>(f); break;
+                        default: t = fp8_table<3>(f); break;
+                        }
+                    }
+                    w[h] = decode_nibbles_fp8(a[wi], t);
+                }
+                *reinterpret_cast<uint4*>(As[buf] + swz(dr, c)) = make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
+            }
+            const Fp8Table tw{kTabLo, kTabHi};
+            const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
+            const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
+            const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
+            const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
+            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
+            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
+            if constexpr (!I32OUT) {
+                sas[buf][dr] = r.sa;
+                if (d < BN)
+                    sws[buf][swc] = r.sw;
+            }
+        };
+
+        // The decode of each group is on the critical path of the next ones:
+        // these waves run at issue priority above the math waves' VALU work.
+        // They keep a register ring of three groups in flight and decode two
+        // groups ahead of the math waves, one workgroup barrier per group
+        // (plus one before the first), the same count the math waves execute.
+        Raw ring[kStages];
+        __builtin_amdgcn_s_setprio(2);
+        if (d < 8 * kStages) {
+            sas[d >> 3][BM + (d & 7)] = 0;
+            sws[d >> 3][BN + (d & 7)] = 0;
         }
-        const Fp8Table tw{kTabLo, kTabHi};
-        const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
-        const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
-        const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
-        const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
-        *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
-        *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
-        if constexpr (!I32OUT) {
-            sas[buf][dr] = r.sa;
-            if (d < BN)
-                sws[buf][swc] = r.sw;
+        const int steps = gemm_steps(fresh_schedule(), blk);
+        fetch_next(ring[0]);
+        fetch_next(ring[1]);
+        fetch_next(ring[2]);
+        stage(ring[0], 0);
+        fetch_next(ring[0]);
+        stage(ring[1], 1);
+        fetch_next(ring[1]);
+        lds_sync();
+        // Step s: decode step s + 2 (ring slot and LDS stage (s + 2) % 3) and
+        // refill the slot with step s + 5.  Straight-line code, so the
+        // compiler waits only for the slot being decoded.
+        auto dstep = [&](int u) {
+            const int k = (u + 2) % kStages;
+            stage(ring[k], k);
+            fetch_next(ring[k]);
+            lds_sync();
+        };
+        int s = 0;
+        for (; s + kStages <= steps; s += kStages) {
+#pragma unroll
+            for (int u = 0; u < kStages; ++u)
+                dstep(u);
         }
-    };
+#pragma unroll
+        for (int u = 0; u < kStages - 1; ++u)
+            if (s + u < steps)
+                dstep(u);
+        return;
+    }
 
     // -------------------------------------------------------- math waves
-    const int wm = (wave & (kMathWaves - 1)) / WAVES_N;
-    const int wn = (wave & (kMathWaves - 1)) % WAVES_N;
-    const int l32 = lane & 31;
-    const int khalf = lane >> 5;
+    // Per-lane fragment indices, recomputed from fresh_tid after every tile's
+    // output code (see above).
+    int lane, wm, wn, l32, khalf;
     int sa_idx[TM], sw_idx[TN];
+    auto set_fragment_indices = [&] {
+        const int t = fresh_tid();
+        const int w = __builtin_amdgcn_readfirstlane(t >> 6) & (kMathWaves - 1);   // wave-uniform
+        lane = t & 63;
+        wm = w / WAVES_N;
+        wn = w % WAVES_N;
+        l32 = t & 31;
+        khalf = (t >> 5) & 1;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-        sa_idx[i] = khalf ? BM : wm * WM + i * 32 + l32;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-        sw_idx[j] = khalf ? BN : wn * WN + j * 32 + l32;
-
-    v16f acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i)
+            sa_idx[i] = khalf ? BM : wm * WM + i * 32 + l32;
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                acc[i][j][r] = 0.0f;
+            sw_idx[j] = khalf ? BN : wn * WN + j * 32 + l32;
+    };
+
+    v16f acc[TM][TN];
 
     // Operands of the group being multiplied, held in registers; each one is
     // refilled with the next group's (from LDS stage nb) right after its last
@@ -325,11 +420,6 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // tile's FMAs (without a use, LLVM sinks them to the end of the loop).
     static_assert(TM == 2 && TN == 2, "prefetch order assumes 2 x 2 tiles");
     v16f p_next, p_last, s_last;       // product of the next tile; last tile's P and S
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        p_last[r] = 0.0f;              // the "last tile" before the first group adds 0
-        s_last[r] = 0.0f;
-    }
     const v16f zero = {};
     auto fma_tile = [&](int i, int j, const v16f& p, const v16f& sc) {
 #pragma unroll
@@ -373,7 +463,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         }
         asm volatile("" : "+v"(acc[i][j]));
     };
-    auto compute = [&](int cb, int nb) {
+    // one group from LDS stage cb; the next group's operands are prefetched
+    // from stage nb unless this is the last group of a segment (LAST)
+    auto compute = [&](int cb, int nb, auto last) {
+        constexpr bool LAST = decltype(last)::value;
         // product of tile 0, then the last tile of the previous group
         p_next = mfma_p(0);
         __builtin_amdgcn_sched_barrier(0);
@@ -399,11 +492,11 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             // (i,1), bf / sw_h[0] by column 0's products and scales
             if (t == 0)
                 load_b(1, cb);          // column 1 of this group (column 0's products are issued)
-            if (t == 2) {
+            if (t == 2 && !LAST) {
                 load_a(0, nb);
                 load_b(0, nb);          // column 0 of the next group
             }
-            if (t == 3)
+            if (t == 3 && !LAST)
                 load_a(1, nb);
             __builtin_amdgcn_sched_barrier(0);
             if (t + 1 < TM * TN) {
@@ -421,134 +514,251 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // accesses across it.
     auto math_barrier = [] { asm volatile("s_barrier" ::: "memory"); };
 
-    // ---- pipeline: decode waves keep a register ring of two groups in flight
-    // and decode two groups ahead of the math waves.  The two roles run
-    // separate loops with the same barriers (one before the first group and
-    // one after each), so their registers never overlap in liveness.
-    if (decoder) {
-        Raw ring[2];
-        // the decode of each group is on the critical path of the next ones:
-        // give these waves issue priority over the math waves
-        __builtin_amdgcn_s_setprio(2);
-        if (d < 8 * kStages) {
-            sas[d >> 3][BM + (d & 7)] = 0;
-            sws[d >> 3][BN + (d & 7)] = 0;
-        }
-        fetch(ring[0], 0);
-        fetch(ring[1], min(1, G - 1));
-        stage(ring[0], 0);
-        fetch(ring[0], min(2, G - 1));
-        stage(ring[1], 1);
-        fetch(ring[1], min(3, G - 1));
-        lds_sync();
-        // Iteration g: decode group g + 2 (ring slot g % 2) into stage
-        // (g + 2) % 3 and refill the slot with group g + 4.  Straight-line
-        // code with clamped prefetch indices (harmless reloads at the end),
-        // so the compiler waits only for the slot being decoded.
-        auto dstep = [&](int u, int g) {
-            stage(ring[u & 1], (u + 2) % kStages);
-            fetch(ring[u & 1], min(g + 4, G - 1));
-            lds_sync();
-        };
-        constexpr int kU = 2 * kStages;
+    // the first n groups of a segment (its first group is in LDS stage 0),
+    // each followed by the next one's operand prefetch
+    using NotLast = std::integral_constant<bool, false>;
+    auto run_groups = [&](int n) {
         int g = 0;
-        for (; g + kU <= G; g += kU) {
-#pragma unroll
-            for (int u = 0; u < kU; ++u)
-                dstep(u, g + u);
-        }
-#pragma unroll
-        for (int u = 0; u < kU - 1; ++u)
-            if (g + u < G)
-                dstep(u, g + u);
-        return;
-    }
-    lds_sync();
-    load_a(0, 0);
-    load_a(1, 0);
-    load_b(0, 0);
-    {
-        // iteration g multiplies group g and prefetches group g + 1 from
-        // stage (g + 1) % 3 (at the last group: a harmless read of a stale stage)
-        int g = 0;
-        for (; g + kStages <= G; g += kStages) {
+        for (; g + kStages <= n; g += kStages) {
 #pragma unroll
             for (int u = 0; u < kStages; ++u) {
-                compute(u % kStages, (u + 1) % kStages);
+                compute(u, (u + 1) % kStages, NotLast());
                 math_barrier();
             }
         }
 #pragma unroll
         for (int u = 0; u < kStages - 1; ++u) {
-            if (g + u < G) {
-                compute(u % kStages, (u + 1) % kStages);
+            if (g + u < n) {
+                compute(u, (u + 1) % kStages, NotLast());
                 math_barrier();
             }
         }
-    }
+    };
 
-    fma_tile(TM - 1, TN - 1, p_last, s_last);
-
-    // ---- epilogue.  Lane l holds column l % 32 of each 32 x 32 tile, rows
+    GemmCursor cur;
+    const int32_t blk = (int32_t)blockIdx.x;
+    // ---- output.  Lane l holds column l % 32 of each 32 x 32 tile, rows
     // 8 (r/4) + 4 khalf + r%4 of register r.
-    if constexpr (I32OUT) {
+    auto store_tile = [&](const v16f (&out)[TM][TN]) {
+        if constexpr (I32OUT) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t col = n0 + wn * WN + j * 32 + l32;
-            if (col >= N)
-                continue;
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = (int64_t)cur.tn * BN + wn * WN + j * 32 + l32;
+                if (col >= N)
+                    continue;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t row = (int64_t)cur.tm * BM + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                        if (row < M)
+                            yi[row * N + col] = (int32_t)out[i][j][r];
+                    }
+                }
+            }
+        } else {
+            // bias and activation per element, then one lane-half swap between the
+            // two column tiles: afterwards lane l holds column l of the wave's 64
+            // columns for one row (tile 0's rows in the first register, tile 1's
+            // khalf = 1 rows in the second), so every store covers a full 128-byte
+            // row segment; the pair is rounded to bf16 (RNE) by one conversion.
+            // Stores go through one buffer range per wave (its 64 rows from its
+            // first column): the row offset is wave-uniform (a scalar operand),
+            // rows past M fall outside the range and are dropped, and lanes
+            // whose column is past N get an offset outside it.
+            static_assert(TN == 2, "the swap pairs the two column tiles");
+            const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
+            const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
+            float b[TN] = {0.0f, 0.0f};
+            if (bias) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    const int64_t c = col_base + j * 32 + l32;
+                    b[j] = c < N ? __uint_as_float((uint32_t)bias[c] << 16) : 0.0f;
+                }
+            }
+            const int64_t rows_in = max((int64_t)0, min(M - row_base, (int64_t)WM));
+            const uint32_t row_bytes = (uint32_t)ldy * 2u;
+            const Rsrc out_r = make_rsrc(y + row_base * ldy + col_base, (uint32_t)rows_in * row_bytes);
+            const uint32_t voff = col_base + lane < N ? (uint32_t)lane * 2u : 0x80000000u;
+            typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+            typedef float f2 __attribute__((ext_vector_type(2)));
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int64_t row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
-                    if (row < M)
-                        yi[row * N + col] = (int32_t)acc[i][j][r];
+                    float v0 = out[i][0][r] + b[0];
+                    float v1 = out[i][1][r] + b[1];
+                    if constexpr (GELU) {
+                        v0 = gelu_tanh(v0);
+                        v1 = gelu_tanh(v1);
+                    }
+                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
+                                                                     __float_as_uint(v1), false, false);
+                    const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
+                    const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
+                    const uint32_t row0 = (uint32_t)(i * 32 + 8 * (r >> 2) + (r & 3));
+                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)pk, out_r, (int)voff,
+                                                          (int)(row0 * row_bytes), 0);
+                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(pk >> 16), out_r, (int)voff,
+                                                          (int)((row0 + 4) * row_bytes), 0);
                 }
             }
         }
-    } else {
-        // bias and activation per element, then one lane-half swap between the
-        // two column tiles: afterwards lane l holds column l of the wave's 64
-        // columns for one row (tile 0's rows in the first register, tile 1's
-        // khalf = 1 rows in the second), so every store covers a full 128-byte
-        // row segment; the pair is rounded to bf16 (RNE) by one conversion
-        static_assert(TN == 2, "the swap pairs the two column tiles");
-        float b[TN] = {0.0f, 0.0f};
-        if (bias) {
+    };
+
+    // Partial sums of a shared tile.  Each math wave handles its own 64 x 64
+    // region independently: it stores its registers to its slot (float4 runs
+    // in register order, 1 KB per instruction), waits until those stores are
+    // complete, and counts itself in the region's counter.  The wave that
+    // completes the count adds every contributor's slot in workgroup order,
+    // so the result does not depend on which one arrives last, resets the
+    // counter for the next call and writes the output.  Nobody waits for
+    // another wave.
+    // Coherence across the XCDs' separate L2 caches comes from the accesses
+    // themselves, not from fences: slot stores and loads carry the sc1 cache
+    // policy (device-coherent: the stores write through, the loads do not
+    // hit stale lines), the same instructions the compiler emits for relaxed
+    // device-scope atomic loads and stores, and the counter is a device-scope
+    // atomic.  A device-scope release / acquire fence would instead write back
+    // and invalidate the whole L2 of the XCD (buffer_wbl2 / buffer_inv),
+    // evicting the operands of every other workgroup on it.  Ordering: the
+    // stores are waited for (vmcnt) before the counter increment, and the
+    // finisher issues its loads only after the increment has returned.
+    constexpr int kRegionFloats = WM * WN;
+    constexpr int kCoherent = 16;      // sc1 cache-policy bit of buffer loads / stores
+    auto slot_rsrc = [&](int slot) {
+        return make_rsrc(slots + ((int64_t)slot * kMathWaves + wave) * kRegionFloats,
+                         kRegionFloats * (uint32_t)sizeof(float));
+    };
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    auto finish_partial = [&] {
+        if constexpr (SPLIT && !I32OUT) {
+            const uint32_t lane_off = (uint32_t)lane * 16u;
+            const Rsrc mine = slot_rsrc(cur.sg.slot);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int64_t c = n0 + wn * WN + j * 32 + l32;
-                b[j] = c < N ? __uint_as_float((uint32_t)bias[c] << 16) : 0.0f;
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const v4f v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                       acc[i][j][4 * q + 3]};
+                        __builtin_amdgcn_raw_buffer_store_b128(
+                            v, mine, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
+                    }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            uint32_t* ctr = counters + (int64_t)cur.sg.sk_tile * kMathWaves + wave;
+            uint32_t arrived = 0;
+            if (lane == 0)
+                arrived = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            arrived = __builtin_amdgcn_readfirstlane(arrived);
+            const GemmSchedule sch_ = fresh_schedule();
+            int32_t b_first, b_last;
+            sk_contributors(sch_, cur.sg.sk_tile, b_first, b_last);
+            if (arrived != (uint32_t)(b_last - b_first))
+                return;
+            asm volatile("" ::: "memory");
+            if (b_last - b_first == 1) {
+                // two contributors (the usual case): add the other one's slot
+                // to the registers; a + b == b + a in floating point, so the
+                // result is the same whichever of the two finishes
+                const int32_t other = b_first == blk ? b_last : b_first;
+                const Rsrc part = slot_rsrc(sk_slot(sch_, other, cur.sg.sk_tile));
+                v4f v[TM][TN][4];
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            v[i][j][q] = __builtin_amdgcn_raw_buffer_load_b128(
+                                part, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                acc[i][j][4 * q + e] += v[i][j][q][e];
+                if (lane == 0)
+                    __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                store_tile(acc);
+                return;
             }
-        }
-        const int64_t col = n0 + wn * WN + lane;
-        typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-        typedef float f2 __attribute__((ext_vector_type(2)));
+            // more contributors: acc = sum of their slots in workgroup order
+            // (this wave's own slot included, re-read: it holds the same values)
+            for (int32_t bb = b_first; bb <= b_last; ++bb) {
+                const Rsrc part = slot_rsrc(sk_slot(sch_, bb, cur.sg.sk_tile));
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+                for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float v0 = acc[i][0][r] + b[0];
-                float v1 = acc[i][1][r] + b[1];
-                if constexpr (GELU) {
-                    v0 = gelu_tanh(v0);
-                    v1 = gelu_tanh(v1);
-                }
-                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
-                                                                 __float_as_uint(v1), false, false);
-                const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
-                const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
-                const int64_t row0 = m0 + wm * WM + i * 32 + 8 * (r >> 2) + (r & 3);
-                const int64_t row1 = row0 + 4;
-                if (col < N) {
-                    if (row0 < M)
-                        y[row0 * ldy + col] = (uint16_t)pk;
-                    if (row1 < M)
-                        y[row1 * ldy + col] = (uint16_t)(pk >> 16);
-                }
+                    for (int j = 0; j < TN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const v4f v = __builtin_amdgcn_raw_buffer_load_b128(
+                                part, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                if (bb == b_first)
+                                    acc[i][j][4 * q + e] = v[e];
+                                else
+                                    acc[i][j][4 * q + e] += v[e];
+                            }
+                        }
             }
+            if (lane == 0)
+                __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            store_tile(acc);
         }
+    };
+
+    auto reset_tile = [&] {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    acc[i][j][r] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            p_last[r] = 0.0f;          // the "last tile" before a segment's first group adds 0
+            s_last[r] = 0.0f;
+        }
+    };
+
+    // Segment by segment: the first group's operands are read from LDS stage
+    // 0, the groups but the last run with the next group's prefetch, the last
+    // one prefetches nothing (so no operand is live across the output code),
+    // the no-op steps that round the segment up to whole 3-step rounds are
+    // barriers only, then the tile's output.  The decode waves meanwhile
+    // stage the next segment's first groups.
+    if (!cursor_begin(fresh_schedule(), blk, cur))
+        return;
+    lds_sync();
+    for (;;) {
+        const int L = cur.sg.g1 - cur.sg.g0;
+        set_fragment_indices();
+        reset_tile();
+        load_a(0, 0);
+        load_a(1, 0);
+        load_b(0, 0);
+        run_groups(L - 1);
+        compute((L - 1) % kStages, 0, std::integral_constant<bool, true>());
+        math_barrier();
+        for (int p = L; p < padded_steps(L); ++p)
+            math_barrier();
+        fma_tile(TM - 1, TN - 1, p_last, s_last);
+        set_fragment_indices();
+        if (!SPLIT || cur.sg.sk_tile < 0)
+            store_tile(acc);
+        else
+            finish_partial();
+        if (!cursor_next(fresh_schedule(), blk, cur))
+            break;
     }
 }
 
@@ -556,16 +766,29 @@ template <bool I32OUT, int GS>
 hipError_t launch_gs(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
                      const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                      int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue,
-                     hipStream_t stream)
+                     const GemmSchedule& sch, uint32_t* counters, float* slots, hipStream_t stream)
 {
-    const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
-    // the epilogue is a compile-time choice, so the plain kernel carries no GELU code
-    if (!I32OUT && epilogue == 1)
-        w4a4_gemm_kernel<GS, false, true><<<grid, dim3(kThreadsPerBlock), 0, stream>>>(
-            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy);
-    else
-        w4a4_gemm_kernel<GS, I32OUT, false><<<grid, dim3(kThreadsPerBlock), 0, stream>>>(
-            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy);
+    const dim3 grid((unsigned)sch.blocks), block(kThreadsPerBlock);
+    // the epilogue and the split part are compile-time choices, so the
+    // whole-tile plain kernel carries neither GELU nor partial-sum code
+    if constexpr (I32OUT) {
+        w4a4_gemm_kernel<GS, true, false, false><<<grid, block, 0, stream>>>(
+            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+    } else if (sch.sk_tiles > 0) {
+        if (epilogue == 1)
+            w4a4_gemm_kernel<GS, false, true, true><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+        else
+            w4a4_gemm_kernel<GS, false, false, true><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+    } else {
+        if (epilogue == 1)
+            w4a4_gemm_kernel<GS, false, true, false><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+        else
+            w4a4_gemm_kernel<GS, false, false, false><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+    }
     return hipGetLastError();
 }
 
@@ -573,41 +796,138 @@ template <bool I32OUT>
 hipError_t launch(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
                   const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                   int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group, int epilogue,
-                  hipStream_t stream)
+                  const GemmSchedule& sch, uint32_t* counters, float* slots, hipStream_t stream)
 {
     switch (lzs_group) {
     case 8:
         return launch_gs<I32OUT, 8>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                    epilogue, stream);
+                                    epilogue, sch, counters, slots, stream);
     case 16:
         return launch_gs<I32OUT, 16>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, stream);
+                                     epilogue, sch, counters, slots, stream);
     case 32:
         return launch_gs<I32OUT, 32>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, stream);
+                                     epilogue, sch, counters, slots, stream);
     default:
         return launch_gs<I32OUT, 64>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, stream);
+                                     epilogue, sch, counters, slots, stream);
     }
+}
+
+// Split only when it saves each workgroup at least kMinSplitSaving groups of
+// work on average (the idle part of the last round of whole tiles): below
+// that, the split's own costs (segments that start mid-tile, partial sums,
+// operands shared less well in L2) eat the gain.  With fewer tiles than
+// workgroups, every workgroup takes at least kMinSplitGroups groups and a
+// tile is shared by about kMaxSplitWays workgroups at most (each extra one
+// costs the finisher a slot read).
+constexpr int64_t kMinSplitSaving = 16;
+constexpr int64_t kMinSplitGroups = 4;
+constexpr int64_t kMaxSplitWays = 8;
+
+size_t counter_bytes(const GemmSchedule& s)
+{
+    return ((size_t)s.sk_tiles * kMathWaves * sizeof(uint32_t) + 255) / 256 * 256;
 }
 
 }  // namespace
 
+GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split)
+{
+    GemmSchedule s{};
+    const int64_t tiles_m = (M + BM - 1) / BM;
+    const int64_t tiles_n = (N + BN - 1) / BN;
+    const int64_t T = tiles_m * tiles_n;
+    const int64_t G = K / 64;
+    s.tiles_n = (int32_t)tiles_n;
+    s.groups = (int32_t)G;
+    if (blocks <= 0 || T <= 0 || G <= 0 || T > kMaxGemmTiles)
+        return s;                              // blocks == 0: nothing to launch
+    // whole tiles only: tile b + r * blocks for r = 0, 1, ...
+    s.blocks = (int32_t)std::min<int64_t>(blocks, T);
+    s.sk_first = (int32_t)T;
+    if (!split || T % blocks == 0)
+        return s;
+    const int64_t rounds = (T + blocks - 1) / blocks;
+    if ((rounds * blocks - T) * G < kMinSplitSaving * blocks)
+        return s;
+    int64_t sk_first, sk_blocks;
+    if (T > blocks) {
+        sk_first = (T / blocks - 1) * blocks;  // leaves between 1 and 2 rounds of tiles to split
+        sk_blocks = blocks;
+    } else {
+        sk_first = 0;
+        const int64_t min_units = std::max(kMinSplitGroups, (G + kMaxSplitWays - 1) / kMaxSplitWays);
+        sk_blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, T * G / min_units));
+    }
+    const int64_t units = (T - sk_first) * G;
+    if (units >= (int64_t(1) << 30))
+        return s;
+    s.blocks = (int32_t)(T > blocks ? blocks : sk_blocks);
+    s.sk_first = (int32_t)sk_first;
+    s.sk_tiles = (int32_t)(T - sk_first);
+    s.sk_blocks = (int32_t)sk_blocks;
+    s.sk_q = (int32_t)(units / sk_blocks);
+    s.sk_r = (int32_t)(units % sk_blocks);
+    return s;
+}
+
+size_t gemm_workspace_bytes(const GemmSchedule& s)
+{
+    if (s.sk_tiles == 0)
+        return 0;
+    return counter_bytes(s) + (size_t)2 * s.sk_blocks * kMathWaves * WM * WN * sizeof(float);
+}
+
+int gemm_resident_blocks()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 0;
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices];
+    if (dev < kMaxDevices) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0)
+            return c;
+    }
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true>),
+            kThreadsPerBlock, 0) != hipSuccess)
+        return 0;
+    const int n = cus * std::max(per_cu, 1);
+    if (dev < kMaxDevices)
+        cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
 hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                               const uint16_t* scales, const uint8_t* w_packed,
                               const uint16_t* bias, uint16_t* y, int64_t M, int64_t N, int64_t K,
-                              int64_t ldy, int lzs_group, int epilogue, hipStream_t stream)
+                              int64_t ldy, int lzs_group, int epilogue, const GemmSchedule& sch,
+                              void* workspace, hipStream_t stream)
 {
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    uint32_t* counters = static_cast<uint32_t*>(workspace);
+    float* slots = sch.sk_tiles > 0
+                       ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(sch))
+                       : nullptr;
     return launch<false>(codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
-                         epilogue, stream);
+                         epilogue, sch, counters, slots, stream);
 }
 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream)
 {
+    const GemmSchedule sch = gemm_schedule(M, N, K, gemm_resident_blocks(), false);
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
     return launch<true>(codes, flags, nullptr, w_packed, nullptr, nullptr, acc, M, N, K, N,
-                        lzs_group, 0, stream);
+                        lzs_group, 0, sch, nullptr, nullptr, stream);
 }
 
 }  // namespace quartz

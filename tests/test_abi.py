@@ -113,7 +113,8 @@ def test_linear_validation(lib):
     assert call(M=0) == OK
     assert call(N=0) == OK
     assert call(K=1 << 21) == ESHAPE
-    assert call(M=65535 * 256 + 1, K=64) == ESHAPE          # grid.y limit of 65535 tiles
+    # more than 2^31 - 1 output tiles of 256 x 128
+    assert call(M=1 << 28, N=1 << 28, ldy=1 << 28, K=64) == ESHAPE
     assert call(N=(1 << 24) + 1, ldy=(1 << 24) + 1, K=1024) == ESHAPE
 
 

@@ -85,6 +85,9 @@ def test_full_size_layer(cfg, layer):
     qa = q.quantize_act(to_dev_bf16(xb), GS)
     pw = q.pack_weight(to_dev_bf16(wb))
     y = q.w4a4_linear(qa, pw, to_dev_bf16(bias), L.epilogue)
+    # the workspace entry point, as bench.py times it
+    ws = q.gemm_workspace(L.M, L.N, L.K, "cuda")
+    y_ws = q.w4a4_linear(qa, pw, to_dev_bf16(bias), L.epilogue, workspace=ws)
     acc = q.w4a4_gemm_i32(qa, pw)
     torch.cuda.synchronize()
 
@@ -96,6 +99,7 @@ def test_full_size_layer(cfg, layer):
     got_i = acc[rows.tolist()][:, cols.tolist()].cpu().numpy()
     np.testing.assert_array_equal(got_i, oracle.gemm_i32(a_ref, wq_ref))
     _check_outputs(y, rows, cols, a_ref, wq_ref, sw_ref, bias[cols], L.epilogue, L.K)
+    _check_outputs(y_ws, rows, cols, a_ref, wq_ref, sw_ref, bias[cols], L.epilogue, L.K)
 
 
 def test_full_size_flux_mlp_pipeline():
@@ -113,7 +117,8 @@ def test_full_size_flux_mlp_pipeline():
     pw1 = q.pack_weight(to_dev_bf16(w1))
     pw2 = q.pack_weight(to_dev_bf16(w2))
     qa1 = q.quantize_act(to_dev_bf16(x1), GS)
-    y1 = q.w4a4_linear(qa1, pw1, to_dev_bf16(b1), 1)
+    y1 = q.w4a4_linear(qa1, pw1, to_dev_bf16(b1), 1,
+                       workspace=q.gemm_workspace(L1.M, L1.N, L1.K, "cuda"))
     torch.cuda.synchronize()
 
     rows = sample_idx(L1.M, 24, 401, 256)
@@ -129,7 +134,8 @@ def test_full_size_flux_mlp_pipeline():
     x2_rows = oracle.to_bf16_bits(y1_64)
     y1[rows.tolist()] = to_dev_bf16(x2_rows)
     qa2 = q.quantize_act(y1, GS)
-    y2 = q.w4a4_linear(qa2, pw2, to_dev_bf16(b2), 0)
+    y2 = q.w4a4_linear(qa2, pw2, to_dev_bf16(b2), 0,
+                       workspace=q.gemm_workspace(L2.M, L2.N, L2.K, "cuda"))
     torch.cuda.synchronize()
     a2_ref = oracle.quantize_act(x2_rows, GS)
     _check_act_rows(qa2, rows, a2_ref)
