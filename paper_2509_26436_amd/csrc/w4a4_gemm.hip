@@ -537,6 +537,18 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
 
     GemmCursor cur;
     const int32_t blk = (int32_t)blockIdx.x;
+    // this lane's bias values of the current tile (bf16 bits), loaded when the
+    // segment starts so that the output code does not wait for them
+    uint16_t bias_bits[TN];
+    auto load_bias = [&] {
+        if constexpr (!I32OUT) {
+            const Rsrc rb = make_rsrc(bias, bias ? (uint32_t)(N * 2) : 0u);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bias_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(
+                    rb, (int)(((int64_t)cur.tn * BN + wn * WN + j * 32 + l32) * 2), 0, 0);
+        }
+    };
     // ---- output.  Lane l holds column l % 32 of each 32 x 32 tile, rows
     // 8 (r/4) + 4 khalf + r%4 of register r.
     auto store_tile = [&](const v16f (&out)[TM][TN]) {
@@ -569,14 +581,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             static_assert(TN == 2, "the swap pairs the two column tiles");
             const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
             const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
-            float b[TN] = {0.0f, 0.0f};
-            if (bias) {
+            float b[TN];
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    const int64_t c = col_base + j * 32 + l32;
-                    b[j] = c < N ? __uint_as_float((uint32_t)bias[c] << 16) : 0.0f;
-                }
-            }
+            for (int j = 0; j < TN; ++j)
+                b[j] = __uint_as_float((uint32_t)bias_bits[j] << 16);
             const int64_t rows_in = max((int64_t)0, min(M - row_base, (int64_t)WM));
             const uint32_t row_bytes = (uint32_t)ldy * 2u;
             const Rsrc out_r = make_rsrc(y + row_base * ldy + col_base, (uint32_t)rows_in * row_bytes);
@@ -742,6 +750,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     for (;;) {
         const int L = cur.sg.g1 - cur.sg.g0;
         set_fragment_indices();
+        load_bias();
         reset_tile();
         load_a(0, 0);
         load_a(1, 0);
