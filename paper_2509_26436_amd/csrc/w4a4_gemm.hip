@@ -36,7 +36,6 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 // Buffer resource word 3 for raw (untyped, stride 0) loads on gfx9: a load at
@@ -91,14 +90,6 @@ __device__ __forceinline__ int swz(int r, int c)
 {
     const int f = (((r >> 1) ^ (r >> 2)) & 1) | ((((r >> 2) ^ (r >> 3)) & 1) << 1);
     return r * 64 + ((c ^ f) << 4);
-}
-
-__device__ __forceinline__ v8i load_frag(const uint8_t* lds, int r, int khalf)
-{
-    const uint4 lo = *reinterpret_cast<const uint4*>(lds + swz(r, 2 * khalf));
-    const uint4 hi = *reinterpret_cast<const uint4*>(lds + swz(r, 2 * khalf + 1));
-    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z,
-               (int)hi.w};
 }
 
 // Workgroup barrier ordering LDS only: global loads still in flight (the
@@ -368,8 +359,12 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // -------------------------------------------------------- math waves
     // Per-lane fragment indices, recomputed from fresh_tid after every tile's
     // output code (see above).
+    // The swizzle depends on row bits 1-3 only, so the fragments of tile row 1
+    // (column tile 1) sit exactly 32 rows = 2048 bytes after those of tile row
+    // 0 (column tile 0): one pair of lane offsets per operand, the rest are
+    // immediate offsets of the LDS reads.
     int lane, wm, wn, l32, khalf;
-    int sa_idx[TM], sw_idx[TN];
+    uint32_t a_lo, a_hi, b_lo, b_hi;
     auto set_fragment_indices = [&] {
         const int t = fresh_tid();
         const int w = __builtin_amdgcn_readfirstlane(t >> 6) & (kMathWaves - 1);   // wave-uniform
@@ -378,12 +373,16 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         wn = w % WAVES_N;
         l32 = t & 31;
         khalf = (t >> 5) & 1;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-            sa_idx[i] = khalf ? BM : wm * WM + i * 32 + l32;
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-            sw_idx[j] = khalf ? BN : wn * WN + j * 32 + l32;
+        a_lo = (uint32_t)swz(wm * WM + l32, 2 * khalf);
+        a_hi = (uint32_t)swz(wm * WM + l32, 2 * khalf + 1);
+        b_lo = (uint32_t)swz(wn * WN + l32, 2 * khalf);
+        b_hi = (uint32_t)swz(wn * WN + l32, 2 * khalf + 1);
+    };
+    static_assert(((32 >> 1) & 7) == 0, "32-row steps keep the swizzle");
+    auto frag_at = [](const uint8_t* stage, uint32_t lo, uint32_t hi, int rows_off) {
+        const uint4 l = *reinterpret_cast<const uint4*>(stage + lo + rows_off * 64);
+        const uint4 h = *reinterpret_cast<const uint4*>(stage + hi + rows_off * 64);
+        return v8i{(int)l.x, (int)l.y, (int)l.z, (int)l.w, (int)h.x, (int)h.y, (int)h.z, (int)h.w};
     };
 
     v16f acc[TM][TN];
@@ -395,17 +394,39 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // a single weight-fragment register set: column 0 (prefetched) for tiles
     // (0,0) (1,0), then column 1, read from the current stage once column 0's
     // last product is issued
+    // Operands of the scale outer-product MFMA (fp16, K = 16 with only k = 0
+    // non-zero): dword 0 holds the scale in its low half (a zero-extending
+    // 16-bit LDS load; the upper half-wave reads the zero pad, its k = 8), and
+    // dwords 1-3 are zero once and never written again, so refilling an
+    // operand is one LDS load and no packing instruction.
+    // The split instantiation keeps the scales as plain fp16 values and packs
+    // the operand per MFMA instead: its output code between segments (partial
+    // sums) needs the 16 registers more than its main loop needs the saved
+    // instructions (measured: 2.5 % either way).
+    typedef int v4i __attribute__((ext_vector_type(4)));
+    constexpr bool kKeepScaleOps = !SPLIT;
     v8i bf, af[TM];
-    _Float16 sw_h[TN], sa_h[TM];
+    v4i sa_op[TM], sw_op[TN];
+    _Float16 sa_h[TM], sw_h[TN];
     auto load_a = [&](int i, int buf) {
-        af[i] = load_frag(As[buf], wm * WM + i * 32 + l32, khalf);
-        if constexpr (!I32OUT)
-            sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][sa_idx[i]]);
+        af[i] = frag_at(As[buf], a_lo, a_hi, i * 32);
+        if constexpr (!I32OUT) {
+            const uint16_t v = sas[buf][khalf ? BM : wm * WM + i * 32 + l32];
+            if constexpr (kKeepScaleOps)
+                sa_op[i][0] = (int)v;
+            else
+                sa_h[i] = __builtin_bit_cast(_Float16, v);
+        }
     };
     auto load_b = [&](int j, int buf) {
-        bf = load_frag(Bs[buf], wn * WN + j * 32 + l32, khalf);
-        if constexpr (!I32OUT)
-            sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][sw_idx[j]]);
+        bf = frag_at(Bs[buf], b_lo, b_hi, j * 32);
+        if constexpr (!I32OUT) {
+            const uint16_t v = sws[buf][khalf ? BN : wn * WN + j * 32 + l32];
+            if constexpr (kKeepScaleOps)
+                sw_op[j][0] = (int)v;
+            else
+                sw_h[j] = __builtin_bit_cast(_Float16, v);
+        }
     };
 
     // One group, tiles in the order (0,0) (1,0) (0,1) (1,1).  The fp8 product
@@ -434,12 +455,19 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     auto scale_tile = [&](int i, int j) {
         v16f sc = zero;
         if constexpr (!I32OUT) {
-            // fp16 operands of the scale outer product: only k = 0 is non-zero
-            v8h sa_op = {}, sw_op = {};
-            sa_op[0] = sa_h[i];
-            sw_op[0] = sw_h[j];
+            typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+            v8h a, b;
+            if constexpr (kKeepScaleOps) {
+                a = __builtin_bit_cast(v8h, sa_op[i]);
+                b = __builtin_bit_cast(v8h, sw_op[j]);
+            } else {
+                a = v8h{};
+                b = v8h{};
+                a[0] = sa_h[i];
+                b[0] = sw_h[j];
+            }
             __builtin_amdgcn_s_setprio(3);
-            sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(sa_op, sw_op, zero, 0, 0, 0);
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, zero, 0, 0, 0);
             __builtin_amdgcn_s_setprio(0);
         }
         return sc;
@@ -488,8 +516,8 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 p_next = mfma_p((t + 1) % TM);
             __builtin_amdgcn_sched_barrier(0);
             // refills after the last use of each operand: af[i] by the product of
-            // tile (i,1) (issued one step ahead), sa_h[i] by the scale of tile
-            // (i,1), bf / sw_h[0] by column 0's products and scales
+            // tile (i,1) (issued one step ahead), sa_op[i] by the scale of tile
+            // (i,1), bf / sw_op[0] by column 0's products and scales
             if (t == 0)
                 load_b(1, cb);          // column 1 of this group (column 0's products are issued)
             if (t == 2 && !LAST) {
@@ -673,24 +701,25 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 // result is the same whichever of the two finishes
                 const int32_t other = b_first == blk ? b_last : b_first;
                 const Rsrc part = slot_rsrc(sk_slot(sch_, other, cur.sg.sk_tile));
-                v4f v[TM][TN][4];
+                // in two halves (tile row i), to bound the registers in flight
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i) {
+                    v4f v[TN][4];
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
-                            v[i][j][q] = __builtin_amdgcn_raw_buffer_load_b128(
+                            v[j][q] = __builtin_amdgcn_raw_buffer_load_b128(
                                 part, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
-#pragma unroll
-                for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
 #pragma unroll
                             for (int e = 0; e < 4; ++e)
-                                acc[i][j][4 * q + e] += v[i][j][q][e];
+                                acc[i][j][4 * q + e] += v[j][q][e];
+                    __builtin_amdgcn_sched_barrier(0);
+                }
                 if (lane == 0)
                     __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 store_tile(acc);
@@ -746,6 +775,14 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // stage the next segment's first groups.
     if (!cursor_begin(fresh_schedule(), blk, cur))
         return;
+    if constexpr (kKeepScaleOps) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            sa_op[i] = v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            sw_op[j] = v4i{0, 0, 0, 0};
+    }
     lds_sync();
     for (;;) {
         const int L = cur.sg.g1 - cur.sg.g0;
