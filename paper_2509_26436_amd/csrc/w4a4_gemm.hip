@@ -664,7 +664,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     constexpr int kRegionFloats = WM * WN;
     constexpr int kCoherent = 16;      // sc1 cache-policy bit of buffer loads / stores
     auto slot_rsrc = [&](int slot) {
-        return make_rsrc(slots + ((int64_t)slot * kMathWaves + wave) * kRegionFloats,
+        return make_rsrc(slots + ((int64_t)slot * kMathWaves + uwave) * kRegionFloats,
                          kRegionFloats * (uint32_t)sizeof(float));
     };
     typedef float v4f __attribute__((ext_vector_type(4)));
@@ -684,7 +684,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                             v, mine, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
                     }
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            uint32_t* ctr = counters + (int64_t)cur.sg.sk_tile * kMathWaves + wave;
+            uint32_t* ctr = counters + (int64_t)cur.sg.sk_tile * kMathWaves + uwave;
             uint32_t arrived = 0;
             if (lane == 0)
                 arrived = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
