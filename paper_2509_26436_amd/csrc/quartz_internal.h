@@ -86,20 +86,6 @@ struct Fp8Table {
 constexpr uint32_t kTabLo = 0x44403800u;
 constexpr uint32_t kTabHi = 0x4E4C4A48u;
 
-// Table for flag byte i (0..3) of `flags8`, a word whose bytes hold 8 * FLAG:
-// the byte is replicated with v_perm_b32 (selector 0x0C yields 0x00, which
-// keeps the entry of magnitude 0 at zero) and added to the exponent fields.
-template <int I>
-__device__ __forceinline__ Fp8Table fp8_table(uint32_t flags8)
-{
-    constexpr uint32_t rep = 0x01010101u * I;
-    constexpr uint32_t rep_lo = (0x01010100u * I) | 0x0Cu;
-    Fp8Table t;
-    t.lo = kTabLo + __builtin_amdgcn_perm(0u, flags8, rep_lo);
-    t.hi = kTabHi + __builtin_amdgcn_perm(0u, flags8, rep);
-    return t;
-}
-
 __device__ __forceinline__ uint2 decode_nibbles_fp8(uint32_t w, Fp8Table t)
 {
     const uint32_t mag_even = w & 0x07070707u;

@@ -101,9 +101,9 @@ __device__ __forceinline__ void lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// The 64 / GS flag bytes of one (group, row), loaded as is; expanded to
-// 8 * FLAG per 8-element word (words 0-3 in `lo`, 4-7 in `hi`, one per byte)
-// only when the group is decoded, so the prefetch never waits for them.
+// The 64 / GS flag bytes of one (group, row), loaded as is and turned into
+// decode tables only when the group is decoded, so the prefetch never waits
+// for them.
 template <int GS>
 using FlagRaw = typename std::conditional<GS == 8, uint2,
                 typename std::conditional<GS == 16, uint32_t, uint16_t>::type>::type;
@@ -121,25 +121,31 @@ __device__ __forceinline__ FlagRaw<GS> load_flags_raw(Rsrc r, uint32_t off)
         return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
 }
 
-template <int GS>
-__device__ __forceinline__ uint2 expand_flags8(FlagRaw<GS> raw)
+// The decode table of flag k (byte k of the raw flags: bytes 0-3 in `lo`, 4-7
+// in `hi`): FLAG replicated into every byte by one v_perm_b32 (selector 0x0C
+// yields 0x00, which keeps the entry of magnitude 0 at zero), then shifted
+// into the e4m3 exponent field and added to the base table in one
+// v_lshl_add_u32 per dword (FLAG <= 4, so 8 FLAG stays inside its byte and
+// no entry carries into the next).
+template <int K>
+__device__ __forceinline__ Fp8Table fp8_table_raw(uint32_t lo, uint32_t hi)
 {
-    uint2 f;
-    if constexpr (GS == 8) {
-        f = raw;
-    } else if constexpr (GS == 16) {
-        f.x = __builtin_amdgcn_perm(0u, raw, 0x01010000u);
-        f.y = __builtin_amdgcn_perm(0u, raw, 0x03030202u);
-    } else if constexpr (GS == 32) {
-        f.x = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x00000000u);
-        f.y = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x01010101u);
-    } else {
-        f.x = __builtin_amdgcn_perm(0u, (uint32_t)raw, 0x00000000u);
-        f.y = f.x;
-    }
-    f.x <<= 3;      // FLAG <= 4, so 8 * FLAG stays inside its byte
-    f.y <<= 3;
-    return f;
+    static_assert(K >= 0 && K < 8, "flag byte");
+    constexpr uint32_t rep = 0x01010101u * K;
+    constexpr uint32_t rep_lo = (0x01010100u * K) | 0x0Cu;
+    Fp8Table t;
+    t.lo = (__builtin_amdgcn_perm(hi, lo, rep_lo) << 3) + kTabLo;
+    t.hi = (__builtin_amdgcn_perm(hi, lo, rep) << 3) + kTabHi;
+    return t;
+}
+
+template <int GS>
+__device__ __forceinline__ uint2 flags_dwords(FlagRaw<GS> raw)
+{
+    if constexpr (GS == 8)
+        return raw;
+    else
+        return uint2{(uint32_t)raw, 0u};
 }
 
 // Decode roles (decode thread d = tid - 512, 0..255): A row d (32 code bytes,
@@ -277,10 +283,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         };
         // decode one group into LDS buffer `buf`
         auto stage = [&](const Raw& r, int buf) {
-            const uint2 fl8 = expand_flags8<GS>(r.f);
+            const uint2 fr = flags_dwords<GS>(r.f);
             const uint32_t a[8] = {r.a0.x, r.a0.y, r.a0.z, r.a0.w, r.a1.x, r.a1.y, r.a1.z, r.a1.w};
             constexpr int kWordsPerFlag = GS / 8;
-            Fp8Table t = fp8_table<0>(fl8.x);
+            Fp8Table t = fp8_table_raw<0>(fr.x, fr.y);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 uint2 w[2];
@@ -288,12 +294,14 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 for (int h = 0; h < 2; ++h) {
                     const int wi = 2 * c + h;           // word index 0..7
                     if (wi % kWordsPerFlag == 0 && wi > 0) {
-                        const uint32_t f = wi < 4 ? fl8.x : fl8.y;
-                        switch (wi & 3) {
-                        case 0: t = fp8_table<0>(f); break;
-                        case 1: t = fp8_table<1>(f); break;
-                        case 2: t = fp8_table<2>(f); break;
-                        default: t = fp8_table<3>(f); break;
+                        switch (wi / kWordsPerFlag) {      // flag index, 1..7
+                        case 1: t = fp8_table_raw<1>(fr.x, fr.y); break;
+                        case 2: t = fp8_table_raw<2>(fr.x, fr.y); break;
+                        case 3: t = fp8_table_raw<3>(fr.x, fr.y); break;
+                        case 4: t = fp8_table_raw<4>(fr.x, fr.y); break;
+                        case 5: t = fp8_table_raw<5>(fr.x, fr.y); break;
+                        case 6: t = fp8_table_raw<6>(fr.x, fr.y); break;
+                        default: t = fp8_table_raw<7>(fr.x, fr.y); break;
                         }
                     }
                     w[h] = decode_nibbles_fp8(a[wi], t);
