@@ -76,6 +76,8 @@ def _load():
     lib.qo_linear_f64_sampled.argtypes = [P, P, P, P, P, P, I64, I32, I32, I32,
                                           P, P, I64, P, P]
     lib.qo_linear_f64_sampled.restype = I32
+    lib.qo_round_bf16.argtypes = [P, I64, P]
+    lib.qo_round_bf16.restype = None
     lib.qo_num_threads.argtypes = []
     lib.qo_num_threads.restype = I32
     _lib = lib
@@ -285,3 +287,22 @@ def to_bf16_bits(y64: np.ndarray) -> np.ndarray:
     """Expected bf16 output bits (RNE) of float64 values."""
     f = np.vectorize(lambda v: _load().qo_f64_to_bf16_rne(float(v)), otypes=[np.uint16])
     return f(y64)
+
+
+def round_bf16(y64: np.ndarray) -> np.ndarray:
+    """bf16 bits (RNE) of float64 values, same shape; the array form of
+    f64_to_bf16_rne."""
+    v = _c(y64, np.float64)
+    out = np.empty(v.shape, np.uint16)
+    _load().qo_round_bf16(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def linear_quantize(a: ActQuant, wq: np.ndarray, sw: np.ndarray, bias_bits=None,
+                    epilogue: int = 0, out_lzs_group: int = 16) -> ActQuant:
+    """The layer's output as the next layer's quantized input: the bf16
+    output y (linear_f64 rounded to bf16, the value the layer stores) run
+    through the activation quantizer with K = N (Eq. 1 and Eq. 2 applied on
+    the fly to the producing layer's result, Appendix C)."""
+    y64, _ = linear_f64(a, wq, sw, bias_bits, epilogue)
+    return quantize_act(round_bf16(y64), out_lzs_group)

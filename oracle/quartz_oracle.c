@@ -455,6 +455,17 @@ int qo_linear_f64_sampled(const int8_t* c, const uint8_t* flags, const uint16_t*
     return QO_OK;
 }
 
+/*
+ * bf16 bit patterns (round to nearest even) of n float64 values: the bf16
+ * output a layer stores for its float64 results, elementwise.
+ */
+void qo_round_bf16(const double* v, int64_t n, uint16_t* out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = qo_f64_to_bf16_rne(v[i]);
+}
+
 /* Number of threads the OpenMP loops above use. */
 #ifdef _OPENMP
 #include <omp.h>
