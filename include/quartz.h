@@ -165,6 +165,40 @@ quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * W4A4 linear layer whose output is quantized on the fly for the next layer
+ * (Appendix C applies the 4-bit compression on the fly; Eq. 1 and Eq. 2 as
+ * for quartz_quantize_act): the bf16 values quartz_w4a4_linear_ws would
+ * store, y[m][n] = bf16(act(sum_g s_a s_w P_g + bias[n])), are not written;
+ * instead the epilogue quantizes each row's 64-column groups of y exactly as
+ * quartz_quantize_act does with K = N (same codes, flags and scales,
+ * bit for bit, as quantizing the stored bf16 output), and writes them in
+ * quartz_quantize_act's layout.  This removes the bf16 round trip through
+ * memory between two layers (the producer's store and the quantizer's load).
+ *
+ *   codes ... epilogue   as for quartz_w4a4_linear (K % 64 == 0).
+ *   N             the next layer's K: N % 64 == 0 (QUARTZ_ERR_SHAPE otherwise).
+ *   out_lzs_group the next layer's G_s: 8, 16, 32 or 64.
+ *   out_mode      QUARTZ_MODE_SYMMETRIC.
+ *   out_codes     u8  [N/64][M][32]
+ *   out_flags     u8  [N/64][M][64/out_lzs_group]
+ *   out_scales    u16 [N/64][M]
+ *   out_zeros     i8  [N/64][M] or NULL (written as 0).
+ *   workspace, workspace_bytes   as for quartz_w4a4_linear_ws (NULL, 0: no
+ *                 split tiles); the values do not depend on it beyond the
+ *                 fp32 summation order of quartz_w4a4_linear_ws.
+ * M = 0 or N = 0 returns QUARTZ_OK without launching.
+ */
+quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* flags,
+                                          const uint16_t* scales, const int8_t* zeros,
+                                          const void* w_packed, const void* bias_bf16, int64_t M,
+                                          int64_t N, int64_t K, int32_t group_size,
+                                          int32_t lzs_group, int32_t epilogue,
+                                          int32_t out_lzs_group, int32_t out_mode,
+                                          uint8_t* out_codes, uint8_t* out_flags,
+                                          uint16_t* out_scales, int8_t* out_zeros, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Test / inspection helpers.
  *
  * quartz_unpack_weight: int8 [N][K] weight codes wq recovered from w_packed.

@@ -20,8 +20,9 @@ __all__ = [
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
-    "quartz_status_string", "QuantizedAct", "PackedWeight",
-    "quantize_act", "pack_weight", "w4a4_linear", "gemm_workspace", "linear_schedule",
+    "quartz_w4a4_linear_quantize", "quartz_status_string", "QuantizedAct", "PackedWeight",
+    "quantize_act", "pack_weight", "w4a4_linear", "w4a4_linear_quantize", "gemm_workspace",
+    "linear_schedule",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
 ]
 
@@ -38,7 +39,7 @@ EXPORTED_SYMBOLS = (
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
-    "quartz_status_string",
+    "quartz_w4a4_linear_quantize", "quartz_status_string",
 )
 
 
@@ -79,6 +80,9 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_linear_ws.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32,
                                           P, SZ, P]
     lib.quartz_w4a4_linear_ws.restype = I32
+    lib.quartz_w4a4_linear_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32,
+                                                I32, I32, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.quartz_w4a4_linear_quantize.restype = I32
     lib.quartz_w4a4_linear_schedule.argtypes = [I64, I64, I64, I32, I32, P, P, I64]
     lib.quartz_w4a4_linear_schedule.restype = I64
     lib.quartz_unpack_weight.argtypes = [P, I64, I64, I32, P, P]
@@ -127,6 +131,16 @@ def quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, 
     return load().quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, K,
                                         ldy, group_size, lzs_group, epilogue, workspace,
                                         workspace_bytes, stream)
+
+
+def quartz_w4a4_linear_quantize(codes, flags, scales, zeros, w_packed, bias, M, N, K,
+                                group_size, lzs_group, epilogue, out_lzs_group, out_mode,
+                                out_codes, out_flags, out_scales, out_zeros, workspace,
+                                workspace_bytes, stream) -> int:
+    return load().quartz_w4a4_linear_quantize(codes, flags, scales, zeros, w_packed, bias, M, N,
+                                              K, group_size, lzs_group, epilogue, out_lzs_group,
+                                              out_mode, out_codes, out_flags, out_scales,
+                                              out_zeros, workspace, workspace_bytes, stream)
 
 
 def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
@@ -256,6 +270,40 @@ def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI
                                    workspace.numel() * workspace.element_size(),
                                    _stream_handle(stream))
         _check(st, "quartz_w4a4_linear_ws")
+    return out
+
+
+def _empty_act(M: int, K: int, lzs_group: int, with_zeros: bool, device) -> QuantizedAct:
+    torch = _torch()
+    G = K // GROUP
+    return QuantizedAct(
+        codes=torch.empty((G, M, 32), dtype=torch.uint8, device=device),
+        flags=torch.empty((G, M, GROUP // lzs_group), dtype=torch.uint8, device=device),
+        scales=torch.empty((G, M), dtype=torch.int16, device=device),
+        zeros=torch.empty((G, M), dtype=torch.int8, device=device) if with_zeros else None,
+        M=M, K=K, lzs_group=lzs_group)
+
+
+def w4a4_linear_quantize(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI_NONE,
+                         out_lzs_group: int = 16, with_zeros: bool = False,
+                         out: QuantizedAct | None = None, stream=None, workspace=None):
+    """The layer's output quantized for the next layer (quartz_w4a4_linear_quantize): a
+    QuantizedAct with M = a.M rows and K = w.N (w.N % 64 == 0), equal to
+    ``quantize_act(w4a4_linear(a, w, ...), out_lzs_group)``."""
+    torch = _torch()
+    if a.K != w.K:
+        raise ValueError("K mismatch between activations and weights")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out is None:
+        out = _empty_act(a.M, w.N, out_lzs_group, with_zeros, a.codes.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_w4a4_linear_quantize(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                                     _ptr(w.data), _ptr(bias), a.M, w.N, a.K, GROUP, a.lzs_group,
+                                     epilogue, out.lzs_group, MODE_SYMMETRIC, _ptr(out.codes),
+                                     _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),
+                                     _ptr(workspace), nbytes, _stream_handle(stream))
+    _check(st, "quartz_w4a4_linear_quantize")
     return out
 
 

@@ -145,26 +145,33 @@ static quartz_status check_gemm(const uint8_t* codes, const uint8_t* flags, cons
     return QUARTZ_OK;
 }
 
+// qout == nullptr: bf16 output y_bf16 [M][ldy]; otherwise the output goes
+// to qout (quantized for the next layer) and y_bf16 / ldy are not used
 static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
                                  const uint16_t* scales, const void* w_packed,
                                  const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
                                  int64_t K, int64_t ldy, int32_t group_size, int32_t lzs_group,
                                  int32_t epilogue, void* workspace, size_t workspace_bytes,
-                                 hipStream_t stream)
+                                 const quartz::QuantOut* qout, hipStream_t stream)
 {
     if (epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH)
         return QUARTZ_ERR_UNSUPPORTED;
     quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, group_size, lzs_group);
     if (st != QUARTZ_OK)
         return st;
-    if (ldy < N || ldy > kMaxLd)
+    if (!qout && (ldy < N || ldy > kMaxLd))
         return QUARTZ_ERR_SHAPE;
+    if (qout && N % 64 != 0)
+        return QUARTZ_ERR_SHAPE;        // the output is the next layer's K
     if (M == 0 || N == 0)
         return QUARTZ_OK;
-    if (!scales || !y_bf16)
+    if (!scales || (!qout && !y_bf16) ||
+        (qout && (!qout->codes || !qout->flags || !qout->scales)))
         return QUARTZ_ERR_NULL;
-    if (!aligned16(scales) || !aligned16(y_bf16) || (bias_bf16 && !aligned16(bias_bf16)) ||
-        (workspace && !aligned16(workspace)))
+    if (!aligned16(scales) || (!qout && !aligned16(y_bf16)) ||
+        (bias_bf16 && !aligned16(bias_bf16)) || (workspace && !aligned16(workspace)) ||
+        (qout && (!aligned16(qout->codes) || !aligned16(qout->flags) ||
+                  !aligned16(qout->scales) || (qout->zeros && !aligned16(qout->zeros)))))
         return QUARTZ_ERR_ALIGN;
     const quartz::GemmSchedule sch =
         quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
@@ -175,7 +182,7 @@ static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
     return from_hip(quartz::launch_w4a4_linear(
         codes, flags, scales, static_cast<const uint8_t*>(w_packed),
         static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
-        lzs_group, epilogue, sch, workspace, stream));
+        lzs_group, epilogue, sch, workspace, qout ? *qout : quartz::QuantOut{}, stream));
 }
 
 quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
@@ -187,7 +194,7 @@ quartz_status quartz_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
 {
     (void)zeros;   // the symmetric mode has zero points 0 by construction
     return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
-                       group_size, lzs_group, epilogue, nullptr, 0, stream);
+                       group_size, lzs_group, epilogue, nullptr, 0, nullptr, stream);
 }
 
 size_t quartz_w4a4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t group_size)
@@ -207,7 +214,29 @@ quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
 {
     (void)zeros;
     return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
-                       group_size, lzs_group, epilogue, workspace, workspace_bytes, stream);
+                       group_size, lzs_group, epilogue, workspace, workspace_bytes, nullptr,
+                       stream);
+}
+
+quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* flags,
+                                          const uint16_t* scales, const int8_t* zeros,
+                                          const void* w_packed, const void* bias_bf16, int64_t M,
+                                          int64_t N, int64_t K, int32_t group_size,
+                                          int32_t lzs_group, int32_t epilogue,
+                                          int32_t out_lzs_group, int32_t out_mode,
+                                          uint8_t* out_codes, uint8_t* out_flags,
+                                          uint16_t* out_scales, int8_t* out_zeros, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream)
+{
+    (void)zeros;
+    if (!lzs_ok(out_lzs_group) || out_mode != QUARTZ_MODE_SYMMETRIC)
+        return QUARTZ_ERR_UNSUPPORTED;
+    // the output is the next layer's activation with K = N
+    if (!size_ok(M, N))
+        return QUARTZ_ERR_SHAPE;
+    const quartz::QuantOut q{out_codes, out_flags, out_scales, out_zeros, out_lzs_group};
+    return linear_impl(codes, flags, scales, w_packed, bias_bf16, nullptr, M, N, K, 0,
+                       group_size, lzs_group, epilogue, workspace, workspace_bytes, &q, stream);
 }
 
 int64_t quartz_w4a4_linear_schedule(int64_t M, int64_t N, int64_t K, int32_t blocks,

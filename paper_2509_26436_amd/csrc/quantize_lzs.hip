@@ -13,31 +13,16 @@
 // small per-lane offset; rows past M fall outside the resource range, so
 // their loads read zero and their stores are dropped.
 //
-// Per group:  alpha = max|x| (exact, 8-lane DPP max)
-//             s = fp16_rne_sat(alpha * fp32(1/127)), r = 1/s
-//             |q| = min(rne(fp32(|x| * r)), 127)     (sign kept aside;
-//                   the clamp only binds for subnormal or saturated s)
-// Per subgroup of G_s: FLAG = max(29 - clz(OR |q|), 0)   (DPP OR across lanes)
-//                      c = sgn * (|q| >> FLAG)           (truncation toward 0)
-// Two exact shortcuts, both checked over their whole input domain:
-//  - fp16_rne(alpha * fp32(1/127)) equals fp16_rne(fp32(alpha / 127)) for every
-//    finite bf16 alpha (alpha / 127 is never within an fp32 ulp of an fp16
-//    rounding boundary);
-//  - one Newton step on the hardware reciprocal, r0 + r0 * (1 - s * r0) with
-//    fused multiply-adds, equals the IEEE quotient 1/s for every finite fp16 s.
-// rne(p) for 0 <= p < 2^22 is read from the low bits of fp32(p + 1.5 * 2^23):
-// that sum has an ulp of 1, so its rounding is round-half-even of p.
+// Per group:  alpha = max|x| (exact, 8-lane DPP max), then Stage 1 and the
+// per-subgroup Stage 2 of lzs_device.h, the subgroup OR taken across the
+// lanes of a subgroup with DPP.
+#include "lzs_device.h"
 #include "quartz_internal.h"
 
 namespace quartz {
 namespace {
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
-typedef unsigned short us2 __attribute__((ext_vector_type(2)));
-
-constexpr float kMagic = 12582912.0f;          // 1.5 * 2^23
-constexpr uint32_t kMagicBits = 0x4B400000u;
-constexpr float kInv127 = 1.0f / 127.0f;       // fp32(1/127)
 constexpr int kRsrcWord3 = 0x00020000;         // raw buffer, out-of-range reads zero
 constexpr int kNonTemporal = 2;                // cache policy: x is streamed once
 constexpr int kGroupsPerItem = 2;
@@ -88,11 +73,13 @@ template <int GS>
 __device__ __forceinline__ void quantize_group(uint4 v, uint32_t& word, int& fl, uint32_t& s16)
 {
     const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+    // max |x| of the lane's 8 values (the fp32 values are those mag_pairs8
+    // forms), then across the team (non-negative floats order as their bits)
     float f[8];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        f[2 * p] = __uint_as_float(d[p] << 16);
-        f[2 * p + 1] = __uint_as_float(d[p] & 0xFFFF0000u);
+    for (int k = 0; k < 4; ++k) {
+        f[2 * k] = __uint_as_float(d[k] << 16);
+        f[2 * k + 1] = __uint_as_float(d[k] & 0xFFFF0000u);
     }
     float amax = fabsf(f[0]);
 #pragma unroll
@@ -100,50 +87,13 @@ __device__ __forceinline__ void quantize_group(uint4 v, uint32_t& word, int& fl,
         amax = fmaxf(amax, fabsf(f[i]));
     const float alpha = __uint_as_float(team8_max(__float_as_uint(amax)));
 
-    // alpha >= 0: the only overflow is +inf (0x7C00), saturated to 65504
-    const _Float16 h = (_Float16)(alpha * kInv127);
-    s16 = min((uint32_t)__builtin_bit_cast(uint16_t, h), 0x7BFFu);
-    const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)s16);
-    const float r0 = __builtin_amdgcn_rcpf(s);
-    const float e = __builtin_fmaf(-s, r0, 1.0f);
-    const float r = s16 == 0 ? 0.0f : __builtin_fmaf(r0, e, r0);
-
-    // rne(|x| * r) <= 127 whenever s is a normal, unsaturated fp16 value (checked
-    // for every bf16 alpha); only groups with a subnormal or saturated scale
-    // need the clamp, and the wave takes that path only if one of its groups does
-    uint32_t b[8];
-    const bool clamp = (s16 - 1u) < 0x3FFu || s16 == 0x7BFFu;
-    if (__builtin_amdgcn_ballot_w64(clamp)) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            b[i] = min(__float_as_uint(fabsf(f[i]) * r + kMagic), kMagicBits + 127u);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            b[i] = __float_as_uint(fabsf(f[i]) * r + kMagic);
-    }
-    const uint32_t mor = subgroup_or<GS>((b[0] | b[1] | b[2] | b[3] | b[4] | b[5] | b[6] | b[7]) & 0x7Fu);
-    fl = max(29 - (int)__builtin_clz(mor | 1u), 0);
-
-    // magnitudes t = |q| >> FLAG (at most 7, so no mask is needed): element
-    // pair (2k, 2k+1) goes to the two 16-bit halves of one word (low bytes of
-    // b), both halves are shifted at once, and pair k lands at nibble k of
-    // each half, i.e. element 8j+i at nibble (i/2) + 4 (i%2)
-    const us2 sh = {(unsigned short)fl, (unsigned short)fl};
-    uint32_t T = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t pair = __builtin_amdgcn_perm(b[2 * k + 1], b[2 * k], 0x0C040C00u);
-        const us2 t = __builtin_bit_cast(us2, pair) >> sh;
-        T |= __builtin_bit_cast(uint32_t, t) << (4 * k);
-    }
-    // sign bits of x moved to bit 3 of each nibble
-    uint32_t S = 0;
-#pragma unroll
-    for (int p = 0; p < 4; ++p)
-        S |= (d[p] & 0x80008000u) >> (12 - 4 * p);
-    // keep a sign only where the magnitude is non-zero: t + 7 sets bit 3 iff t >= 1
-    word = T | (S & (T + 0x77777777u));
+    const GroupScale gs = group_scale(alpha);
+    s16 = gs.s16;
+    // the wave takes the clamped path only if one of its groups needs it
+    uint32_t p[4];
+    mag_pairs8(d, gs.r, __builtin_amdgcn_ballot_w64(gs.clamp) != 0, p);
+    fl = lzs_flag(subgroup_or<GS>(pairs_or(p)));
+    word = lzs_word(p, sign_nibbles(d), fl);
 }
 
 template <int GS>

@@ -55,13 +55,25 @@ GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool spl
 size_t gemm_workspace_bytes(const GemmSchedule& s);
 int gemm_resident_blocks();
 
+// Destination of an output quantized for the next layer (its K is this
+// layer's N): the arrays of quartz_quantize_act with M rows and N / 64
+// groups; codes == nullptr means a plain bf16 output.
+struct QuantOut {
+    uint8_t* codes;
+    uint8_t* flags;
+    uint16_t* scales;
+    int8_t* zeros;       // may be nullptr
+    int32_t lzs;         // LZS subgroup size of the output: 8, 16, 32 or 64
+};
+
 // `workspace`: gemm_workspace_bytes(sch) bytes whose counter part is zero
-// (left zero again by the launch); unused unless sch.persistent.
+// (left zero again by the launch); unused unless sch.sk_tiles > 0.  With
+// qout.codes set, y is not written and N % 64 == 0.
 hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                               const uint16_t* scales, const uint8_t* w_packed,
                               const uint16_t* bias, uint16_t* y, int64_t M, int64_t N, int64_t K,
                               int64_t ldy, int lzs_group, int epilogue, const GemmSchedule& sch,
-                              void* workspace, hipStream_t stream);
+                              void* workspace, const QuantOut& qout, hipStream_t stream);
 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,

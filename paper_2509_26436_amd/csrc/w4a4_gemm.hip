@@ -29,6 +29,7 @@
 #include <type_traits>
 
 #include "gemm_schedule.h"
+#include "lzs_device.h"
 #include "quartz_internal.h"
 
 namespace quartz {
@@ -36,6 +37,8 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 // Buffer resource word 3 for raw (untyped, stride 0) loads on gfx9: a load at
@@ -148,6 +151,15 @@ __device__ __forceinline__ uint2 flags_dwords(FlagRaw<GS> raw)
         return uint2{(uint32_t)raw, 0u};
 }
 
+// One math wave's 64 x 64 bf16 output tile, staged in LDS by the epilogue
+// that quantizes the output for the next layer (QOUT), addressed through
+// LDS-typed pointers.
+constexpr int kTransposeBytes = WM * WN * 2;
+constexpr int kTransposeLds = kMathWaves * kTransposeBytes;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(3))) v4u lds_v4u;
+
 // Decode roles (decode thread d = tid - 512, 0..255): A row d (32 code bytes,
 // the row's 64 / G_s flags, s_a) and B column d/2, half d%2 (16 code bytes);
 // threads d < 128 also carry s_w of column d.  Rows past M and columns past
@@ -158,20 +170,28 @@ __device__ __forceinline__ uint2 flags_dwords(FlagRaw<GS> raw)
 // single pipeline.  The decode waves fetch and decode across segment
 // boundaries without a break, so while the math waves write one tile's
 // output the next tile's first groups are already being staged.  SPLIT
-// instantiations carry the partial-sum code of shared tiles.
-template <int GS, bool I32OUT, bool GELU, bool SPLIT>
+// instantiations carry the partial-sum code of shared tiles; QOUT ones write
+// the output quantized for the next layer instead of bf16 (QuantOut).
+template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT>
 __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
-    uint32_t* __restrict__ counters, float* __restrict__ slots)
+    uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout)
 {
     // three LDS stages: group g + 2 is decoded into one while the math waves
     // read the operands of group g + 1 from another (and multiply group g
     // from registers)
-    __shared__ __attribute__((aligned(16))) uint8_t As[kStages][BM * 64];
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[kStages][BN * 64];
+    // One LDS array holds the operand stages and, in QOUT kernels, the
+    // output transpose regions after them: the stages stay at the lowest
+    // addresses, where every fragment address of the main loop is a lane
+    // offset plus an immediate (a larger array placed first would push them
+    // past the 16-bit immediate range and cost a register per stage).
+    constexpr int kStageBytes = kStages * (BM + BN) * 64;
+    __shared__ __attribute__((aligned(16))) uint8_t lds_main[kStageBytes + (QOUT ? kTransposeLds : 0)];
+    uint8_t (*const As)[BM * 64] = reinterpret_cast<uint8_t (*)[BM * 64]>(lds_main);
+    uint8_t (*const Bs)[BN * 64] = reinterpret_cast<uint8_t (*)[BN * 64]>(lds_main + kStages * BM * 64);
     // group scales as fp16 bits; entries BM (BN) stay 0: the upper half-wave's
     // k = 8 operand slot of the outer-product MFMA reads them
     __shared__ uint16_t sas[kStages][BM + 8];
@@ -585,10 +605,149 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                     rb, (int)(((int64_t)cur.tn * BN + wn * WN + j * 32 + l32) * 2), 0, 0);
         }
     };
+    // ---- output quantized for the next layer (QOUT): the bf16 values the
+    // plain epilogue would store, run through the activation quantizer with
+    // this layer's N as the next layer's K.  The wave's 64 columns are one
+    // 64-group of each of its 64 rows (N % 64 == 0).  The bf16 tile goes
+    // through the wave's own LDS region and comes back one row per lane, so
+    // the group maximum, the subgroup ORs and the code packing are in-lane
+    // arithmetic (lzs_device.h).  Row r's 16-byte chunk c (its elements
+    // 8c..8c+7, one 8-element block) sits at chunk c ^ ((r >> 1) & 7): a read
+    // of one chunk per row by 16 consecutive lanes (8 chunk positions x 2 row
+    // parities) then covers all 64 banks.  Three passes over the row keep
+    // few values in registers: the group maximum; per block |q| (written back
+    // over the block's chunk), its OR and sign bits; per block the code word
+    // once the subgroup FLAGs are known.
+    // Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
+    // [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside
+    // the buffer ranges and are dropped.
+    lds_u8* const tbuf = (lds_u8*)(lds_main + kStageBytes);
+    auto quantize_out = [&](const v16f (&out)[TM][TN]) {
+        if constexpr (QOUT) {
+            static_assert(TN == 2 && WN == 64, "one 64-group per wave row");
+            const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
+            if (col_base >= N)
+                return;                              // wave-uniform
+            const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
+            lds_u8* const tb = tbuf + uwave * kTransposeBytes;
+            float b[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                b[j] = __uint_as_float((uint32_t)bias_bits[j] << 16);
+            const uint32_t lane2 = (uint32_t)lane * 2u;
+            typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+            typedef float f2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    float v0 = out[i][0][r] + b[0];
+                    float v1 = out[i][1][r] + b[1];
+                    if constexpr (GELU) {
+                        v0 = gelu_tanh(v0);
+                        v1 = gelu_tanh(v1);
+                    }
+                    // after the swap lane l holds column l of rows row0, row0 + 4
+                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
+                                                                     __float_as_uint(v1), false, false);
+                    const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
+                    const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
+                    const int row0 = i * 32 + 8 * (r >> 2) + (r & 3);
+                    const uint32_t x0 = (uint32_t)((row0 >> 1) & 7) << 4;
+                    const uint32_t x1 = (uint32_t)(((row0 + 4) >> 1) & 7) << 4;
+                    *(lds_u16*)(tb + row0 * 128 + (lane2 ^ x0)) = (uint16_t)pk;
+                    *(lds_u16*)(tb + (row0 + 4) * 128 + (lane2 ^ x1)) = (uint16_t)(pk >> 16);
+                }
+            }
+            // the wave reads back only what it wrote itself: LDS order within
+            // the wave suffices, the clobber keeps the compiler's order
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            lds_u8* const row = tb + lane * 128;
+            const uint32_t rx = (uint32_t)((lane >> 1) & 7) << 4;
+            auto chunk = [&](int c) { return (lds_v4u*)(row + (((uint32_t)c << 4) ^ rx)); };
+            // pass 1: max |x| on the bf16 magnitude bits (their unsigned order
+            // is the order of |x|), two values per instruction
+            lzs_us2 m2 = {0, 0};
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const v4u v = *chunk(c);
+                const uint32_t d[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(lzs_us2, d[k] & 0x7FFF7FFFu));
+            }
+            const uint32_t am = max((uint32_t)m2[0], (uint32_t)m2[1]);
+            const GroupScale gsc = group_scale(__uint_as_float(am << 16));
+            const bool clamp = __builtin_amdgcn_ballot_w64(gsc.clamp) != 0;
+            // pass 2: |q| pairs of each block, replacing its chunk
+            uint32_t S[8], m8[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const v4u v = *chunk(c);
+                const uint32_t d[4] = {v[0], v[1], v[2], v[3]};
+                uint32_t p[4];
+                mag_pairs8(d, gsc.r, clamp, p);
+                m8[c] = pairs_or(p);
+                S[c] = sign_nibbles(d);
+                *chunk(c) = v4u{p[0], p[1], p[2], p[3]};
+            }
+            // FLAG per block from the OR over its subgroup
+            const int qgs = qout.lzs;
+            uint32_t o16[4], o32[2];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                o16[k] = m8[2 * k] | m8[2 * k + 1];
+            o32[0] = o16[0] | o16[1];
+            o32[1] = o16[2] | o16[3];
+            const uint32_t o64 = o32[0] | o32[1];
+            int fl[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                fl[k] = lzs_flag(qgs == 8 ? m8[k] : qgs == 16 ? o16[k / 2] : qgs == 32 ? o32[k / 4] : o64);
+            // pass 3: code words
+            uint32_t w[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const v4u v = *chunk(c);
+                const uint32_t p[4] = {v[0], v[1], v[2], v[3]};
+                w[c] = lzs_word(p, S[c], fl[c]);
+            }
+
+            const int64_t g = col_base / 64;
+            const int64_t rg0 = g * M + row_base;           // (group, first row)
+            const uint32_t rows_in = (uint32_t)max((int64_t)0, min(M - row_base, (int64_t)WM));
+            const Rsrc rc = make_rsrc(qout.codes + rg0 * 32, rows_in * 32u);
+            __builtin_amdgcn_raw_buffer_store_b128(v4u{w[0], w[1], w[2], w[3]}, rc, lane * 32, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(v4u{w[4], w[5], w[6], w[7]}, rc, lane * 32 + 16, 0, 0);
+            const uint32_t fb = (uint32_t)(64 / qgs);
+            const Rsrc rf = make_rsrc(qout.flags + rg0 * fb, rows_in * fb);
+            if (qgs == 8) {
+                const uint32_t lo = fl[0] | fl[1] << 8 | fl[2] << 16 | fl[3] << 24;
+                const uint32_t hi = fl[4] | fl[5] << 8 | fl[6] << 16 | fl[7] << 24;
+                __builtin_amdgcn_raw_buffer_store_b64(v2u{lo, hi}, rf, lane * 8, 0, 0);
+            } else if (qgs == 16) {
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    (uint32_t)(fl[0] | fl[2] << 8 | fl[4] << 16 | fl[6] << 24), rf, lane * 4, 0, 0);
+            } else if (qgs == 32) {
+                __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(fl[0] | fl[4] << 8), rf, lane * 2, 0, 0);
+            } else {
+                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl[0], rf, lane, 0, 0);
+            }
+            const Rsrc rs = make_rsrc(qout.scales + rg0, rows_in * 2u);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)gsc.s16, rs, lane * 2, 0, 0);
+            if (qout.zeros) {
+                const Rsrc rz = make_rsrc(qout.zeros + rg0, rows_in);
+                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)0, rz, lane, 0, 0);
+            }
+        }
+    };
+
     // ---- output.  Lane l holds column l % 32 of each 32 x 32 tile, rows
     // 8 (r/4) + 4 khalf + r%4 of register r.
     auto store_tile = [&](const v16f (&out)[TM][TN]) {
-        if constexpr (I32OUT) {
+        if constexpr (QOUT) {
+            quantize_out(out);
+        } else if constexpr (I32OUT) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int64_t col = (int64_t)cur.tn * BN + wn * WN + j * 32 + l32;
@@ -676,7 +835,9 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                          kRegionFloats * (uint32_t)sizeof(float));
     };
     typedef float v4f __attribute__((ext_vector_type(4)));
-    auto finish_partial = [&] {
+    // Returns true for the wave that completes the region (acc then holds
+    // the whole sum and the caller writes the output).
+    auto finish_partial = [&]() -> bool {
         if constexpr (SPLIT && !I32OUT) {
             const uint32_t lane_off = (uint32_t)lane * 16u;
             const Rsrc mine = slot_rsrc(cur.sg.slot);
@@ -701,7 +862,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             int32_t b_first, b_last;
             sk_contributors(sch_, cur.sg.sk_tile, b_first, b_last);
             if (arrived != (uint32_t)(b_last - b_first))
-                return;
+                return false;
             asm volatile("" ::: "memory");
             if (b_last - b_first == 1) {
                 // two contributors (the usual case): add the other one's slot
@@ -730,8 +891,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 }
                 if (lane == 0)
                     __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                store_tile(acc);
-                return;
+                return true;
             }
             // more contributors: acc = sum of their slots in workgroup order
             // (this wave's own slot included, re-read: it holds the same values)
@@ -756,8 +916,9 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             }
             if (lane == 0)
                 __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            store_tile(acc);
+            return true;
         }
+        return false;
     };
 
     auto reset_tile = [&] {
@@ -807,41 +968,52 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             math_barrier();
         fma_tile(TM - 1, TN - 1, p_last, s_last);
         set_fragment_indices();
-        if (!SPLIT || cur.sg.sk_tile < 0)
+        // one output call site, so the epilogue is inlined once
+        if (!SPLIT || cur.sg.sk_tile < 0 || finish_partial())
             store_tile(acc);
-        else
-            finish_partial();
         if (!cursor_next(fresh_schedule(), blk, cur))
             break;
     }
 }
 
+template <bool B>
+using bool_c = std::integral_constant<bool, B>;
+
 template <bool I32OUT, int GS>
 hipError_t launch_gs(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
                      const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                      int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue,
-                     const GemmSchedule& sch, uint32_t* counters, float* slots, hipStream_t stream)
+                     const GemmSchedule& sch, uint32_t* counters, float* slots,
+                     const QuantOut& qout, hipStream_t stream)
 {
     const dim3 grid((unsigned)sch.blocks), block(kThreadsPerBlock);
-    // the epilogue and the split part are compile-time choices, so the
-    // whole-tile plain kernel carries neither GELU nor partial-sum code
+    // the epilogue, the split part and the quantized output are compile-time
+    // choices, so the whole-tile plain kernel carries none of their code
     if constexpr (I32OUT) {
-        w4a4_gemm_kernel<GS, true, false, false><<<grid, block, 0, stream>>>(
-            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
-    } else if (sch.sk_tiles > 0) {
-        if (epilogue == 1)
-            w4a4_gemm_kernel<GS, false, true, true><<<grid, block, 0, stream>>>(
-                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
-        else
-            w4a4_gemm_kernel<GS, false, false, true><<<grid, block, 0, stream>>>(
-                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+        w4a4_gemm_kernel<GS, true, false, false, false><<<grid, block, 0, stream>>>(
+            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout);
     } else {
+        auto go = [&](auto gelu, auto split, auto q) {
+            w4a4_gemm_kernel<GS, false, decltype(gelu)::value, decltype(split)::value,
+                             decltype(q)::value><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout);
+        };
+        auto with_q = [&](auto gelu, auto split) {
+            if (qout.codes)
+                go(gelu, split, bool_c<true>());
+            else
+                go(gelu, split, bool_c<false>());
+        };
+        auto with_split = [&](auto gelu) {
+            if (sch.sk_tiles > 0)
+                with_q(gelu, bool_c<true>());
+            else
+                with_q(gelu, bool_c<false>());
+        };
         if (epilogue == 1)
-            w4a4_gemm_kernel<GS, false, true, false><<<grid, block, 0, stream>>>(
-                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+            with_split(bool_c<true>());
         else
-            w4a4_gemm_kernel<GS, false, false, false><<<grid, block, 0, stream>>>(
-                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots);
+            with_split(bool_c<false>());
     }
     return hipGetLastError();
 }
@@ -850,21 +1022,22 @@ template <bool I32OUT>
 hipError_t launch(const uint8_t* codes, const uint8_t* flags, const uint16_t* scales,
                   const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                   int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group, int epilogue,
-                  const GemmSchedule& sch, uint32_t* counters, float* slots, hipStream_t stream)
+                  const GemmSchedule& sch, uint32_t* counters, float* slots,
+                  const QuantOut& qout, hipStream_t stream)
 {
     switch (lzs_group) {
     case 8:
         return launch_gs<I32OUT, 8>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                    epilogue, sch, counters, slots, stream);
+                                    epilogue, sch, counters, slots, qout, stream);
     case 16:
         return launch_gs<I32OUT, 16>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, stream);
+                                     epilogue, sch, counters, slots, qout, stream);
     case 32:
         return launch_gs<I32OUT, 32>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, stream);
+                                     epilogue, sch, counters, slots, qout, stream);
     default:
         return launch_gs<I32OUT, 64>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, stream);
+                                     epilogue, sch, counters, slots, qout, stream);
     }
 }
 
@@ -948,7 +1121,7 @@ int gemm_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false>),
             kThreadsPerBlock, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
@@ -961,7 +1134,7 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                               const uint16_t* scales, const uint8_t* w_packed,
                               const uint16_t* bias, uint16_t* y, int64_t M, int64_t N, int64_t K,
                               int64_t ldy, int lzs_group, int epilogue, const GemmSchedule& sch,
-                              void* workspace, hipStream_t stream)
+                              void* workspace, const QuantOut& qout, hipStream_t stream)
 {
     if (sch.blocks <= 0)
         return hipErrorInvalidConfiguration;
@@ -970,7 +1143,7 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                        ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(sch))
                        : nullptr;
     return launch<false>(codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
-                         epilogue, sch, counters, slots, stream);
+                         epilogue, sch, counters, slots, qout, stream);
 }
 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
@@ -981,7 +1154,7 @@ hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
     if (sch.blocks <= 0)
         return hipErrorInvalidConfiguration;
     return launch<true>(codes, flags, nullptr, w_packed, nullptr, nullptr, acc, M, N, K, N,
-                        lzs_group, 0, sch, nullptr, nullptr, stream);
+                        lzs_group, 0, sch, nullptr, nullptr, QuantOut{}, stream);
 }
 
 }  // namespace quartz

@@ -118,6 +118,35 @@ def test_linear_validation(lib):
     assert call(N=(1 << 24) + 1, ldy=(1 << 24) + 1, K=1024) == ESHAPE
 
 
+def test_linear_quantize_validation(lib):
+    f = q.quartz_w4a4_linear_quantize
+    args = dict(codes=A, flags=A, scales=A, zeros=None, w=A, bias=None,
+                oc=A, of=A, os=A, oz=None, ws=None)
+
+    def call(M=8, N=64, K=128, gs=64, lzs=16, epi=0, olzs=16, omode=0, wsb=0, **over):
+        a = dict(args, **over)
+        return f(a["codes"], a["flags"], a["scales"], a["zeros"], a["w"], a["bias"], M, N, K,
+                 gs, lzs, epi, olzs, omode, a["oc"], a["of"], a["os"], a["oz"], a["ws"], wsb, None)
+    assert call(olzs=4) == EUNSUP
+    assert call(olzs=128) == EUNSUP
+    assert call(omode=1) == EUNSUP
+    assert call(gs=32) == EUNSUP
+    assert call(epi=3) == EUNSUP
+    assert call(N=96) == ESHAPE          # the output is the next layer's K: N % 64 == 0
+    assert call(N=32) == ESHAPE
+    assert call(K=100) == ESHAPE
+    assert call(M=-1) == ESHAPE
+    assert call(oc=None) == ENULL
+    assert call(of=None) == ENULL
+    assert call(os=None) == ENULL
+    assert call(scales=None) == ENULL
+    assert call(oc=A + 4) == EALIGN
+    assert call(oz=A + 8) == EALIGN
+    assert call(ws=A + 2, wsb=1 << 20) == EALIGN
+    assert call(M=0) == OK
+    assert call(N=0) == OK
+
+
 def test_debug_entry_validation(lib):
     assert q.quartz_unpack_weight(A, 8, 100, 64, A, None) == ESHAPE
     assert q.quartz_unpack_weight(None, 8, 128, 64, A, None) == ENULL

@@ -17,28 +17,10 @@ import oracle
 import workloads as W
 
 
-def _int_rows(g, rows, K, top):
-    """Integers in [-top, top] with one +-top in every 64-group of every row."""
-    a = g.integers(-top, top + 1, size=(rows, K)).astype(np.int64)
-    for r in range(rows):
-        for k0 in range(0, K, 64):
-            a[r, k0 + g.integers(0, 64)] = top * (1 if g.integers(0, 2) else -1)
-    return a
-
-
 def _exact_case(seed, M, N, K, gs):
-    g = np.random.Generator(np.random.PCG64(seed))
-    A = _int_rows(g, M, K, 127)
-    Wi = _int_rows(g, N, K, 7)
-    e = g.integers(-6, -1, size=M)
-    f = g.integers(-9, -4, size=N)
-    x = W.to_bf16_bits(np.ldexp(A.astype(np.float64), e[:, None]))
-    w = W.to_bf16_bits(np.ldexp(Wi.astype(np.float64), f[:, None]))
-    b_int = g.integers(-255, 256, size=N)     # 8 significant bits: exact in bf16
-    bias_val = np.ldexp(b_int.astype(np.float64), f + e.max())
-    bias = W.to_bf16_bits(bias_val)
-    assert np.array_equal(W.bf16_bits_to_f32(bias).astype(np.float64), bias_val)
-    return A, Wi, e, f, x, w, bias, bias_val
+    c = W.make_exact_case(seed, M, N, K)
+    assert np.array_equal(W.bf16_bits_to_f32(c.bias).astype(np.float64), c.bias_val)
+    return c.A, c.Wi, c.e, c.f, c.x, c.w, c.bias, c.bias_val
 
 
 @pytest.mark.parametrize("gs,out_gs", [(16, 16), (8, 32), (64, 8)])

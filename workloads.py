@@ -209,3 +209,44 @@ def make_random_x(seed_value: int, M: int, K: int, kind: str = "laplace",
     else:
         raise ValueError(kind)
     return to_bf16_bits(x)
+
+
+@dataclass(frozen=True)
+class ExactCase:
+    """Inputs whose layer output is exact in fp32 (see make_exact_case)."""
+    A: np.ndarray          # int64 [M][K], |A| <= 127, a +-127 in every 64-group of a row
+    Wi: np.ndarray         # int64 [N][K], |Wi| <= 7, a +-7 in every 64-group of a row
+    e: np.ndarray          # int64 [M]: row m of x is A[m] * 2^e[m]
+    f: np.ndarray          # int64 [N]: row n of w is Wi[n] * 2^f[n]
+    x: np.ndarray          # bf16 bits [M][K]
+    w: np.ndarray          # bf16 bits [N][K]
+    bias: np.ndarray       # bf16 bits [N]: b_int[n] * 2^(f[n] + max e)
+    bias_val: np.ndarray   # float64 [N]
+
+
+def _int_rows(g: np.random.Generator, rows: int, K: int, top: int) -> np.ndarray:
+    a = g.integers(-top, top + 1, size=(rows, K)).astype(np.int64)
+    for k0 in range(0, K, 64):
+        pos = g.integers(0, 64, size=rows)
+        sign = np.where(g.integers(0, 2, size=rows) == 1, 1, -1)
+        a[np.arange(rows), k0 + pos] = top * sign
+    return a
+
+
+def make_exact_case(seed_value: int, M: int, N: int, K: int) -> ExactCase:
+    """Activations A * 2^e (integers up to 127 with a +-127 in every 64-group)
+    and weights Wi * 2^f (integers up to 7 with a +-7 in every 64-group): every
+    group's max |x| / 127 and max |w| / 7 is a power of two, and the bias is an
+    integer of at most 8 bits times 2^(f + max e).  Any sum of products of such
+    values with scales 2^e, 2^f is an integer times 2^(e + f); for K up to a
+    few thousand it stays below 2^24 of that unit, i.e. exact in fp32."""
+    g = np.random.Generator(np.random.PCG64(seed_value))
+    A = _int_rows(g, M, K, 127)
+    Wi = _int_rows(g, N, K, 7)
+    e = g.integers(-6, -1, size=M)
+    f = g.integers(-9, -4, size=N)
+    x = to_bf16_bits(np.ldexp(A.astype(np.float64), e[:, None]))
+    w = to_bf16_bits(np.ldexp(Wi.astype(np.float64), f[:, None]))
+    b_int = g.integers(-255, 256, size=N)
+    bias_val = np.ldexp(b_int.astype(np.float64), f + e.max())
+    return ExactCase(A, Wi, e, f, x, w, to_bf16_bits(bias_val), bias_val)
