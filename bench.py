@@ -41,7 +41,7 @@ PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
-                for f in ("w4a4_gemm.hip", "gemm_schedule.h", "quartz_internal.h")]
+                for f in ("w4a4_gemm.hip", "gemm_schedule.h", "quartz_internal.h", "lzs_device.h")]
 
 
 def log(*a):
@@ -118,7 +118,8 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
     12288->3072.  Per layer: mean quantize and GEMM time over `reps` passes
     (HIP events on the launch stream), and the end-to-end time against the
     sum of the two roofline times (quantize bytes at 8 TB/s + GEMM ops at the
-    fp8 dense peak)."""
+    fp8 dense peak).  Then the same pipeline with fc2's input quantized in
+    fc1's epilogue, its time, and whether fc2's output is bit-identical."""
     dev = torch.device("cuda", 0)
     cfg = W.CONFIGS[4]
     L1, L2 = cfg.layers
@@ -151,6 +152,32 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
         if it >= 2:
             t += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(4)])
     t = t / reps * 1e3        # us
+    # the same pipeline with fc2's input quantized in fc1's epilogue
+    # (quartz_w4a4_linear_quantize): no bf16 fc1 output, no separate quantize
+    qa2f = q.w4a4_linear_quantize(qa1, pw1, b1, 1, gs, workspace=ws1)
+    y2f = q.w4a4_linear(qa2f, pw2, b2, 0, workspace=ws2)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(y2f.view(torch.int16), y2.view(torch.int16)))
+    tf = np.zeros(3)
+    for it in range(reps + 2):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        q.quantize_act(x1, lzs_group=gs, out=qa1)
+        ev[1].record(stream)
+        q.w4a4_linear_quantize(qa1, pw1, b1, 1, gs, out=qa2f, workspace=ws1)
+        ev[2].record(stream)
+        q.w4a4_linear(qa2f, pw2, b2, 0, out=y2f, workspace=ws2)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        if it >= 2:
+            tf += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(3)])
+    tf = tf / reps * 1e3      # us
+    fused = {"step": "quantize + fc1 (GELU; its epilogue quantizes the output for fc2) + fc2",
+             "quantize_us": round(tf[0], 2), "fc1_quantize_us": round(tf[1], 2),
+             "fc2_gemm_us": round(tf[2], 2), "end_to_end_us": round(tf.sum(), 2),
+             "unfused_end_to_end_us": round(t.sum(), 2),
+             "speedup": round(t.sum() / tf.sum(), 4),
+             "fc2_output_identical": same}
     out = []
     for li, L in enumerate((L1, L2)):
         qb, _, _ = layer_bytes(L, gs)
@@ -163,7 +190,8 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
                     "end_to_end_us": round(tq + tg, 2), "roofline_us": round(roof, 2),
                     "frac": round(roof / (tq + tg), 4)})
     return {"workload": cfg.name, "lzs_group": gs,
-            "step": "quantize + fc1 (GELU) + quantize + fc2", "per_layer": out}
+            "step": "quantize + fc1 (GELU) + quantize + fc2", "per_layer": out,
+            "fused_quantize": fused}
 
 
 def main():

@@ -56,8 +56,8 @@ __device__ __forceinline__ GroupScale group_scale(float alpha)
 // |q| of the 8 values in d[0..3], as 4 pairs: pair k holds |q| of elements
 // 2k and 2k + 1 in its two 16-bit halves.  `clamp` (wave-uniform) selects
 // the clamped form.
-__device__ __forceinline__ void mag_pairs8(const uint32_t (&d)[4], float r, bool clamp,
-                                           uint32_t (&p)[4])
+template <bool CLAMP>
+__device__ __forceinline__ void mag_pairs8_t(const uint32_t (&d)[4], float r, uint32_t (&p)[4])
 {
     float f[8];
 #pragma unroll
@@ -66,19 +66,25 @@ __device__ __forceinline__ void mag_pairs8(const uint32_t (&d)[4], float r, bool
         f[2 * k + 1] = __uint_as_float(d[k] & 0xFFFF0000u);
     }
     uint32_t b[8];
-    if (clamp) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-            b[i] = min(__float_as_uint(fabsf(f[i]) * r + kMagic), kMagicBits + 127u);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            b[i] = __float_as_uint(fabsf(f[i]) * r + kMagic);
+    for (int i = 0; i < 8; ++i) {
+        b[i] = __float_as_uint(fabsf(f[i]) * r + kMagic);
+        if constexpr (CLAMP)
+            b[i] = min(b[i], kMagicBits + 127u);
     }
     // the low byte of each sum is |q| (at most 127); two of them per pair
 #pragma unroll
     for (int k = 0; k < 4; ++k)
         p[k] = __builtin_amdgcn_perm(b[2 * k + 1], b[2 * k], 0x0C040C00u);
+}
+
+__device__ __forceinline__ void mag_pairs8(const uint32_t (&d)[4], float r, bool clamp,
+                                           uint32_t (&p)[4])
+{
+    if (clamp)
+        mag_pairs8_t<true>(d, r, p);
+    else
+        mag_pairs8_t<false>(d, r, p);
 }
 
 // OR of the 8 magnitudes of mag_pairs8

@@ -614,10 +614,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // arithmetic (lzs_device.h).  Row r's 16-byte chunk c (its elements
     // 8c..8c+7, one 8-element block) sits at chunk c ^ ((r >> 1) & 7): a read
     // of one chunk per row by 16 consecutive lanes (8 chunk positions x 2 row
-    // parities) then covers all 64 banks.  Three passes over the row keep
-    // few values in registers: the group maximum; per block |q| (written back
-    // over the block's chunk), its OR and sign bits; per block the code word
-    // once the subgroup FLAGs are known.
+    // parities) then covers all 64 banks.  The row is read once; per block
+    // the |q| pairs go back over the block's chunk (so they need no registers
+    // while the subgroup FLAGs are formed) and are read again for the code
+    // words.
     // Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
     // [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside
     // the buffer ranges and are dropped.
@@ -665,46 +665,59 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             lds_u8* const row = tb + lane * 128;
             const uint32_t rx = (uint32_t)((lane >> 1) & 7) << 4;
             auto chunk = [&](int c) { return (lds_v4u*)(row + (((uint32_t)c << 4) ^ rx)); };
-            // pass 1: max |x| on the bf16 magnitude bits (their unsigned order
-            // is the order of |x|), two values per instruction
-            lzs_us2 m2 = {0, 0};
+            uint32_t X[8][4];
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 const v4u v = *chunk(c);
-                const uint32_t d[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
-                    m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(lzs_us2, d[k] & 0x7FFF7FFFu));
+                    X[c][k] = v[k];
             }
+            // max |x| on the bf16 magnitude bits (their unsigned order is the
+            // order of |x|), two values per instruction
+            lzs_us2 m2 = {0, 0};
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(lzs_us2, X[c][k] & 0x7FFF7FFFu));
             const uint32_t am = max((uint32_t)m2[0], (uint32_t)m2[1]);
             const GroupScale gsc = group_scale(__uint_as_float(am << 16));
-            const bool clamp = __builtin_amdgcn_ballot_w64(gsc.clamp) != 0;
-            // pass 2: |q| pairs of each block, replacing its chunk
+            // |q| pairs of each 8-element block (written back over its chunk),
+            // their OR and the sign bits; one branch for the wave
             uint32_t S[8], m8[8];
+            auto pairs = [&](auto clamp) {
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const v4u v = *chunk(c);
-                const uint32_t d[4] = {v[0], v[1], v[2], v[3]};
-                uint32_t p[4];
-                mag_pairs8(d, gsc.r, clamp, p);
-                m8[c] = pairs_or(p);
-                S[c] = sign_nibbles(d);
-                *chunk(c) = v4u{p[0], p[1], p[2], p[3]};
-            }
-            // FLAG per block from the OR over its subgroup
+                for (int c = 0; c < 8; ++c) {
+                    uint32_t p[4];
+                    mag_pairs8_t<decltype(clamp)::value>(X[c], gsc.r, p);
+                    m8[c] = pairs_or(p);
+                    S[c] = sign_nibbles(X[c]);
+                    *chunk(c) = v4u{p[0], p[1], p[2], p[3]};
+                }
+            };
+            if (__builtin_amdgcn_ballot_w64(gsc.clamp))
+                pairs(std::integral_constant<bool, true>());
+            else
+                pairs(std::integral_constant<bool, false>());
+            // FLAG per block: the OR over its subgroup, built by OR-ing the
+            // blocks at distance 1, 2 and 4 under wave-uniform masks that keep
+            // only partners in the same subgroup
             const int qgs = qout.lzs;
-            uint32_t o16[4], o32[2];
+            const uint32_t k16 = qgs >= 16 ? ~0u : 0u, k32 = qgs >= 32 ? ~0u : 0u,
+                           k64 = qgs >= 64 ? ~0u : 0u;
+            uint32_t o1[8], o2[8];
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
-                o16[k] = m8[2 * k] | m8[2 * k + 1];
-            o32[0] = o16[0] | o16[1];
-            o32[1] = o16[2] | o16[3];
-            const uint32_t o64 = o32[0] | o32[1];
+            for (int k = 0; k < 8; ++k)
+                o1[k] = m8[k] | (m8[k ^ 1] & k16);
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                o2[k] = o1[k] | (o1[k ^ 2] & k32);
             int fl[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k)
-                fl[k] = lzs_flag(qgs == 8 ? m8[k] : qgs == 16 ? o16[k / 2] : qgs == 32 ? o32[k / 4] : o64);
-            // pass 3: code words
+                fl[k] = lzs_flag(o2[k] | (o2[k ^ 4] & k64));
+            // code words from the stored pairs
             uint32_t w[8];
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
