@@ -76,6 +76,13 @@ def _load():
     lib.qo_linear_f64_sampled.argtypes = [P, P, P, P, P, P, I64, I32, I32, I32,
                                           P, P, I64, P, P]
     lib.qo_linear_f64_sampled.restype = I32
+    lib.qo_quantize_act_static.argtypes = [P, I64, I64, I64, ctypes.c_float, I32, P, P, P]
+    lib.qo_quantize_act_static.restype = I32
+    lib.qo_quantize_weight_per_channel.argtypes = [P, I64, I64, P, P]
+    lib.qo_quantize_weight_per_channel.restype = I32
+    lib.qo_linear_static_f64.argtypes = [P, P, ctypes.c_float, P, P, P, I64, I64, I64, I32, I32,
+                                         P, P]
+    lib.qo_linear_static_f64.restype = I32
     lib.qo_round_bf16.argtypes = [P, I64, P]
     lib.qo_round_bf16.restype = None
     lib.qo_num_threads.argtypes = []
@@ -306,3 +313,52 @@ def linear_quantize(a: ActQuant, wq: np.ndarray, sw: np.ndarray, bias_bits=None,
     the fly to the producing layer's result, Appendix C)."""
     y64, _ = linear_f64(a, wq, sw, bias_bits, epilogue)
     return quantize_act(round_bf16(y64), out_lzs_group)
+
+
+# ----------------------------------------------- LDM setting (reading R8)
+
+def quantize_act_static(x_bits: np.ndarray, scale: float, lzs_group: int = 16) -> ActQuant:
+    """Static per-tensor quantizer with the fp32 scale ``scale``; the result's
+    scales / zeros are None (there are no per-group scales)."""
+    x_bits = _c(x_bits, np.uint16)
+    M, K = x_bits.shape
+    q8 = np.empty((M, K), np.int8)
+    c = np.empty((M, K), np.int8)
+    flags = np.empty((M, K // lzs_group), np.uint8)
+    rc = _load().qo_quantize_act_static(_ptr(x_bits), M, K, K, float(np.float32(scale)), lzs_group,
+                                        _ptr(q8), _ptr(c), _ptr(flags))
+    if rc != 0:
+        raise ValueError("oracle quantize_act_static: invalid arguments")
+    return ActQuant(q8, c, flags, None, None, lzs_group)
+
+
+def quantize_weight_per_channel(w_bits: np.ndarray):
+    """w_bits: uint16 bf16 [N][K]; returns (wq int8 [N][K], sw uint16 [N])."""
+    w_bits = _c(w_bits, np.uint16)
+    N, K = w_bits.shape
+    wq = np.empty((N, K), np.int8)
+    sw = np.empty(N, np.uint16)
+    rc = _load().qo_quantize_weight_per_channel(_ptr(w_bits), N, K, _ptr(wq), _ptr(sw))
+    if rc != 0:
+        raise ValueError("oracle quantize_weight_per_channel: invalid arguments")
+    return wq, sw
+
+
+def linear_static_f64(a: ActQuant, scale: float, wq: np.ndarray, sw: np.ndarray,
+                      bias_bits=None, epilogue: int = 0):
+    """LDM-setting layer: returns (y64 float64 [M][N], S float64 [M][N])."""
+    c = _c(a.c, np.int8)
+    flags = _c(a.flags, np.uint8)
+    wq = _c(wq, np.int8)
+    sw = _c(sw, np.uint16)
+    bias = None if bias_bits is None else _c(bias_bits, np.uint16)
+    M, K = c.shape
+    N = wq.shape[0]
+    y = np.empty((M, N), np.float64)
+    s = np.empty((M, N), np.float64)
+    rc = _load().qo_linear_static_f64(_ptr(c), _ptr(flags), float(np.float32(scale)), _ptr(wq),
+                                      _ptr(sw), _ptr(bias), M, N, K, a.lzs_group, epilogue,
+                                      _ptr(y), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle linear_static_f64: invalid arguments")
+    return y, s

@@ -38,6 +38,14 @@
  *   R6  The integer MMA with a per-subgroup power-of-two (Section 4.4) equals
  *       sum_k d[m,k] * wq[n,k] over each 64-group (distributivity); the
  *       per-group float dequantization multiplies by s_a[m,g] * s_w[n,g].
+ *   R8  The LDM setting (the experimental-details appendix): static
+ *       per-tensor activation quantization takes one fp32 scale s fixed
+ *       ahead of time (calibration is outside the hot path), r = fp32(1/s),
+ *       q = clamp(rne(fp32(x * r)), -127, 127), then Stage 2 as in R3/R4;
+ *       per-channel weight quantization takes s_w[n] = fp16(max over all of
+ *       K of |w[n,k]| / 7) and wq = clamp(rne(fp32(w * (1/s_w[n]))), -7, 7).
+ *       The layer output is y = s * s_w[n] * I[m,n] + bias with I the exact
+ *       integer sum over all of K of d * wq.
  */
 #include <math.h>
 #include <stdint.h>
@@ -452,6 +460,113 @@ int qo_linear_f64_sampled(const int8_t* c, const uint8_t* flags, const uint16_t*
     for (int64_t i = 0; i < count; ++i)
         y[i] = linear_one(c, flags, scales, wq, sw, bias, K, group, lzs_group, epilogue,
                           rows[i], cols[i], absum ? &absum[i] : NULL);
+    return QO_OK;
+}
+
+/* ------------------------------------------- LDM setting (reading R8) */
+
+/*
+ * Static per-tensor activation quantizer: Stage 1 with the given scale s
+ * (fp32, s > 0), then Stage 2 per subgroup of lzs_group elements.  Outputs
+ * as qo_quantize_act (q8 may be NULL); there are no per-group scales.
+ */
+int qo_quantize_act_static(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, float s,
+                           int lzs_group, int8_t* q8, int8_t* c, uint8_t* flags)
+{
+    if (!(s > 0.0f) || lzs_group < 1 || 64 % lzs_group != 0 || K % 64 != 0 || ldx < K)
+        return QO_EINVAL;
+    const float r = 1.0f / s;                    /* IEEE binary32 division */
+    const int64_t S = K / lzs_group;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t j = 0; j < S; ++j) {
+            int8_t q[64];
+            for (int i = 0; i < lzs_group; ++i) {
+                float p = qo_bf16_to_f32(x[m * ldx + j * lzs_group + i]) * r;
+                double v = qo_rne((double)p);
+                if (v > 127.0)
+                    v = 127.0;
+                if (v < -127.0)
+                    v = -127.0;
+                q[i] = (int8_t)v;
+                if (q8)
+                    q8[m * K + j * lzs_group + i] = q[i];
+            }
+            flags[m * S + j] = (uint8_t)qo_lzs_subgroup(q, lzs_group, c + m * K + j * lzs_group);
+        }
+    }
+    return QO_OK;
+}
+
+/* Per-channel weight quantizer: one fp16 scale per output channel n. */
+int qo_quantize_weight_per_channel(const uint16_t* w, int64_t N, int64_t K, int8_t* wq,
+                                   uint16_t* sw)
+{
+    if (K % 64 != 0)
+        return QO_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; ++n) {
+        float beta = 0.0f;
+        for (int64_t k = 0; k < K; ++k) {
+            float a = fabsf(qo_bf16_to_f32(w[n * K + k]));
+            if (a > beta)
+                beta = a;
+        }
+        uint16_t s16 = qo_f32_to_f16_rne_sat(beta / 7.0f);
+        float sc = qo_f16_to_f32(s16);
+        float r = (sc == 0.0f) ? 0.0f : 1.0f / sc;
+        sw[n] = s16;
+        for (int64_t k = 0; k < K; ++k) {
+            float p = qo_bf16_to_f32(w[n * K + k]) * r;
+            double v = qo_rne((double)p);
+            if (v > 7.0)
+                v = 7.0;
+            if (v < -7.0)
+                v = -7.0;
+            wq[n * K + k] = (int8_t)v;
+        }
+    }
+    return QO_OK;
+}
+
+/*
+ * One output of the LDM-setting layer, in double:
+ *   y = s * s_w[n] * I[m,n] + bias[n]   (then GELU-tanh),
+ * I = sum over all k of d[m,k] * wq[n,k] (exact).  *absum receives
+ * S = |s * s_w[n] * I| + |bias|.
+ */
+static double linear_static_one(const int8_t* c, const uint8_t* flags, float s, const int8_t* wq,
+                                const uint16_t* sw, const uint16_t* bias, int64_t K,
+                                int lzs_group, int epilogue, int64_t m, int64_t n, double* absum)
+{
+    int64_t I = 0;
+    for (int64_t k = 0; k < K; ++k)
+        I += (int64_t)decoded(c, flags, K, lzs_group, m, k) * wq[n * K + k];
+    double t = (double)s * (double)qo_f16_to_f32(sw[n]) * (double)I;
+    double y = t, a = fabs(t);
+    if (bias) {
+        double b = (double)qo_bf16_to_f32(bias[n]);
+        y += b;
+        a += fabs(b);
+    }
+    if (epilogue == 1)
+        y = qo_gelu_tanh(y);
+    if (absum)
+        *absum = a;
+    return y;
+}
+
+int qo_linear_static_f64(const int8_t* c, const uint8_t* flags, float s, const int8_t* wq,
+                         const uint16_t* sw, const uint16_t* bias, int64_t M, int64_t N, int64_t K,
+                         int lzs_group, int epilogue, double* y, double* absum)
+{
+    if (K % 64 != 0 || lzs_group < 1 || 64 % lzs_group != 0)
+        return QO_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t n = 0; n < N; ++n)
+            y[m * N + n] = linear_static_one(c, flags, s, wq, sw, bias, K, lzs_group, epilogue, m,
+                                             n, absum ? &absum[m * N + n] : NULL);
     return QO_OK;
 }
 
