@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched-mlp", action="store_true",
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
+    ap.add_argument("--no-ldm", action="store_true",
+                    help="skip the LDM-setting (static activation scale) layer measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -192,6 +194,47 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
     return {"workload": cfg.name, "lzs_group": gs,
             "step": "quantize + fc1 (GELU) + quantize + fc2", "per_layer": out,
             "fused_quantize": fused}
+
+
+def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
+    """The LDM setting (static per-tensor activation scale, per-channel weight
+    scales; the K loop is pure integer MFMA) on the same layers: per layer the
+    static quantizer and GEMM times (HIP events on the launch stream, mean over
+    `reps` passes after two untimed ones).  The static scale is fixed once from
+    the synthetic tensor (max |x| / 127, outside the timed region)."""
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    out = []
+    for li, ((x, w, b), L) in enumerate(zip(dev_in, cfg.layers)):
+        s = float(x.abs().max().float().item()) / 127.0
+        qa = q.quantize_act_static(x, s, gs)
+        pw = q.pack_weight_per_channel(w)
+        ws = q.gemm_workspace(L.M, L.N, L.K, dev)
+        y = q.w4a4_linear_static(qa, pw, s, b, L.epilogue, workspace=ws)
+        torch.cuda.synchronize()
+        t = np.zeros(2)
+        for it in range(reps + 2):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record(stream)
+            q.quantize_act_static(x, s, gs, out=qa)
+            ev[1].record(stream)
+            q.w4a4_linear_static(qa, pw, s, b, L.epilogue, out=y, workspace=ws)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            if it >= 2:
+                t += np.array([ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])])
+        t = t / reps * 1e3     # us
+        ops = 2.0 * L.M * L.N * L.K
+        out.append({"layer": L.name, "quantize_us": round(t[0], 2), "gemm_us": round(t[1], 2),
+                    "gemm_tflops": round(ops / (t[1] * 1e6), 1),
+                    "gemm_frac": round(ops / (t[1] * 1e6) / PEAK_FP8_TFLOPS, 4)})
+        del qa, pw, ws, y
+    tot_ops = sum(2.0 * L.M * L.N * L.K for L in cfg.layers)
+    tot_us = sum(r["gemm_us"] for r in out)
+    return {"step": "quantize_act_static + w4a4_linear_static (workspace) per layer",
+            "gemm_tflops": round(tot_ops / (tot_us * 1e6), 1),
+            "gemm_frac": round(tot_ops / (tot_us * 1e6) / PEAK_FP8_TFLOPS, 4),
+            "per_layer": out}
 
 
 def main():
@@ -336,6 +379,12 @@ def main():
     torch.cuda.synchronize()
     q_stream_gbps = qrounds * qbytes.sum() / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
+    ldm = None
+    if not args.no_ldm:
+        t_l = time.time()
+        ldm = ldm_layers(q, W, torch, np, cfg, dev_in, gs)
+        log(f"LDM-setting layers measured in {time.time() - t_l:.1f}s")
+
     mlp = None
     if not args.no_batched_mlp:
         del outs, dev_in, workspaces
@@ -404,6 +453,7 @@ def main():
         "pack_gbps": round(pack_gbps, 1),
         "per_layer": per_layer,
         "batched_mlp": mlp,
+        "ldm_static": ldm,
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }

@@ -199,6 +199,55 @@ quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* f
                                           size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * The LDM setting (the paper's experimental-details appendix): static
+ * per-tensor activation quantization and per-channel weight quantization,
+ * with the 4-bit LZS compression of Section 3 applied on the fly.
+ *
+ * quartz_quantize_act_static: Stage 1 with one scale s for the whole tensor,
+ * fixed ahead of time (calibration is not part of this library):
+ *   q = clamp(rne(fp32(x * r)), -127, 127),  r = fp32(1 / s)  (values beyond
+ *   127 s clip), then Stage 2 exactly as quartz_quantize_act.
+ *   scale      fp32 s, positive, normal and finite (QUARTZ_ERR_UNSUPPORTED
+ *              otherwise).
+ *   codes, flags   as for quartz_quantize_act; no scales or zero points.
+ *   Other arguments and errors as for quartz_quantize_act.
+ *
+ * quartz_pack_weight_per_channel: one fp16 scale per output channel,
+ *   s_w[n] = fp16(max over all of K of |w[n,k]| / 7) (RNE, saturating),
+ *   wq = clamp(rne(w * (1/s_w[n])), -7, 7); the same packed layout and size
+ *   as quartz_pack_weight (quartz_packed_weight_bytes), with s_w[n] in every
+ *   group's scale slot, so quartz_unpack_weight reads it back alike.
+ *   w_scales   u16 [N] copy of the channel scales, or NULL.
+ *
+ * quartz_w4a4_linear_static: for every output (m, n)
+ *   y[m][n] = bf16( act( act_scale * s_w[n] * I[m,n] + bias[n] ) ),
+ *   I[m,n] = sum over all k of (c[m,k] * 2^FLAG) * wq[n,k],
+ * accumulated by the matrix cores in fp32: exact while every partial sum
+ * stays below 2^24 in magnitude, which |I| <= 784 K guarantees for K <=
+ * 21376 (beyond that, within fp32 rounding of the sum).
+ *   codes, flags   output of quartz_quantize_act_static for M, K, lzs_group.
+ *   act_scale      the s given to quartz_quantize_act_static (any finite fp32).
+ *   w_packed       output of quartz_pack_weight_per_channel for N, K.
+ *   bias_bf16, y_bf16, ldy, epilogue, workspace, workspace_bytes
+ *                  as for quartz_w4a4_linear_ws (the same workspace size
+ *                  query applies; NULL, 0: no split tiles).
+ */
+quartz_status quartz_quantize_act_static(const void* x_bf16, int64_t M, int64_t K, int64_t ldx,
+                                         float scale, int32_t lzs_group, uint8_t* codes,
+                                         uint8_t* flags, hipStream_t stream);
+
+quartz_status quartz_pack_weight_per_channel(const void* w_bf16, int64_t N, int64_t K,
+                                             void* w_packed, uint16_t* w_scales,
+                                             hipStream_t stream);
+
+quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags,
+                                        float act_scale, const void* w_packed,
+                                        const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
+                                        int64_t K, int64_t ldy, int32_t lzs_group,
+                                        int32_t epilogue, void* workspace, size_t workspace_bytes,
+                                        hipStream_t stream);
+
+/*
  * Test / inspection helpers.
  *
  * quartz_unpack_weight: int8 [N][K] weight codes wq recovered from w_packed.

@@ -20,9 +20,10 @@ __all__ = [
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
-    "quartz_w4a4_linear_quantize", "quartz_status_string", "QuantizedAct", "PackedWeight",
+    "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
+    "quartz_w4a4_linear_static", "quartz_status_string", "QuantizedAct", "PackedWeight",
     "quantize_act", "pack_weight", "w4a4_linear", "w4a4_linear_quantize", "gemm_workspace",
-    "linear_schedule",
+    "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "linear_schedule",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
 ]
 
@@ -39,7 +40,8 @@ EXPORTED_SYMBOLS = (
     "quartz_quantize_act", "quartz_packed_weight_bytes", "quartz_pack_weight",
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
-    "quartz_w4a4_linear_quantize", "quartz_status_string",
+    "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
+    "quartz_w4a4_linear_static", "quartz_status_string",
 )
 
 
@@ -80,6 +82,14 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_linear_ws.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32,
                                           P, SZ, P]
     lib.quartz_w4a4_linear_ws.restype = I32
+    F32 = ctypes.c_float
+    lib.quartz_quantize_act_static.argtypes = [P, I64, I64, I64, F32, I32, P, P, P]
+    lib.quartz_quantize_act_static.restype = I32
+    lib.quartz_pack_weight_per_channel.argtypes = [P, I64, I64, P, P, P]
+    lib.quartz_pack_weight_per_channel.restype = I32
+    lib.quartz_w4a4_linear_static.argtypes = [P, P, F32, P, P, P, I64, I64, I64, I64, I32, I32, P,
+                                              ctypes.c_size_t, P]
+    lib.quartz_w4a4_linear_static.restype = I32
     lib.quartz_w4a4_linear_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32,
                                                 I32, I32, P, P, P, P, P, ctypes.c_size_t, P]
     lib.quartz_w4a4_linear_quantize.restype = I32
@@ -141,6 +151,21 @@ def quartz_w4a4_linear_quantize(codes, flags, scales, zeros, w_packed, bias, M, 
                                               K, group_size, lzs_group, epilogue, out_lzs_group,
                                               out_mode, out_codes, out_flags, out_scales,
                                               out_zeros, workspace, workspace_bytes, stream)
+
+
+def quartz_quantize_act_static(x, M, K, ldx, scale, lzs_group, codes, flags, stream) -> int:
+    return load().quartz_quantize_act_static(x, M, K, ldx, scale, lzs_group, codes, flags, stream)
+
+
+def quartz_pack_weight_per_channel(w, N, K, w_packed, w_scales, stream) -> int:
+    return load().quartz_pack_weight_per_channel(w, N, K, w_packed, w_scales, stream)
+
+
+def quartz_w4a4_linear_static(codes, flags, act_scale, w_packed, bias, y, M, N, K, ldy,
+                              lzs_group, epilogue, workspace, workspace_bytes, stream) -> int:
+    return load().quartz_w4a4_linear_static(codes, flags, act_scale, w_packed, bias, y, M, N, K,
+                                            ldy, lzs_group, epilogue, workspace, workspace_bytes,
+                                            stream)
 
 
 def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
@@ -304,6 +329,62 @@ def w4a4_linear_quantize(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: 
                                      _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),
                                      _ptr(workspace), nbytes, _stream_handle(stream))
     _check(st, "quartz_w4a4_linear_quantize")
+    return out
+
+
+def quantize_act_static(x, scale: float, lzs_group: int = 16, stream=None,
+                        out: QuantizedAct | None = None) -> QuantizedAct:
+    """LDM setting: x bf16 [M, K] quantized with one per-tensor fp32 ``scale``
+    (quartz_quantize_act_static); the result has no scales or zero points."""
+    torch = _torch()
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+    M, K = x.shape
+    if out is None:
+        G = K // GROUP
+        out = QuantizedAct(
+            codes=torch.empty((G, M, 32), dtype=torch.uint8, device=x.device),
+            flags=torch.empty((G, M, GROUP // lzs_group), dtype=torch.uint8, device=x.device),
+            scales=None, zeros=None, M=M, K=K, lzs_group=lzs_group)
+    st = quartz_quantize_act_static(_ptr(x), M, K, x.stride(0), float(scale), lzs_group,
+                                    _ptr(out.codes), _ptr(out.flags), _stream_handle(stream))
+    _check(st, "quartz_quantize_act_static")
+    return out
+
+
+def pack_weight_per_channel(w, with_scales: bool = True, stream=None) -> PackedWeight:
+    """LDM setting: w bf16 [N, K] packed with one fp16 scale per output channel
+    (``scales``: int16 [N] fp16 bit patterns)."""
+    torch = _torch()
+    if w.dtype != torch.bfloat16 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous 2-D bf16 tensor")
+    N, K = w.shape
+    nbytes = quartz_packed_weight_bytes(N, K, GROUP)
+    data = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=w.device)
+    scales = torch.empty((N,), dtype=torch.int16, device=w.device) if with_scales else None
+    st = quartz_pack_weight_per_channel(_ptr(w), N, K, _ptr(data), _ptr(scales),
+                                        _stream_handle(stream))
+    _check(st, "quartz_pack_weight_per_channel")
+    return PackedWeight(data=data, scales=scales, N=N, K=K)
+
+
+def w4a4_linear_static(a: QuantizedAct, w: PackedWeight, act_scale: float, bias=None,
+                       epilogue: int = EPI_NONE, out=None, stream=None, workspace=None):
+    """LDM-setting layer (quartz_w4a4_linear_static): ``a`` from quantize_act_static with
+    ``act_scale``, ``w`` from pack_weight_per_channel; returns y bf16 [M, N]."""
+    torch = _torch()
+    if a.K != w.K:
+        raise ValueError("K mismatch between activations and weights")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out is None:
+        out = torch.empty((a.M, w.N), dtype=torch.bfloat16, device=a.codes.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_w4a4_linear_static(_ptr(a.codes), _ptr(a.flags), float(act_scale), _ptr(w.data),
+                                   _ptr(bias), _ptr(out), a.M, w.N, a.K, out.stride(0),
+                                   a.lzs_group, epilogue, _ptr(workspace), nbytes,
+                                   _stream_handle(stream))
+    _check(st, "quartz_w4a4_linear_static")
     return out
 
 

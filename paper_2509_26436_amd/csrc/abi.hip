@@ -1,5 +1,8 @@
 // C-ABI entry points of libquartz.so: host-side validation, then the launch on
 // the caller's stream.  See include/quartz.h for the contract of each call.
+#include <cfloat>
+#include <cmath>
+
 #include "quartz.h"
 #include "quartz_internal.h"
 
@@ -84,6 +87,27 @@ quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int6
                                                 lzs_group, codes, flags, scales, zeros, stream));
 }
 
+quartz_status quartz_quantize_act_static(const void* x_bf16, int64_t M, int64_t K, int64_t ldx,
+                                         float scale, int32_t lzs_group, uint8_t* codes,
+                                         uint8_t* flags, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group) || !(scale >= FLT_MIN) || !std::isfinite(scale))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (!size_ok(M, K) || ldx < K || ldx > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (ldx % 8 != 0)
+        return QUARTZ_ERR_ALIGN;
+    if (M == 0 || K == 0)
+        return QUARTZ_OK;
+    if (!x_bf16 || !codes || !flags)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(x_bf16) || !aligned16(codes) || !aligned16(flags))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_quantize_act_static(static_cast<const uint16_t*>(x_bf16), M, K,
+                                                       ldx, scale, lzs_group, codes, flags,
+                                                       stream));
+}
+
 size_t quartz_packed_weight_bytes(int64_t N, int64_t K, int32_t group_size)
 {
     if (group_size != 64 || N < 0 || K < 0 || K % 64 != 0)
@@ -106,6 +130,23 @@ quartz_status quartz_pack_weight(const void* w_bf16, int64_t N, int64_t K, int32
         return QUARTZ_ERR_ALIGN;
     return from_hip(quartz::launch_pack_weight(static_cast<const uint16_t*>(w_bf16), N, K,
                                                static_cast<uint8_t*>(w_packed), w_scales, stream));
+}
+
+quartz_status quartz_pack_weight_per_channel(const void* w_bf16, int64_t N, int64_t K,
+                                             void* w_packed, uint16_t* w_scales,
+                                             hipStream_t stream)
+{
+    if (!size_ok(N, K))
+        return QUARTZ_ERR_SHAPE;
+    if (N == 0 || K == 0)
+        return QUARTZ_OK;
+    if (!w_bf16 || !w_packed)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(w_bf16) || !aligned16(w_packed) || (w_scales && !aligned16(w_scales)))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_pack_weight_per_channel(static_cast<const uint16_t*>(w_bf16), N,
+                                                           K, static_cast<uint8_t*>(w_packed),
+                                                           w_scales, stream));
 }
 
 quartz_status quartz_unpack_weight(const void* w_packed, int64_t N, int64_t K,
@@ -216,6 +257,40 @@ quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
     return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
                        group_size, lzs_group, epilogue, workspace, workspace_bytes, nullptr,
                        stream);
+}
+
+quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags,
+                                        float act_scale, const void* w_packed,
+                                        const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
+                                        int64_t K, int64_t ldy, int32_t lzs_group,
+                                        int32_t epilogue, void* workspace, size_t workspace_bytes,
+                                        hipStream_t stream)
+{
+    if ((epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH) ||
+        !std::isfinite(act_scale))
+        return QUARTZ_ERR_UNSUPPORTED;
+    quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, 64, lzs_group);
+    if (st != QUARTZ_OK)
+        return st;
+    if (ldy < N || ldy > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (M == 0 || N == 0)
+        return QUARTZ_OK;
+    if (!y_bf16)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(y_bf16) || (bias_bf16 && !aligned16(bias_bf16)) ||
+        (workspace && !aligned16(workspace)))
+        return QUARTZ_ERR_ALIGN;
+    const quartz::GemmSchedule sch =
+        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+    if (sch.blocks <= 0)
+        return QUARTZ_ERR_HIP;
+    if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    return from_hip(quartz::launch_w4a4_linear_static(
+        codes, flags, act_scale, static_cast<const uint8_t*>(w_packed),
+        static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
+        lzs_group, epilogue, sch, workspace, stream));
 }
 
 quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* flags,

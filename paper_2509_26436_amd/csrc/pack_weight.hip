@@ -1,6 +1,10 @@
 // Weight pre-pack: symmetric round-to-nearest int4 per 64-element group along
 // K with an fp16 group scale (the weight setting of Appendix C), written in
 // the GEMM's panel layout (see quartz_internal.h), plus the debug unpack.
+// The per-channel variant (the LDM setting of the experimental-details
+// appendix) first reduces each output channel's max |w| over all of K to one
+// fp16 scale, then packs with it; the scale is stored in every group's scale
+// slot, so the layout is the same.
 //
 // A team of 8 lanes owns one (column n, group g): each lane loads 8 bf16,
 // the team reduces max|w| with DPP, every lane computes
@@ -53,6 +57,8 @@ __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes)
 // fp16 scale.  r = 1/s is one Newton step on the hardware reciprocal, equal to
 // the IEEE quotient for every finite fp16 s; the scale itself keeps the IEEE
 // division (fp16(beta * fp32(1/7)) differs from fp16(beta / 7) for a few beta).
+// PER_CHANNEL: s16 is the channel's scale on entry instead of the group's.
+template <bool PER_CHANNEL>
 __device__ __forceinline__ void pack_group(uint4 v, uint32_t& word, uint32_t& s16)
 {
     const uint32_t d[4] = {v.x, v.y, v.z, v.w};
@@ -62,16 +68,18 @@ __device__ __forceinline__ void pack_group(uint4 v, uint32_t& word, uint32_t& s1
         f[2 * p] = __uint_as_float(d[p] << 16);
         f[2 * p + 1] = __uint_as_float(d[p] & 0xFFFF0000u);
     }
-    float amax = fabsf(f[0]);
+    if constexpr (!PER_CHANNEL) {
+        float amax = fabsf(f[0]);
 #pragma unroll
-    for (int i = 1; i < 8; ++i)
-        amax = fmaxf(amax, fabsf(f[i]));
-    uint32_t ab = __float_as_uint(amax);
-    ab = max(ab, dpp_xor1(ab));
-    ab = max(ab, dpp_xor2(ab));
-    ab = max(ab, dpp_half_mirror(ab));
-    const float beta = __uint_as_float(ab);
-    s16 = f16_bits_rne_sat(beta / 7.0f);
+        for (int i = 1; i < 8; ++i)
+            amax = fmaxf(amax, fabsf(f[i]));
+        uint32_t ab = __float_as_uint(amax);
+        ab = max(ab, dpp_xor1(ab));
+        ab = max(ab, dpp_xor2(ab));
+        ab = max(ab, dpp_half_mirror(ab));
+        const float beta = __uint_as_float(ab);
+        s16 = f16_bits_rne_sat(beta / 7.0f);
+    }
     const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)s16);
     const float r0 = __builtin_amdgcn_rcpf(s);
     const float e = __builtin_fmaf(-s, r0, 1.0f);
@@ -96,6 +104,7 @@ __device__ __forceinline__ void pack_group(uint4 v, uint32_t& word, uint32_t& s1
 // with a grid stride and load the next item before packing the current one.
 // Columns past N read as zero (outside the buffer range) and pack to zero
 // codes and scales, as the padded panel layout requires.
+template <bool PER_CHANNEL>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void pack_weight_kernel(
     const uint16_t* __restrict__ w, int64_t N, int64_t K, int64_t panels,
     uint8_t* __restrict__ w_packed, uint16_t* __restrict__ w_scales)
@@ -143,14 +152,17 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void pack_weight_kernel(
         for (int j = 0; j < kGroupsPerItem; ++j) {
             if (j >= t.ng)
                 break;
-            uint32_t word, s16;
-            pack_group(v[j], word, s16);
+            uint32_t word, s16 = 0;
             const int64_t g = t.g0 + j;
+            if constexpr (PER_CHANNEL)      // written to group 0's slot by row_scale_kernel
+                s16 = reinterpret_cast<const uint16_t*>(
+                    w_packed + t.panel * G * kChunkBytes + kChunkCodeBytes)[cpan];
+            pack_group<PER_CHANNEL>(v[j], word, s16);
             uint8_t* chunk = w_packed + (t.panel * G + g) * kChunkBytes;
             reinterpret_cast<uint32_t*>(chunk + cpan * 32)[u] = word;
-            if (u == 0) {
+            if (u == 0 && (!PER_CHANNEL || g > 0)) {
                 reinterpret_cast<uint16_t*>(chunk + kChunkCodeBytes)[cpan] = (uint16_t)s16;
-                if (n < N && w_scales)
+                if (!PER_CHANNEL && n < N && w_scales)
                     w_scales[n * G + g] = (uint16_t)s16;
             }
         }
@@ -182,6 +194,42 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void pack_weight_kernel(
     }
 }
 
+// One wave per column n of the padded panels: s_w[n] = fp16_rne_sat(max over
+// all of K of |w[n,k]| / 7), written to the scale slot of group 0 of its
+// panel (0 for the padding columns) and to w_scales[n] if given.
+__global__ __launch_bounds__(64 * kWavesPerBlock) void row_scale_kernel(
+    const uint16_t* __restrict__ w, int64_t N, int64_t K, int64_t cols,
+    uint8_t* __restrict__ w_packed, uint16_t* __restrict__ w_scales)
+{
+    const int64_t n = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (n >= cols)
+        return;
+    uint32_t ab = 0;           // max |w| as fp32 bits (non-negative floats order as their bits)
+    if (n < N) {
+        const Rsrc rw = make_rsrc(w + n * K, (uint32_t)(K * 2));
+        for (int64_t k = (int64_t)lane * 8; k < K; k += 64 * 8) {
+            const uint4 v = __builtin_bit_cast(
+                uint4, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(k * 2), 0, kNonTemporal));
+            const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+                ab = max(ab, max((d[p] << 16) & 0x7FFFFFFFu, d[p] & 0x7FFF0000u));
+        }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        ab = max(ab, (uint32_t)__shfl_xor((int)ab, off));
+    if (lane == 0) {
+        const uint32_t s16 = f16_bits_rne_sat(__uint_as_float(ab) / 7.0f);
+        const int64_t G = K / 64;
+        reinterpret_cast<uint16_t*>(w_packed + (n / kPanel) * G * kChunkBytes +
+                                    kChunkCodeBytes)[n % kPanel] = (uint16_t)s16;
+        if (n < N && w_scales)
+            w_scales[n] = (uint16_t)s16;
+    }
+}
+
 // one thread per 8 weights: decode a nibble word back to int8 values
 __global__ __launch_bounds__(256) void unpack_weight_kernel(
     const uint8_t* __restrict__ w_packed, int64_t N, int64_t K, int8_t* __restrict__ wq)
@@ -209,10 +257,9 @@ __global__ __launch_bounds__(256) void unpack_weight_kernel(
     reinterpret_cast<uint2*>(wq + n * K + j * 8)[0] = make_uint2(out[0], out[1]);
 }
 
-}  // namespace
-
-hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
-                              uint16_t* w_scales, hipStream_t stream)
+template <bool PER_CHANNEL>
+hipError_t launch_pack(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
+                       uint16_t* w_scales, hipStream_t stream)
 {
     const int64_t panels = (N + kPanel - 1) / kPanel;
     const int64_t gpairs = (K / 64 + kGroupsPerItem - 1) / kGroupsPerItem;
@@ -220,9 +267,31 @@ hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* 
     // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock,
                                (int64_t)(256 * 32 / kWavesPerBlock));
-    pack_weight_kernel<<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
+    pack_weight_kernel<PER_CHANNEL><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
         w, N, K, panels, w_packed, w_scales);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
+                              uint16_t* w_scales, hipStream_t stream)
+{
+    return launch_pack<false>(w, N, K, w_packed, w_scales, stream);
+}
+
+hipError_t launch_pack_weight_per_channel(const uint16_t* w, int64_t N, int64_t K,
+                                          uint8_t* w_packed, uint16_t* w_scales,
+                                          hipStream_t stream)
+{
+    const int64_t cols = (N + kPanel - 1) / kPanel * kPanel;
+    const int64_t blocks = (cols + kWavesPerBlock - 1) / kWavesPerBlock;
+    row_scale_kernel<<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
+        w, N, K, cols, w_packed, w_scales);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    return launch_pack<true>(w, N, K, w_packed, nullptr, stream);
 }
 
 hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, int8_t* wq,

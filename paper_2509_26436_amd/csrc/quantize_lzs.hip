@@ -68,11 +68,22 @@ __device__ __forceinline__ uint32_t subgroup_or(uint32_t v)
 }
 
 // One group of one lane: 8 bf16 values (a 16-byte load) -> the nibble word,
-// the lane's FLAG and the group's fp16 scale.
-template <int GS>
-__device__ __forceinline__ void quantize_group(uint4 v, uint32_t& word, int& fl, uint32_t& s16)
+// the lane's FLAG and the group's fp16 scale.  STATIC (the LDM setting): the
+// reciprocal r of the caller's per-tensor scale replaces the group's, values
+// beyond 127 s clip, and there is no group scale.
+template <int GS, bool STATIC>
+__device__ __forceinline__ void quantize_group(uint4 v, float r_static, uint32_t& word, int& fl,
+                                               uint32_t& s16)
 {
     const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+    if constexpr (STATIC) {
+        uint32_t p[4];
+        mag_pairs8_t<true>(d, r_static, p);
+        s16 = 0;
+        fl = lzs_flag(subgroup_or<GS>(pairs_or(p)));
+        word = lzs_word(p, sign_nibbles(d), fl);
+        return;
+    }
     // max |x| of the lane's 8 values (the fp32 values are those mag_pairs8
     // forms), then across the team (non-negative floats order as their bits)
     float f[8];
@@ -96,11 +107,11 @@ __device__ __forceinline__ void quantize_group(uint4 v, uint32_t& word, int& fl,
     word = lzs_word(p, sign_nibbles(d), fl);
 }
 
-template <int GS>
+template <int GS, bool STATIC>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
     const uint16_t* __restrict__ x, int64_t M, int64_t G, int64_t ldx, int64_t quads,
     int64_t items, uint8_t* __restrict__ codes, uint8_t* __restrict__ flags,
-    uint16_t* __restrict__ scales, int8_t* __restrict__ zeros)
+    uint16_t* __restrict__ scales, int8_t* __restrict__ zeros, float r_static)
 {
     constexpr int FB = 64 / GS;     // flag bytes per (row, group)
     const int lane = threadIdx.x & 63;
@@ -142,14 +153,14 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
                 break;
             uint32_t word, s16;
             int fl;
-            quantize_group<GS>(v[j], word, fl, s16);
+            quantize_group<GS, STATIC>(v[j], r_static, word, fl, s16);
             const int64_t rg0 = (t.g0 + j) * M + t.row0;     // (group, first row), K-group-major
             const Rsrc rc = make_rsrc(codes + rg0 * 32, (uint32_t)(t.rows * 32));
             __builtin_amdgcn_raw_buffer_store_b32(word, rc, team * 32 + u * 4, 0, 0);
             const Rsrc rf = make_rsrc(flags + rg0 * FB, (uint32_t)(t.rows * FB));
             if ((u & (GS / 8 - 1)) == 0)
                 __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl, rf, team * FB + u / (GS / 8), 0, 0);
-            if (u == 0) {
+            if (!STATIC && u == 0) {
                 const Rsrc rs = make_rsrc(scales + rg0, (uint32_t)(t.rows * 2));
                 __builtin_amdgcn_raw_buffer_store_b16((uint16_t)s16, rs, team * 2, 0, 0);
                 if (zeros) {
@@ -187,9 +198,10 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
     }
 }
 
-template <int GS>
+template <int GS, bool STATIC>
 hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
-                     uint8_t* flags, uint16_t* scales, int8_t* zeros, hipStream_t stream)
+                     uint8_t* flags, uint16_t* scales, int8_t* zeros, float r_static,
+                     hipStream_t stream)
 {
     const int64_t G = K / 64;
     const int64_t quads = (G + kGroupsPerItem - 1) / kGroupsPerItem;
@@ -197,9 +209,26 @@ hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8
     // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
     const int64_t max_blocks = 256 * 32 / kWavesPerBlock;
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock, max_blocks);
-    quantize_act_kernel<GS><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
-        x, M, G, ldx, quads, items, codes, flags, scales, zeros);
+    quantize_act_kernel<GS, STATIC><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
+        x, M, G, ldx, quads, items, codes, flags, scales, zeros, r_static);
     return hipGetLastError();
+}
+
+template <bool STATIC>
+hipError_t launch_any(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int lzs_group,
+                      uint8_t* codes, uint8_t* flags, uint16_t* scales, int8_t* zeros,
+                      float r_static, hipStream_t stream)
+{
+    switch (lzs_group) {
+    case 8:
+        return launch_gs<8, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+    case 16:
+        return launch_gs<16, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+    case 32:
+        return launch_gs<32, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+    default:
+        return launch_gs<64, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+    }
 }
 
 }  // namespace
@@ -208,16 +237,16 @@ hipError_t launch_quantize_act(const uint16_t* x, int64_t M, int64_t K, int64_t 
                                int lzs_group, uint8_t* codes, uint8_t* flags,
                                uint16_t* scales, int8_t* zeros, hipStream_t stream)
 {
-    switch (lzs_group) {
-    case 8:
-        return launch_gs<8>(x, M, K, ldx, codes, flags, scales, zeros, stream);
-    case 16:
-        return launch_gs<16>(x, M, K, ldx, codes, flags, scales, zeros, stream);
-    case 32:
-        return launch_gs<32>(x, M, K, ldx, codes, flags, scales, zeros, stream);
-    default:
-        return launch_gs<64>(x, M, K, ldx, codes, flags, scales, zeros, stream);
-    }
+    return launch_any<false>(x, M, K, ldx, lzs_group, codes, flags, scales, zeros, 0.0f, stream);
+}
+
+hipError_t launch_quantize_act_static(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
+                                      float scale, int lzs_group, uint8_t* codes,
+                                      uint8_t* flags, hipStream_t stream)
+{
+    // r = 1/s, the IEEE quotient (host division)
+    return launch_any<true>(x, M, K, ldx, lzs_group, codes, flags, nullptr, nullptr, 1.0f / scale,
+                            stream);
 }
 
 }  // namespace quartz

@@ -75,6 +75,22 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
                               int64_t ldy, int lzs_group, int epilogue, const GemmSchedule& sch,
                               void* workspace, const QuantOut& qout, hipStream_t stream);
 
+// The LDM setting: codes and flags of quartz_quantize_act_static, w_packed of
+// the per-channel pack (the channel scale in every group's scale slot).
+hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags, float act_scale,
+                                     const uint8_t* w_packed, const uint16_t* bias, uint16_t* y,
+                                     int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group,
+                                     int epilogue, const GemmSchedule& sch, void* workspace,
+                                     hipStream_t stream);
+
+hipError_t launch_quantize_act_static(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
+                                      float scale, int lzs_group, uint8_t* codes,
+                                      uint8_t* flags, hipStream_t stream);
+
+hipError_t launch_pack_weight_per_channel(const uint16_t* w, int64_t N, int64_t K,
+                                          uint8_t* w_packed, uint16_t* w_scales,
+                                          hipStream_t stream);
+
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream);

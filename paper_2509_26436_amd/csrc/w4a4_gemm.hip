@@ -172,14 +172,20 @@ typedef __attribute__((address_space(3))) v4u lds_v4u;
 // output the next tile's first groups are already being staged.  SPLIT
 // instantiations carry the partial-sum code of shared tiles; QOUT ones write
 // the output quantized for the next layer instead of bf16 (QuantOut).
-template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT>
+// STATIC instantiations are the LDM setting (the experimental-details
+// appendix): one per-tensor activation scale and per-channel weight scales,
+// so the K loop has no per-group scales at all: the fp8 MFMAs accumulate the
+// exact integer sum in place and the epilogue applies act_scale * s_w[n].
+template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC>
 __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
-    uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout)
+    uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout, float act_scale)
 {
+    // per-group scales are staged and applied only by the per-group kernels
+    constexpr bool kGroupScales = !I32OUT && !STATIC;
     // three LDS stages: group g + 2 is decoded into one while the math waves
     // read the operands of group g + 1 from another (and multiply group g
     // from registers)
@@ -283,7 +289,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                                       __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
             r.f = load_flags_raw<GS>(rf, f_off);
             r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
-            if constexpr (!I32OUT) {   // the integer path has no scales (scales == nullptr)
+            if constexpr (kGroupScales) {   // the integer and static paths have none
                 const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
                 r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
                 r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
@@ -335,7 +341,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
             *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
             *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
-            if constexpr (!I32OUT) {
+            if constexpr (kGroupScales) {
                 sas[buf][dr] = r.sa;
                 if (d < BN)
                     sws[buf][swc] = r.sw;
@@ -347,38 +353,43 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         // They keep a register ring of three groups in flight and decode two
         // groups ahead of the math waves, one workgroup barrier per group
         // (plus one before the first), the same count the math waves execute.
-        Raw ring[kStages];
+        // The ring is deeper for the static kernel: its steps are short
+        // (fp8 MFMAs only), so three steps of prefetch no longer cover the
+        // load latency.  Its depth is a multiple of the stage count.
+        constexpr int kRing = STATIC ? 2 * kStages : kStages;
+        Raw ring[kRing];
         __builtin_amdgcn_s_setprio(2);
         if (d < 8 * kStages) {
             sas[d >> 3][BM + (d & 7)] = 0;
             sws[d >> 3][BN + (d & 7)] = 0;
         }
         const int steps = gemm_steps(fresh_schedule(), blk);
-        fetch_next(ring[0]);
-        fetch_next(ring[1]);
-        fetch_next(ring[2]);
+#pragma unroll
+        for (int i = 0; i < kRing; ++i)
+            fetch_next(ring[i]);
         stage(ring[0], 0);
         fetch_next(ring[0]);
         stage(ring[1], 1);
         fetch_next(ring[1]);
         lds_sync();
-        // Step s: decode step s + 2 (ring slot and LDS stage (s + 2) % 3) and
-        // refill the slot with step s + 5.  Straight-line code, so the
-        // compiler waits only for the slot being decoded.
+        // Step s (u = s mod kRing): decode step s + 2 (ring slot (s + 2) mod
+        // kRing, LDS stage (s + 2) mod 3) and refill the slot with step
+        // s + 2 + kRing.  Straight-line code, so the compiler waits only for
+        // the slot being decoded.
         auto dstep = [&](int u) {
-            const int k = (u + 2) % kStages;
-            stage(ring[k], k);
+            const int k = (u + 2) % kRing;
+            stage(ring[k], (u + 2) % kStages);
             fetch_next(ring[k]);
             lds_sync();
         };
         int s = 0;
-        for (; s + kStages <= steps; s += kStages) {
+        for (; s + kRing <= steps; s += kRing) {
 #pragma unroll
-            for (int u = 0; u < kStages; ++u)
+            for (int u = 0; u < kRing; ++u)
                 dstep(u);
         }
 #pragma unroll
-        for (int u = 0; u < kStages - 1; ++u)
+        for (int u = 0; u < kRing - 1; ++u)
             if (s + u < steps)
                 dstep(u);
         return;
@@ -432,13 +443,13 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // sums) needs the 16 registers more than its main loop needs the saved
     // instructions (measured: 2.5 % either way).
     typedef int v4i __attribute__((ext_vector_type(4)));
-    constexpr bool kKeepScaleOps = !SPLIT;
+    constexpr bool kKeepScaleOps = !SPLIT && kGroupScales;
     v8i bf, af[TM];
     v4i sa_op[TM], sw_op[TN];
     _Float16 sa_h[TM], sw_h[TN];
     auto load_a = [&](int i, int buf) {
         af[i] = frag_at(As[buf], a_lo, a_hi, i * 32);
-        if constexpr (!I32OUT) {
+        if constexpr (kGroupScales) {
             const uint16_t v = sas[buf][khalf ? BM : wm * WM + i * 32 + l32];
             if constexpr (kKeepScaleOps)
                 sa_op[i][0] = (int)v;
@@ -448,7 +459,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     };
     auto load_b = [&](int j, int buf) {
         bf = frag_at(Bs[buf], b_lo, b_hi, j * 32);
-        if constexpr (!I32OUT) {
+        if constexpr (kGroupScales) {
             const uint16_t v = sws[buf][khalf ? BN : wn * WN + j * 32 + l32];
             if constexpr (kKeepScaleOps)
                 sw_op[j][0] = (int)v;
@@ -521,7 +532,39 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     };
     // one group from LDS stage cb; the next group's operands are prefetched
     // from stage nb unless this is the last group of a segment (LAST)
+    // STATIC: both weight columns in registers (bq), each fp8 MFMA adds its
+    // product to the tile's accumulators in place (exact: every partial sum
+    // is an integer; see include/quartz.h for the K range), and the operands
+    // of the next group are read from stage nb after their last use here.
+    v8i bq[TN];
+    auto load_bq = [&](int j, int buf) { bq[j] = frag_at(Bs[buf], b_lo, b_hi, j * 32); };
+    auto compute_static = [&](int cb, int nb, auto last) {
+        constexpr bool LAST = decltype(last)::value;
+        (void)cb;
+        __builtin_amdgcn_s_setprio(3);
+        acc[0][0] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[0], bq[0], acc[0][0], 0, 0, 0, 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[1], bq[0], acc[1][0], 0, 0, 0, 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+        if (!LAST)
+            load_bq(0, nb);
+        __builtin_amdgcn_s_setprio(3);
+        acc[0][1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[0], bq[1], acc[0][1], 0, 0, 0, 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+        if (!LAST)
+            load_a(0, nb);
+        __builtin_amdgcn_s_setprio(3);
+        acc[1][1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[1], bq[1], acc[1][1], 0, 0, 0, 0, 0, 0);
+        __builtin_amdgcn_s_setprio(0);
+        if (!LAST) {
+            load_a(1, nb);
+            load_bq(1, nb);
+        }
+    };
     auto compute = [&](int cb, int nb, auto last) {
+        if constexpr (STATIC) {
+            compute_static(cb, nb, last);
+            return;
+        }
         constexpr bool LAST = decltype(last)::value;
         // product of tile 0, then the last tile of the previous group
         p_next = mfma_p(0);
@@ -595,7 +638,9 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     const int32_t blk = (int32_t)blockIdx.x;
     // this lane's bias values of the current tile (bf16 bits), loaded when the
     // segment starts so that the output code does not wait for them
-    uint16_t bias_bits[TN];
+    // STATIC: also the channel scales s_w[n] of its columns (fp16 bits, from
+    // the scale slot of group 0 in the packed weight)
+    uint16_t bias_bits[TN], cscale_bits[TN];
     auto load_bias = [&] {
         if constexpr (!I32OUT) {
             const Rsrc rb = make_rsrc(bias, bias ? (uint32_t)(N * 2) : 0u);
@@ -604,6 +649,31 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                 bias_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(
                     rb, (int)(((int64_t)cur.tn * BN + wn * WN + j * 32 + l32) * 2), 0, 0);
         }
+        if constexpr (STATIC) {
+            // the wave's 64 columns are one panel: its group-0 chunk
+            const int64_t panel = (int64_t)cur.tn * (BN / kPanel) + wn;
+            const Rsrc rs = make_rsrc(w_packed + panel * (K / 64) * kChunkBytes + kChunkCodeBytes,
+                                      panel < (N + kPanel - 1) / kPanel ? (uint32_t)(kPanel * 2) : 0u);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                cscale_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(rs, (j * 32 + l32) * 2, 0, 0);
+        }
+    };
+    // the value of acc before bias and activation: acc itself, or for STATIC
+    // the integer sum times act_scale * s_w[n]
+    float cs[TN];
+    auto set_out_scale = [&] {
+        if constexpr (STATIC) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                cs[j] = act_scale * (float)__builtin_bit_cast(_Float16, cscale_bits[j]);
+        }
+    };
+    auto out_value = [&](float a, int j, float bj) {
+        if constexpr (STATIC)
+            return fmaf(a, cs[j], bj);
+        else
+            return a + bj;
     };
     // ---- output quantized for the next layer (QOUT): the bf16 values the
     // plain epilogue would store, run through the activation quantizer with
@@ -625,6 +695,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     auto quantize_out = [&](const v16f (&out)[TM][TN]) {
         if constexpr (QOUT) {
             static_assert(TN == 2 && WN == 64, "one 64-group per wave row");
+            set_out_scale();
             const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
             if (col_base >= N)
                 return;                              // wave-uniform
@@ -641,8 +712,8 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             for (int i = 0; i < TM; ++i) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    float v0 = out[i][0][r] + b[0];
-                    float v1 = out[i][1][r] + b[1];
+                    float v0 = out_value(out[i][0][r], 0, b[0]);
+                    float v1 = out_value(out[i][1][r], 1, b[1]);
                     if constexpr (GELU) {
                         v0 = gelu_tanh(v0);
                         v1 = gelu_tanh(v1);
@@ -787,6 +858,7 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             // rows past M fall outside the range and are dropped, and lanes
             // whose column is past N get an offset outside it.
             static_assert(TN == 2, "the swap pairs the two column tiles");
+            set_out_scale();
             const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
             const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
             float b[TN];
@@ -803,8 +875,8 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             for (int i = 0; i < TM; ++i) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    float v0 = out[i][0][r] + b[0];
-                    float v1 = out[i][1][r] + b[1];
+                    float v0 = out_value(out[i][0][r], 0, b[0]);
+                    float v1 = out_value(out[i][1][r], 1, b[1]);
                     if constexpr (GELU) {
                         v0 = gelu_tanh(v0);
                         v1 = gelu_tanh(v1);
@@ -973,13 +1045,19 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         reset_tile();
         load_a(0, 0);
         load_a(1, 0);
-        load_b(0, 0);
+        if constexpr (STATIC) {
+            load_bq(0, 0);
+            load_bq(1, 0);
+        } else {
+            load_b(0, 0);
+        }
         run_groups(L - 1);
         compute((L - 1) % kStages, 0, std::integral_constant<bool, true>());
         math_barrier();
         for (int p = L; p < padded_steps(L); ++p)
             math_barrier();
-        fma_tile(TM - 1, TN - 1, p_last, s_last);
+        if constexpr (!STATIC)
+            fma_tile(TM - 1, TN - 1, p_last, s_last);
         set_fragment_indices();
         // one output call site, so the epilogue is inlined once
         if (!SPLIT || cur.sg.sk_tile < 0 || finish_partial())
@@ -989,6 +1067,10 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     }
 }
 
+// Output mode of a launch: bf16, quantized for the next layer, or the static
+// (LDM) layer with a bf16 output.
+enum class OutMode { kPlain, kQuant, kStatic };
+
 template <bool B>
 using bool_c = std::integral_constant<bool, B>;
 
@@ -997,31 +1079,35 @@ hipError_t launch_gs(const uint8_t* codes, const uint8_t* flags, const uint16_t*
                      const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                      int64_t M, int64_t N, int64_t K, int64_t ldy, int epilogue,
                      const GemmSchedule& sch, uint32_t* counters, float* slots,
-                     const QuantOut& qout, hipStream_t stream)
+                     const QuantOut& qout, OutMode mode, float act_scale, hipStream_t stream)
 {
     const dim3 grid((unsigned)sch.blocks), block(kThreadsPerBlock);
-    // the epilogue, the split part and the quantized output are compile-time
+    // the epilogue, the split part and the output mode are compile-time
     // choices, so the whole-tile plain kernel carries none of their code
     if constexpr (I32OUT) {
-        w4a4_gemm_kernel<GS, true, false, false, false><<<grid, block, 0, stream>>>(
-            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout);
+        w4a4_gemm_kernel<GS, true, false, false, false, false><<<grid, block, 0, stream>>>(
+            codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout,
+            act_scale);
     } else {
-        auto go = [&](auto gelu, auto split, auto q) {
+        auto go = [&](auto gelu, auto split, auto q, auto st) {
             w4a4_gemm_kernel<GS, false, decltype(gelu)::value, decltype(split)::value,
-                             decltype(q)::value><<<grid, block, 0, stream>>>(
-                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout);
+                             decltype(q)::value, decltype(st)::value><<<grid, block, 0, stream>>>(
+                codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy, sch, counters, slots, qout,
+                act_scale);
         };
-        auto with_q = [&](auto gelu, auto split) {
-            if (qout.codes)
-                go(gelu, split, bool_c<true>());
+        auto with_mode = [&](auto gelu, auto split) {
+            if (mode == OutMode::kQuant)
+                go(gelu, split, bool_c<true>(), bool_c<false>());
+            else if (mode == OutMode::kStatic)
+                go(gelu, split, bool_c<false>(), bool_c<true>());
             else
-                go(gelu, split, bool_c<false>());
+                go(gelu, split, bool_c<false>(), bool_c<false>());
         };
         auto with_split = [&](auto gelu) {
             if (sch.sk_tiles > 0)
-                with_q(gelu, bool_c<true>());
+                with_mode(gelu, bool_c<true>());
             else
-                with_q(gelu, bool_c<false>());
+                with_mode(gelu, bool_c<false>());
         };
         if (epilogue == 1)
             with_split(bool_c<true>());
@@ -1036,21 +1122,21 @@ hipError_t launch(const uint8_t* codes, const uint8_t* flags, const uint16_t* sc
                   const uint8_t* w_packed, const uint16_t* bias, uint16_t* y, int32_t* yi,
                   int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group, int epilogue,
                   const GemmSchedule& sch, uint32_t* counters, float* slots,
-                  const QuantOut& qout, hipStream_t stream)
+                  const QuantOut& qout, OutMode mode, float act_scale, hipStream_t stream)
 {
     switch (lzs_group) {
     case 8:
         return launch_gs<I32OUT, 8>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                    epilogue, sch, counters, slots, qout, stream);
+                                    epilogue, sch, counters, slots, qout, mode, act_scale, stream);
     case 16:
         return launch_gs<I32OUT, 16>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, qout, stream);
+                                     epilogue, sch, counters, slots, qout, mode, act_scale, stream);
     case 32:
         return launch_gs<I32OUT, 32>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, qout, stream);
+                                     epilogue, sch, counters, slots, qout, mode, act_scale, stream);
     default:
         return launch_gs<I32OUT, 64>(codes, flags, scales, w_packed, bias, y, yi, M, N, K, ldy,
-                                     epilogue, sch, counters, slots, qout, stream);
+                                     epilogue, sch, counters, slots, qout, mode, act_scale, stream);
     }
 }
 
@@ -1134,13 +1220,22 @@ int gemm_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false>),
             kThreadsPerBlock, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
     if (dev < kMaxDevices)
         cache[dev].store(n, std::memory_order_relaxed);
     return n;
+}
+
+static void split_workspace(const GemmSchedule& sch, void* workspace, uint32_t*& counters,
+                            float*& slots)
+{
+    counters = static_cast<uint32_t*>(workspace);
+    slots = sch.sk_tiles > 0
+                ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(sch))
+                : nullptr;
 }
 
 hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
@@ -1151,12 +1246,28 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
 {
     if (sch.blocks <= 0)
         return hipErrorInvalidConfiguration;
-    uint32_t* counters = static_cast<uint32_t*>(workspace);
-    float* slots = sch.sk_tiles > 0
-                       ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(sch))
-                       : nullptr;
+    uint32_t* counters;
+    float* slots;
+    split_workspace(sch, workspace, counters, slots);
     return launch<false>(codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
-                         epilogue, sch, counters, slots, qout, stream);
+                         epilogue, sch, counters, slots, qout,
+                         qout.codes ? OutMode::kQuant : OutMode::kPlain, 0.0f, stream);
+}
+
+hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags, float act_scale,
+                                     const uint8_t* w_packed, const uint16_t* bias, uint16_t* y,
+                                     int64_t M, int64_t N, int64_t K, int64_t ldy, int lzs_group,
+                                     int epilogue, const GemmSchedule& sch, void* workspace,
+                                     hipStream_t stream)
+{
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    uint32_t* counters;
+    float* slots;
+    split_workspace(sch, workspace, counters, slots);
+    return launch<false>(codes, flags, nullptr, w_packed, bias, y, nullptr, M, N, K, ldy,
+                         lzs_group, epilogue, sch, counters, slots, QuantOut{}, OutMode::kStatic,
+                         act_scale, stream);
 }
 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
@@ -1167,7 +1278,8 @@ hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
     if (sch.blocks <= 0)
         return hipErrorInvalidConfiguration;
     return launch<true>(codes, flags, nullptr, w_packed, nullptr, nullptr, acc, M, N, K, N,
-                        lzs_group, 0, sch, nullptr, nullptr, QuantOut{}, stream);
+                        lzs_group, 0, sch, nullptr, nullptr, QuantOut{}, OutMode::kPlain, 0.0f,
+                        stream);
 }
 
 }  // namespace quartz

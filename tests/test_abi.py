@@ -147,6 +147,44 @@ def test_linear_quantize_validation(lib):
     assert call(N=0) == OK
 
 
+def test_ldm_entry_validation(lib):
+    qs = q.quartz_quantize_act_static
+    assert qs(A, 8, 128, 128, 0.0, 16, A, A, None) == EUNSUP
+    assert qs(A, 8, 128, 128, -1.0, 16, A, A, None) == EUNSUP
+    assert qs(A, 8, 128, 128, float("inf"), 16, A, A, None) == EUNSUP
+    assert qs(A, 8, 128, 128, float("nan"), 16, A, A, None) == EUNSUP
+    assert qs(A, 8, 128, 128, 1e-40, 16, A, A, None) == EUNSUP      # subnormal: 1/s overflows
+    assert qs(A, 8, 128, 128, 0.01, 12, A, A, None) == EUNSUP
+    assert qs(A, 8, 100, 128, 0.01, 16, A, A, None) == ESHAPE
+    assert qs(A, 8, 128, 64, 0.01, 16, A, A, None) == ESHAPE
+    assert qs(A, 8, 128, 132, 0.01, 16, A, A, None) == EALIGN
+    assert qs(A, 0, 128, 128, 0.01, 16, A, A, None) == OK
+    assert qs(None, 8, 128, 128, 0.01, 16, A, A, None) == ENULL
+    assert qs(A, 8, 128, 128, 0.01, 16, A, None, None) == ENULL
+    assert qs(A, 8, 128, 128, 0.01, 16, A + 2, A, None) == EALIGN
+    pc = q.quartz_pack_weight_per_channel
+    assert pc(A, 8, 100, A, None, None) == ESHAPE
+    assert pc(A, 0, 128, A, None, None) == OK
+    assert pc(None, 8, 128, A, None, None) == ENULL
+    assert pc(A, 8, 128, A + 8, None, None) == EALIGN
+    assert pc(A, 8, 128, A, A + 2, None) == EALIGN
+    ls = q.quartz_w4a4_linear_static
+
+    def call(M=8, N=8, K=128, ldy=8, lzs=16, epi=0, scale=0.01, y=A, codes=A, ws=None, wsb=0):
+        return ls(codes, A, scale, A, None, y, M, N, K, ldy, lzs, epi, ws, wsb, None)
+    assert call(epi=2) == EUNSUP
+    assert call(scale=float("inf")) == EUNSUP
+    assert call(lzs=5) == EUNSUP
+    assert call(K=96) == ESHAPE
+    assert call(ldy=4) == ESHAPE
+    assert call(codes=None) == ENULL
+    assert call(y=None) == ENULL
+    assert call(y=A + 4) == EALIGN
+    assert call(ws=A + 4, wsb=1 << 20) == EALIGN
+    assert call(M=0) == OK
+    assert call(N=0) == OK
+
+
 def test_debug_entry_validation(lib):
     assert q.quartz_unpack_weight(A, 8, 100, 64, A, None) == ESHAPE
     assert q.quartz_unpack_weight(None, 8, 128, 64, A, None) == ENULL
