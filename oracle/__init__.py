@@ -83,6 +83,12 @@ def _load():
     lib.qo_linear_static_f64.argtypes = [P, P, ctypes.c_float, P, P, P, I64, I64, I64, I32, I32,
                                          P, P]
     lib.qo_linear_static_f64.restype = I32
+    lib.qo_quantize_act_asym.argtypes = [P, I64, I64, I64, I32, P, P, P, P, P]
+    lib.qo_quantize_act_asym.restype = I32
+    lib.qo_weight_group_sums.argtypes = [P, I64, I64, P]
+    lib.qo_weight_group_sums.restype = I32
+    lib.qo_linear_asym_f64.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I32, I32, P, P]
+    lib.qo_linear_asym_f64.restype = I32
     lib.qo_round_bf16.argtypes = [P, I64, P]
     lib.qo_round_bf16.restype = None
     lib.qo_num_threads.argtypes = []
@@ -361,4 +367,54 @@ def linear_static_f64(a: ActQuant, scale: float, wq: np.ndarray, sw: np.ndarray,
                                       _ptr(y), _ptr(s))
     if rc != 0:
         raise ValueError("oracle linear_static_f64: invalid arguments")
+    return y, s
+
+
+# ------------------------------------------- asymmetric mode (reading R9)
+
+def quantize_act_asym(x_bits: np.ndarray, lzs_group: int = 16) -> ActQuant:
+    """Asymmetric quantizer: like quantize_act, with the zero points in ``zeros``."""
+    x_bits = _c(x_bits, np.uint16)
+    M, K = x_bits.shape
+    q8 = np.empty((M, K), np.int8)
+    c = np.empty((M, K), np.int8)
+    flags = np.empty((M, K // lzs_group), np.uint8)
+    scales = np.empty((M, K // 64), np.uint16)
+    zeros = np.empty((M, K // 64), np.int8)
+    rc = _load().qo_quantize_act_asym(_ptr(x_bits), M, K, K, lzs_group, _ptr(q8), _ptr(c),
+                                      _ptr(flags), _ptr(scales), _ptr(zeros))
+    if rc != 0:
+        raise ValueError("oracle quantize_act_asym: invalid arguments")
+    return ActQuant(q8, c, flags, scales, zeros, lzs_group)
+
+
+def weight_group_sums(wq: np.ndarray) -> np.ndarray:
+    """int16 [N][K/64] sums of the int4 weight codes over each 64-group."""
+    wq = _c(wq, np.int8)
+    N, K = wq.shape
+    out = np.empty((N, K // 64), np.int16)
+    if _load().qo_weight_group_sums(_ptr(wq), N, K, _ptr(out)) != 0:
+        raise ValueError("oracle weight_group_sums: invalid arguments")
+    return out
+
+
+def linear_asym_f64(a: ActQuant, wq: np.ndarray, sw: np.ndarray, bias_bits=None,
+                    epilogue: int = 0):
+    """Asymmetric-mode layer: returns (y64 float64 [M][N], S float64 [M][N])."""
+    c = _c(a.c, np.int8)
+    flags = _c(a.flags, np.uint8)
+    scales = _c(a.scales, np.uint16)
+    zeros = _c(a.zeros, np.int8)
+    wq = _c(wq, np.int8)
+    sw = _c(sw, np.uint16)
+    bias = None if bias_bits is None else _c(bias_bits, np.uint16)
+    M, K = c.shape
+    N = wq.shape[0]
+    y = np.empty((M, N), np.float64)
+    s = np.empty((M, N), np.float64)
+    rc = _load().qo_linear_asym_f64(_ptr(c), _ptr(flags), _ptr(scales), _ptr(zeros), _ptr(wq),
+                                    _ptr(sw), _ptr(bias), M, N, K, a.lzs_group, epilogue,
+                                    _ptr(y), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle linear_asym_f64: invalid arguments")
     return y, s

@@ -46,6 +46,14 @@
  *       K of |w[n,k]| / 7) and wq = clamp(rne(fp32(w * (1/s_w[n]))), -7, 7).
  *       The layer output is y = s * s_w[n] * I[m,n] + bias with I the exact
  *       integer sum over all of K of d * wq.
+ *   R9  Asymmetric mode (Eq. 1's zero point, repaired so that 255 signed
+ *       levels cover the group's range including 0): lo = min(x_min, 0),
+ *       hi = max(x_max, 0), s = fp16(fp32(hi - lo) / 254) (RNE, saturating),
+ *       r = 1/s (fp32), z = -127 - rne(fp32(lo * r)) in [-127, 127],
+ *       q = clamp(rne(fp32(x * r)) + z, -127, 127); Stage 2 on q as in R3/R4;
+ *       the dequantized value is s * (d - z).  The layer output is
+ *       y = sum_g s_a s_w (P_g - z[m,g] * W_g[n]) + bias, with
+ *       W_g[n] = sum over the group of wq[n,k] (the weight group sums).
  */
 #include <math.h>
 #include <stdint.h>
@@ -460,6 +468,133 @@ int qo_linear_f64_sampled(const int8_t* c, const uint8_t* flags, const uint16_t*
     for (int64_t i = 0; i < count; ++i)
         y[i] = linear_one(c, flags, scales, wq, sw, bias, K, group, lzs_group, epilogue,
                           rows[i], cols[i], absum ? &absum[i] : NULL);
+    return QO_OK;
+}
+
+/* ------------------------------------------ asymmetric mode (reading R9) */
+
+static void stage1_group_asym(const uint16_t* x, int group, int8_t* q, uint16_t* s16_out,
+                              int8_t* z_out)
+{
+    float xmin = 0.0f, xmax = 0.0f;              /* the range always includes 0 */
+    for (int k = 0; k < group; ++k) {
+        float v = qo_bf16_to_f32(x[k]);
+        if (v < xmin)
+            xmin = v;
+        if (v > xmax)
+            xmax = v;
+    }
+    float span = xmax - xmin;                    /* binary32 subtraction */
+    uint16_t s16 = qo_f32_to_f16_rne_sat(span / 254.0f);
+    float s = qo_f16_to_f32(s16);
+    float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+    double zl = qo_rne((double)(xmin * r));      /* in [-254, 0] */
+    int z = -127 - (int)zl;
+    if (z > 127)
+        z = 127;
+    if (z < -127)
+        z = -127;
+    for (int k = 0; k < group; ++k) {
+        float p = qo_bf16_to_f32(x[k]) * r;
+        double v = qo_rne((double)p) + (double)z;
+        if (v > 127.0)
+            v = 127.0;
+        if (v < -127.0)
+            v = -127.0;
+        q[k] = (int8_t)v;
+    }
+    *s16_out = s16;
+    *z_out = (int8_t)z;
+}
+
+/* Asymmetric activation quantizer: outputs as qo_quantize_act, zeros = z. */
+int qo_quantize_act_asym(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int lzs_group,
+                         int8_t* q8, int8_t* c, uint8_t* flags, uint16_t* scales, int8_t* zeros)
+{
+    if (lzs_group < 1 || 64 % lzs_group != 0 || K % 64 != 0 || ldx < K)
+        return QO_EINVAL;
+    const int64_t G = K / 64, S = K / lzs_group;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+        int8_t q[64];
+        for (int64_t g = 0; g < G; ++g) {
+            stage1_group_asym(x + m * ldx + g * 64, 64, q, &scales[m * G + g], &zeros[m * G + g]);
+            if (q8)
+                memcpy(q8 + m * K + g * 64, q, 64);
+            for (int j = 0; j < 64 / lzs_group; ++j) {
+                int64_t sub = g * (64 / lzs_group) + j;
+                flags[m * S + sub] = (uint8_t)qo_lzs_subgroup(
+                    q + j * lzs_group, lzs_group, c + m * K + g * 64 + j * lzs_group);
+            }
+        }
+    }
+    return QO_OK;
+}
+
+/* Weight group sums W_g[n] = sum over group g of wq[n,k], int16 [N][K/64]. */
+int qo_weight_group_sums(const int8_t* wq, int64_t N, int64_t K, int16_t* sums)
+{
+    if (K % 64 != 0)
+        return QO_EINVAL;
+    const int64_t G = K / 64;
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t g = 0; g < G; ++g) {
+            int t = 0;
+            for (int k = 0; k < 64; ++k)
+                t += wq[n * K + g * 64 + k];
+            sums[n * G + g] = (int16_t)t;
+        }
+    return QO_OK;
+}
+
+/*
+ * One output of the asymmetric-mode layer, in double:
+ *   y = sum_g s_a[m,g] s_w[n,g] (P_g[m,n] - z[m,g] W_g[n]) + bias[n]   (then GELU)
+ * *absum receives S = sum_g |s_a s_w (P_g - z W_g)| + |bias|.
+ */
+static double linear_asym_one(const int8_t* c, const uint8_t* flags, const uint16_t* scales,
+                              const int8_t* zeros, const int8_t* wq, const uint16_t* sw,
+                              const uint16_t* bias, int64_t K, int lzs_group, int epilogue,
+                              int64_t m, int64_t n, double* absum)
+{
+    const int64_t G = K / 64;
+    double y = 0.0, a = 0.0;
+    for (int64_t g = 0; g < G; ++g) {
+        int64_t p = 0, wsum = 0;
+        for (int64_t k = g * 64; k < (g + 1) * 64; ++k) {
+            p += (int64_t)decoded(c, flags, K, lzs_group, m, k) * wq[n * K + k];
+            wsum += wq[n * K + k];
+        }
+        int64_t pz = p - (int64_t)zeros[m * G + g] * wsum;
+        double t = (double)qo_f16_to_f32(scales[m * G + g]) * (double)qo_f16_to_f32(sw[n * G + g]) *
+                   (double)pz;
+        y += t;
+        a += fabs(t);
+    }
+    if (bias) {
+        double b = (double)qo_bf16_to_f32(bias[n]);
+        y += b;
+        a += fabs(b);
+    }
+    if (epilogue == 1)
+        y = qo_gelu_tanh(y);
+    if (absum)
+        *absum = a;
+    return y;
+}
+
+int qo_linear_asym_f64(const int8_t* c, const uint8_t* flags, const uint16_t* scales,
+                       const int8_t* zeros, const int8_t* wq, const uint16_t* sw,
+                       const uint16_t* bias, int64_t M, int64_t N, int64_t K, int lzs_group,
+                       int epilogue, double* y, double* absum)
+{
+    if (K % 64 != 0 || lzs_group < 1 || 64 % lzs_group != 0)
+        return QO_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t n = 0; n < N; ++n)
+            y[m * N + n] = linear_asym_one(c, flags, scales, zeros, wq, sw, bias, K, lzs_group,
+                                           epilogue, m, n, absum ? &absum[m * N + n] : NULL);
     return QO_OK;
 }
 
