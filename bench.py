@@ -41,7 +41,8 @@ PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
-                for f in ("w4a4_gemm.hip", "gemm_schedule.h", "quartz_internal.h", "lzs_device.h")]
+                for f in ("w4a4_gemm_kernel.h", "w4a4_gemm.hip", "w4a4_gemm_plain.hip",
+                          "gemm_schedule.h", "quartz_internal.h", "lzs_device.h")]
 
 
 def log(*a):

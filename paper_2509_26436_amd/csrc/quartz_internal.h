@@ -66,6 +66,31 @@ struct QuantOut {
     int32_t lzs;         // LZS subgroup size of the output: 8, 16, 32 or 64
 };
 
+// Arguments of one GEMM launch (see the kernel template in w4a4_gemm_kernel.h).
+struct GemmLaunch {
+    const uint8_t* codes;
+    const uint8_t* flags;
+    const uint16_t* scales;
+    const uint8_t* w_packed;
+    const uint16_t* bias;
+    uint16_t* y;
+    int32_t* yi;
+    int64_t M, N, K, ldy;
+    int lzs_group;
+    int epilogue;
+    GemmSchedule sch;
+    uint32_t* counters;
+    float* slots;
+    QuantOut qout;
+    float act_scale;
+};
+
+// One output mode each (w4a4_gemm_<mode>.hip).
+hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);
+
 // `workspace`: gemm_workspace_bytes(sch) bytes whose counter part is zero
 // (left zero again by the launch); unused unless sch.sk_tiles > 0.  With
 // qout.codes set, y is not written and N % 64 == 0.
