@@ -54,7 +54,7 @@ typedef enum quartz_status {
     QUARTZ_ERR_WORKSPACE = 6    /* workspace smaller than the size query asks for */
 } quartz_status;
 
-enum { QUARTZ_MODE_SYMMETRIC = 0 };
+enum { QUARTZ_MODE_SYMMETRIC = 0, QUARTZ_MODE_ASYMMETRIC = 1 };
 enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
 
 /*
@@ -63,7 +63,14 @@ enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
  *
  *   x_bf16  bf16 [M][ldx], row-major, K <= ldx <= 2^24, ldx % 8 == 0.
  *   M, K    rows (tokens) and reduction size; K % 64 == 0.
- *   mode    QUARTZ_MODE_SYMMETRIC (s = max|x| / 127 per 64-group, zero point 0).
+ *   mode    QUARTZ_MODE_SYMMETRIC (s = max|x| / 127 per 64-group, zero point 0), or
+ *           QUARTZ_MODE_ASYMMETRIC: Eq. 1's zero point, with the range repaired
+ *           so that the 255 signed levels cover it: lo = min(x_min, 0),
+ *           hi = max(x_max, 0), s = fp16(fp32(hi - lo) / 254) (RNE,
+ *           saturating), r = fp32(1/s), z = clamp(-127 - rne(fp32(lo r)),
+ *           -127, 127), q = clamp(rne(fp32(x r)) + z, -127, 127); Stage 2 then
+ *           acts on q; the decoded value is s * (c * 2^FLAG - z).  zeros is
+ *           required (QUARTZ_ERR_NULL otherwise).
  * Outputs, K-group-major (all rows of 64-group 0, then all rows of group 1, ...),
  * so that one group of a tile of rows is one contiguous run for the GEMM:
  *   codes   u8  [K/64][M][32]   4-bit codes c in [-7, 7] of the 64 elements of
@@ -76,8 +83,9 @@ enum { QUARTZ_EPI_NONE = 0, QUARTZ_EPI_GELU_TANH = 1 };
  *   flags   u8  [K/64][M][64/lzs_group]  FLAG in 0..4 of each subgroup.
  *   scales  u16 [K/64][M]   fp16 scale s of each (group, row): fp16(max|x| / 127),
  *                         round-to-nearest-even, saturating at 65504.
- *   zeros   i8  [K/64][M] or NULL; the symmetric mode writes 0.
- * The decoded activation is x~ = s * c * 2^FLAG.
+ *   zeros   i8  [K/64][M] zero point z of each (group, row); may be NULL in
+ *           the symmetric mode, which writes 0.
+ * The decoded activation is x~ = s * (c * 2^FLAG - z).
  * M = 0 returns QUARTZ_OK without launching.
  */
 quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int64_t ldx,
@@ -197,6 +205,38 @@ quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* f
                                           uint8_t* out_codes, uint8_t* out_flags,
                                           uint16_t* out_scales, int8_t* out_zeros, void* workspace,
                                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The asymmetric mode (Eq. 1's zero point; the activation side is
+ * QUARTZ_MODE_ASYMMETRIC of quartz_quantize_act).  With x~ = s_a (d - z),
+ * d = c * 2^FLAG, the group product of the layer is
+ *   sum over the group of (d - z) wq = P_g - z[m,g] * W_g[n],
+ *   W_g[n] = sum over the 64 k of group g of wq[n,k]  (the weight group sums),
+ * so that for every output (m, n)
+ *   y[m][n] = bf16( act( sum_g s_a[m,g] s_w[n,g] (P_g - z[m,g] W_g[n]) + bias[n] ) ).
+ * P_g - z W_g is exact (|.| < 2^17) before the fp32 scaling.
+ *
+ * quartz_weight_group_sums: W_g[n] from a packed weight (once per layer).
+ *   w_packed   output of quartz_pack_weight for N, K.
+ *   w_sums     i16 [K/64][N] (group-major), caller-allocated.
+ *
+ * quartz_w4a4_linear_asym: the layer above.
+ *   codes, flags, scales, zeros   outputs of quartz_quantize_act in
+ *                                 QUARTZ_MODE_ASYMMETRIC (zeros required).
+ *   w_packed, w_sums              quartz_pack_weight and quartz_weight_group_sums.
+ *   The other arguments are those of quartz_w4a4_linear_ws (the same
+ *   workspace size query applies; NULL, 0: no split tiles).
+ */
+quartz_status quartz_weight_group_sums(const void* w_packed, int64_t N, int64_t K,
+                                      int32_t group_size, int16_t* w_sums, hipStream_t stream);
+
+quartz_status quartz_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
+                                      const uint16_t* scales, const int8_t* zeros,
+                                      const void* w_packed, const int16_t* w_sums,
+                                      const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
+                                      int64_t K, int64_t ldy, int32_t group_size,
+                                      int32_t lzs_group, int32_t epilogue, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
 
 /*
  * The LDM setting (the paper's experimental-details appendix): static

@@ -21,9 +21,11 @@ __all__ = [
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
-    "quartz_w4a4_linear_static", "quartz_status_string", "QuantizedAct", "PackedWeight",
+    "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
+    "quartz_status_string", "QuantizedAct", "PackedWeight",
     "quantize_act", "pack_weight", "w4a4_linear", "w4a4_linear_quantize", "gemm_workspace",
-    "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "linear_schedule",
+    "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "weight_group_sums",
+    "w4a4_linear_asym", "linear_schedule",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
 ]
 
@@ -32,6 +34,7 @@ _LIB_PATH = os.path.join(_HERE, "libquartz.so")
 
 QUARTZ_OK = 0
 MODE_SYMMETRIC = 0
+MODE_ASYMMETRIC = 1
 EPI_NONE = 0
 EPI_GELU_TANH = 1
 GROUP = 64
@@ -41,7 +44,8 @@ EXPORTED_SYMBOLS = (
     "quartz_w4a4_linear", "quartz_w4a4_linear_workspace_bytes", "quartz_w4a4_linear_ws",
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
-    "quartz_w4a4_linear_static", "quartz_status_string",
+    "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
+    "quartz_status_string",
 )
 
 
@@ -90,6 +94,11 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_linear_static.argtypes = [P, P, F32, P, P, P, I64, I64, I64, I64, I32, I32, P,
                                               ctypes.c_size_t, P]
     lib.quartz_w4a4_linear_static.restype = I32
+    lib.quartz_weight_group_sums.argtypes = [P, I64, I64, I32, P, P]
+    lib.quartz_weight_group_sums.restype = I32
+    lib.quartz_w4a4_linear_asym.argtypes = [P, P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32,
+                                            I32, P, ctypes.c_size_t, P]
+    lib.quartz_w4a4_linear_asym.restype = I32
     lib.quartz_w4a4_linear_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32,
                                                 I32, I32, P, P, P, P, P, ctypes.c_size_t, P]
     lib.quartz_w4a4_linear_quantize.restype = I32
@@ -168,6 +177,18 @@ def quartz_w4a4_linear_static(codes, flags, act_scale, w_packed, bias, y, M, N, 
                                             stream)
 
 
+def quartz_weight_group_sums(w_packed, N, K, group_size, w_sums, stream) -> int:
+    return load().quartz_weight_group_sums(w_packed, N, K, group_size, w_sums, stream)
+
+
+def quartz_w4a4_linear_asym(codes, flags, scales, zeros, w_packed, w_sums, bias, y, M, N, K,
+                            ldy, group_size, lzs_group, epilogue, workspace, workspace_bytes,
+                            stream) -> int:
+    return load().quartz_w4a4_linear_asym(codes, flags, scales, zeros, w_packed, w_sums, bias, y,
+                                          M, N, K, ldy, group_size, lzs_group, epilogue,
+                                          workspace, workspace_bytes, stream)
+
+
 def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
     return int(load().quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments,
                                                   capacity))
@@ -226,8 +247,9 @@ class PackedWeight:
 
 
 def quantize_act(x, lzs_group: int = 16, with_zeros: bool = False, stream=None,
-                 out: QuantizedAct | None = None) -> QuantizedAct:
-    """x: bf16 [M, K] CUDA tensor whose rows are 16-byte aligned (stride(1) == 1)."""
+                 out: QuantizedAct | None = None, mode: int = MODE_SYMMETRIC) -> QuantizedAct:
+    """x: bf16 [M, K] CUDA tensor whose rows are 16-byte aligned (stride(1) == 1).
+    ``mode=MODE_ASYMMETRIC`` always returns the zero points."""
     torch = _torch()
     if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
         raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
@@ -240,9 +262,10 @@ def quantize_act(x, lzs_group: int = 16, with_zeros: bool = False, stream=None,
             codes=torch.empty((G, M, 32), dtype=torch.uint8, device=dev),
             flags=torch.empty((G, M, GROUP // lzs_group), dtype=torch.uint8, device=dev),
             scales=torch.empty((G, M), dtype=torch.int16, device=dev),
-            zeros=torch.empty((G, M), dtype=torch.int8, device=dev) if with_zeros else None,
+            zeros=(torch.empty((G, M), dtype=torch.int8, device=dev)
+                   if with_zeros or mode == MODE_ASYMMETRIC else None),
             M=M, K=K, lzs_group=lzs_group)
-    st = quartz_quantize_act(_ptr(x), M, K, ldx, GROUP, lzs_group, MODE_SYMMETRIC,
+    st = quartz_quantize_act(_ptr(x), M, K, ldx, GROUP, lzs_group, mode,
                              _ptr(out.codes), _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),
                              _stream_handle(stream))
     _check(st, "quartz_quantize_act")
@@ -385,6 +408,35 @@ def w4a4_linear_static(a: QuantizedAct, w: PackedWeight, act_scale: float, bias=
                                    a.lzs_group, epilogue, _ptr(workspace), nbytes,
                                    _stream_handle(stream))
     _check(st, "quartz_w4a4_linear_static")
+    return out
+
+
+def weight_group_sums(w: PackedWeight, stream=None):
+    """int16 [K/64, N] sums of the int4 weight codes over each 64-group."""
+    torch = _torch()
+    out = torch.empty((w.K // GROUP, w.N), dtype=torch.int16, device=w.data.device)
+    st = quartz_weight_group_sums(_ptr(w.data), w.N, w.K, GROUP, _ptr(out), _stream_handle(stream))
+    _check(st, "quartz_weight_group_sums")
+    return out
+
+
+def w4a4_linear_asym(a: QuantizedAct, w: PackedWeight, w_sums, bias=None,
+                     epilogue: int = EPI_NONE, out=None, stream=None, workspace=None):
+    """Asymmetric-mode layer (quartz_w4a4_linear_asym): ``a`` from quantize_act with
+    ``mode=MODE_ASYMMETRIC``, ``w_sums`` from weight_group_sums(w)."""
+    torch = _torch()
+    if a.K != w.K or a.zeros is None:
+        raise ValueError("need asymmetric activations with zero points and matching K")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out is None:
+        out = torch.empty((a.M, w.N), dtype=torch.bfloat16, device=a.codes.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_w4a4_linear_asym(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                                 _ptr(w.data), _ptr(w_sums), _ptr(bias), _ptr(out), a.M, w.N, a.K,
+                                 out.stride(0), GROUP, a.lzs_group, epilogue, _ptr(workspace),
+                                 nbytes, _stream_handle(stream))
+    _check(st, "quartz_w4a4_linear_asym")
     return out
 
 

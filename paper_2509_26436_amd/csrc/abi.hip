@@ -70,7 +70,8 @@ quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int6
                                   uint8_t* codes, uint8_t* flags, uint16_t* scales,
                                   int8_t* zeros, hipStream_t stream)
 {
-    if (group_size != 64 || !lzs_ok(lzs_group) || mode != QUARTZ_MODE_SYMMETRIC)
+    if (group_size != 64 || !lzs_ok(lzs_group) ||
+        (mode != QUARTZ_MODE_SYMMETRIC && mode != QUARTZ_MODE_ASYMMETRIC))
         return QUARTZ_ERR_UNSUPPORTED;
     if (!size_ok(M, K) || ldx < K || ldx > kMaxLd)
         return QUARTZ_ERR_SHAPE;
@@ -78,13 +79,14 @@ quartz_status quartz_quantize_act(const void* x_bf16, int64_t M, int64_t K, int6
         return QUARTZ_ERR_ALIGN;       // 16-byte aligned rows for the vector loads
     if (M == 0 || K == 0)
         return QUARTZ_OK;
-    if (!x_bf16 || !codes || !flags || !scales)
+    if (!x_bf16 || !codes || !flags || !scales || (mode == QUARTZ_MODE_ASYMMETRIC && !zeros))
         return QUARTZ_ERR_NULL;
     if (!aligned16(x_bf16) || !aligned16(codes) || !aligned16(flags) || !aligned16(scales) ||
         (zeros && !aligned16(zeros)))
         return QUARTZ_ERR_ALIGN;
     return from_hip(quartz::launch_quantize_act(static_cast<const uint16_t*>(x_bf16), M, K, ldx,
-                                                lzs_group, codes, flags, scales, zeros, stream));
+                                                lzs_group, codes, flags, scales, zeros,
+                                                mode == QUARTZ_MODE_ASYMMETRIC, stream));
 }
 
 quartz_status quartz_quantize_act_static(const void* x_bf16, int64_t M, int64_t K, int64_t ldx,
@@ -147,6 +149,23 @@ quartz_status quartz_pack_weight_per_channel(const void* w_bf16, int64_t N, int6
     return from_hip(quartz::launch_pack_weight_per_channel(static_cast<const uint16_t*>(w_bf16), N,
                                                            K, static_cast<uint8_t*>(w_packed),
                                                            w_scales, stream));
+}
+
+quartz_status quartz_weight_group_sums(const void* w_packed, int64_t N, int64_t K,
+                                      int32_t group_size, int16_t* w_sums, hipStream_t stream)
+{
+    if (group_size != 64)
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (!size_ok(N, K))
+        return QUARTZ_ERR_SHAPE;
+    if (N == 0 || K == 0)
+        return QUARTZ_OK;
+    if (!w_packed || !w_sums)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(w_packed) || !aligned16(w_sums))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_weight_group_sums(static_cast<const uint8_t*>(w_packed), N, K,
+                                                     w_sums, stream));
 }
 
 quartz_status quartz_unpack_weight(const void* w_packed, int64_t N, int64_t K,
@@ -289,6 +308,40 @@ quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* fla
         return QUARTZ_ERR_WORKSPACE;
     return from_hip(quartz::launch_w4a4_linear_static(
         codes, flags, act_scale, static_cast<const uint8_t*>(w_packed),
+        static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
+        lzs_group, epilogue, sch, workspace, stream));
+}
+
+quartz_status quartz_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
+                                      const uint16_t* scales, const int8_t* zeros,
+                                      const void* w_packed, const int16_t* w_sums,
+                                      const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
+                                      int64_t K, int64_t ldy, int32_t group_size,
+                                      int32_t lzs_group, int32_t epilogue, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream)
+{
+    if (epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH)
+        return QUARTZ_ERR_UNSUPPORTED;
+    quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, group_size, lzs_group);
+    if (st != QUARTZ_OK)
+        return st;
+    if (ldy < N || ldy > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (M == 0 || N == 0)
+        return QUARTZ_OK;
+    if (!scales || !zeros || !w_sums || !y_bf16)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(scales) || !aligned16(zeros) || !aligned16(w_sums) || !aligned16(y_bf16) ||
+        (bias_bf16 && !aligned16(bias_bf16)) || (workspace && !aligned16(workspace)))
+        return QUARTZ_ERR_ALIGN;
+    const quartz::GemmSchedule sch =
+        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+    if (sch.blocks <= 0)
+        return QUARTZ_ERR_HIP;
+    if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    return from_hip(quartz::launch_w4a4_linear_asym(
+        codes, flags, scales, zeros, static_cast<const uint8_t*>(w_packed), w_sums,
         static_cast<const uint16_t*>(bias_bf16), static_cast<uint16_t*>(y_bf16), M, N, K, ldy,
         lzs_group, epilogue, sch, workspace, stream));
 }

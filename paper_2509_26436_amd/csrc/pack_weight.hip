@@ -230,6 +230,37 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void row_scale_kernel(
     }
 }
 
+// One thread per (group g, column n): the sum of the 64 int4 weight codes of
+// that group, int16 [K/64][N] (the weight group sums of the asymmetric mode).
+__global__ __launch_bounds__(256) void weight_sums_kernel(const uint8_t* __restrict__ w_packed,
+                                                          int64_t N, int64_t K,
+                                                          int16_t* __restrict__ sums)
+{
+    const int64_t G = K / 64;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= G * N)
+        return;
+    const int64_t g = t / N;
+    const int64_t n = t - g * N;
+    const uint4* src = reinterpret_cast<const uint4*>(
+        w_packed + ((n / kPanel) * G + g) * kChunkBytes + (n % kPanel) * 32);
+    int total = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint4 v = src[h];
+        const uint32_t words[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t nib = (words[w] >> (4 * i)) & 0xFu;
+                const int mag = (int)(nib & 7u);
+                total += (nib & 8u) ? -mag : mag;
+            }
+    }
+    sums[g * N + n] = (int16_t)total;
+}
+
 // one thread per 8 weights: decode a nibble word back to int8 values
 __global__ __launch_bounds__(256) void unpack_weight_kernel(
     const uint8_t* __restrict__ w_packed, int64_t N, int64_t K, int8_t* __restrict__ wq)
@@ -292,6 +323,15 @@ hipError_t launch_pack_weight_per_channel(const uint16_t* w, int64_t N, int64_t 
     if (e != hipSuccess)
         return e;
     return launch_pack<true>(w, N, K, w_packed, nullptr, stream);
+}
+
+hipError_t launch_weight_group_sums(const uint8_t* w_packed, int64_t N, int64_t K,
+                                    int16_t* sums, hipStream_t stream)
+{
+    const int64_t threads = N * (K / 64);
+    const int64_t blocks = (threads + 255) / 256;
+    weight_sums_kernel<<<dim3((unsigned)blocks), dim3(256), 0, stream>>>(w_packed, N, K, sums);
+    return hipGetLastError();
 }
 
 hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, int8_t* wq,

@@ -28,6 +28,10 @@ constexpr int kNonTemporal = 2;                // cache policy: x is streamed on
 constexpr int kGroupsPerItem = 2;
 constexpr int kWavesPerBlock = 4;
 
+// Stage-1 modes: symmetric per group (Eq. 1, reading R1), static per tensor
+// (the LDM setting), asymmetric per group (Eq. 1's zero point, repaired).
+enum { kModeSym = 0, kModeStatic = 1, kModeAsym = 2 };
+
 // DPP controls (gfx9 encoding).
 constexpr int kQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]
 constexpr int kQuadXor2 = 0x4E;     // quad_perm [2,3,0,1]
@@ -54,6 +58,22 @@ __device__ __forceinline__ uint32_t team8_max(uint32_t v)
     return v;
 }
 
+// min / max of floats over the 8 lanes of a team
+__device__ __forceinline__ float team8_fmin(float v)
+{
+    v = fminf(v, __uint_as_float(dpp<kQuadXor1>(__float_as_uint(v))));
+    v = fminf(v, __uint_as_float(dpp<kQuadXor2>(__float_as_uint(v))));
+    v = fminf(v, __uint_as_float(dpp<kHalfMirror>(__float_as_uint(v))));
+    return v;
+}
+__device__ __forceinline__ float team8_fmax(float v)
+{
+    v = fmaxf(v, __uint_as_float(dpp<kQuadXor1>(__float_as_uint(v))));
+    v = fmaxf(v, __uint_as_float(dpp<kQuadXor2>(__float_as_uint(v))));
+    v = fmaxf(v, __uint_as_float(dpp<kHalfMirror>(__float_as_uint(v))));
+    return v;
+}
+
 // OR over the lanes that share one LZS subgroup (G_s / 8 lanes)
 template <int GS>
 __device__ __forceinline__ uint32_t subgroup_or(uint32_t v)
@@ -68,15 +88,59 @@ __device__ __forceinline__ uint32_t subgroup_or(uint32_t v)
 }
 
 // One group of one lane: 8 bf16 values (a 16-byte load) -> the nibble word,
-// the lane's FLAG and the group's fp16 scale.  STATIC (the LDM setting): the
-// reciprocal r of the caller's per-tensor scale replaces the group's, values
-// beyond 127 s clip, and there is no group scale.
-template <int GS, bool STATIC>
+// the lane's FLAG and the group's fp16 scale.  kModeStatic (the LDM
+// setting): the reciprocal r of the caller's per-tensor scale replaces the
+// group's, values beyond 127 s clip, and there is no group scale.
+// kModeAsym: the group's range [min(x_min, 0), max(x_max, 0)] spread over
+// the 255 signed levels: s = fp16(span / 254), z = -127 - rne(lo r),
+// q = clamp(rne(x r) + z, -127, 127), then Stage 2 on q (its sign and
+// magnitude, not those of x); z8 receives z.
+template <int GS, int MODE>
 __device__ __forceinline__ void quantize_group(uint4 v, float r_static, uint32_t& word, int& fl,
-                                               uint32_t& s16)
+                                               uint32_t& s16, int& z8)
 {
     const uint32_t d[4] = {v.x, v.y, v.z, v.w};
-    if constexpr (STATIC) {
+    z8 = 0;
+    if constexpr (MODE == kModeAsym) {
+        float f[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            f[2 * k] = __uint_as_float(d[k] << 16);
+            f[2 * k + 1] = __uint_as_float(d[k] & 0xFFFF0000u);
+        }
+        float mn = 0.0f, mx = 0.0f;              // the range always includes 0
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            mn = fminf(mn, f[i]);
+            mx = fmaxf(mx, f[i]);
+        }
+        mn = team8_fmin(mn);
+        mx = team8_fmax(mx);
+        const float span = mx - mn;
+        const _Float16 h = (_Float16)(span / 254.0f);
+        s16 = min((uint32_t)__builtin_bit_cast(uint16_t, h), 0x7BFFu);
+        const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)s16);
+        const float r0 = __builtin_amdgcn_rcpf(s);
+        const float e = __builtin_fmaf(-s, r0, 1.0f);
+        const float r = s16 == 0 ? 0.0f : __builtin_fmaf(r0, e, r0);
+        // rne of a value in (-2^22, 2^22) from the low bits of fp32(v + 1.5 * 2^23)
+        auto rne_int = [](float t) { return (int)(__float_as_uint(t + kMagic) - kMagicBits); };
+        const int z = min(max(-127 - rne_int(mn * r), -127), 127);
+        z8 = z;
+        uint32_t p[4], S = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int q0 = min(max(rne_int(f[2 * k] * r) + z, -127), 127);
+            const int q1 = min(max(rne_int(f[2 * k + 1] * r) + z, -127), 127);
+            p[k] = (uint32_t)abs(q0) | ((uint32_t)abs(q1) << 16);
+            S |= ((uint32_t)q0 >> 31) << (3 + 4 * k);
+            S |= ((uint32_t)q1 >> 31) << (19 + 4 * k);
+        }
+        fl = lzs_flag(subgroup_or<GS>(pairs_or(p)));
+        word = lzs_word(p, S, fl);
+        return;
+    }
+    if constexpr (MODE == kModeStatic) {
         uint32_t p[4];
         mag_pairs8_t<true>(d, r_static, p);
         s16 = 0;
@@ -107,7 +171,7 @@ __device__ __forceinline__ void quantize_group(uint4 v, float r_static, uint32_t
     word = lzs_word(p, sign_nibbles(d), fl);
 }
 
-template <int GS, bool STATIC>
+template <int GS, int MODE>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
     const uint16_t* __restrict__ x, int64_t M, int64_t G, int64_t ldx, int64_t quads,
     int64_t items, uint8_t* __restrict__ codes, uint8_t* __restrict__ flags,
@@ -152,20 +216,20 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
             if (j >= t.ng)
                 break;
             uint32_t word, s16;
-            int fl;
-            quantize_group<GS, STATIC>(v[j], r_static, word, fl, s16);
+            int fl, z8;
+            quantize_group<GS, MODE>(v[j], r_static, word, fl, s16, z8);
             const int64_t rg0 = (t.g0 + j) * M + t.row0;     // (group, first row), K-group-major
             const Rsrc rc = make_rsrc(codes + rg0 * 32, (uint32_t)(t.rows * 32));
             __builtin_amdgcn_raw_buffer_store_b32(word, rc, team * 32 + u * 4, 0, 0);
             const Rsrc rf = make_rsrc(flags + rg0 * FB, (uint32_t)(t.rows * FB));
             if ((u & (GS / 8 - 1)) == 0)
                 __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl, rf, team * FB + u / (GS / 8), 0, 0);
-            if (!STATIC && u == 0) {
+            if (MODE != kModeStatic && u == 0) {
                 const Rsrc rs = make_rsrc(scales + rg0, (uint32_t)(t.rows * 2));
                 __builtin_amdgcn_raw_buffer_store_b16((uint16_t)s16, rs, team * 2, 0, 0);
                 if (zeros) {
                     const Rsrc rz = make_rsrc(zeros + rg0, (uint32_t)t.rows);
-                    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)0, rz, team, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)z8, rz, team, 0, 0);
                 }
             }
         }
@@ -198,7 +262,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void quantize_act_kernel(
     }
 }
 
-template <int GS, bool STATIC>
+template <int GS, int MODE>
 hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8_t* codes,
                      uint8_t* flags, uint16_t* scales, int8_t* zeros, float r_static,
                      hipStream_t stream)
@@ -209,25 +273,25 @@ hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8
     // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
     const int64_t max_blocks = 256 * 32 / kWavesPerBlock;
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock, max_blocks);
-    quantize_act_kernel<GS, STATIC><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
+    quantize_act_kernel<GS, MODE><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
         x, M, G, ldx, quads, items, codes, flags, scales, zeros, r_static);
     return hipGetLastError();
 }
 
-template <bool STATIC>
+template <int MODE>
 hipError_t launch_any(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int lzs_group,
                       uint8_t* codes, uint8_t* flags, uint16_t* scales, int8_t* zeros,
                       float r_static, hipStream_t stream)
 {
     switch (lzs_group) {
     case 8:
-        return launch_gs<8, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+        return launch_gs<8, MODE>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
     case 16:
-        return launch_gs<16, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+        return launch_gs<16, MODE>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
     case 32:
-        return launch_gs<32, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+        return launch_gs<32, MODE>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
     default:
-        return launch_gs<64, STATIC>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
+        return launch_gs<64, MODE>(x, M, K, ldx, codes, flags, scales, zeros, r_static, stream);
     }
 }
 
@@ -235,9 +299,14 @@ hipError_t launch_any(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, int 
 
 hipError_t launch_quantize_act(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
                                int lzs_group, uint8_t* codes, uint8_t* flags,
-                               uint16_t* scales, int8_t* zeros, hipStream_t stream)
+                               uint16_t* scales, int8_t* zeros, bool asymmetric,
+                               hipStream_t stream)
 {
-    return launch_any<false>(x, M, K, ldx, lzs_group, codes, flags, scales, zeros, 0.0f, stream);
+    if (asymmetric)
+        return launch_any<kModeAsym>(x, M, K, ldx, lzs_group, codes, flags, scales, zeros, 0.0f,
+                                     stream);
+    return launch_any<kModeSym>(x, M, K, ldx, lzs_group, codes, flags, scales, zeros, 0.0f,
+                                stream);
 }
 
 hipError_t launch_quantize_act_static(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
@@ -245,7 +314,7 @@ hipError_t launch_quantize_act_static(const uint16_t* x, int64_t M, int64_t K, i
                                       uint8_t* flags, hipStream_t stream)
 {
     // r = 1/s, the IEEE quotient (host division)
-    return launch_any<true>(x, M, K, ldx, lzs_group, codes, flags, nullptr, nullptr, 1.0f / scale,
+    return launch_any<kModeStatic>(x, M, K, ldx, lzs_group, codes, flags, nullptr, nullptr, 1.0f / scale,
                             stream);
 }
 

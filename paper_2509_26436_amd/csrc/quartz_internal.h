@@ -37,10 +37,14 @@ constexpr int64_t kGemmBlockCols = 128;
 // C-ABI layer before these are called.
 hipError_t launch_quantize_act(const uint16_t* x, int64_t M, int64_t K, int64_t ldx,
                                int lzs_group, uint8_t* codes, uint8_t* flags,
-                               uint16_t* scales, int8_t* zeros, hipStream_t stream);
+                               uint16_t* scales, int8_t* zeros, bool asymmetric,
+                               hipStream_t stream);
 
 hipError_t launch_pack_weight(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packed,
                               uint16_t* w_scales, hipStream_t stream);
+
+hipError_t launch_weight_group_sums(const uint8_t* w_packed, int64_t N, int64_t K,
+                                    int16_t* sums, hipStream_t stream);
 
 hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, int8_t* wq,
                                 hipStream_t stream);
@@ -83,6 +87,8 @@ struct GemmLaunch {
     float* slots;
     QuantOut qout;
     float act_scale;
+    const int8_t* zeros;      // asymmetric mode only
+    const int16_t* wsums;
 };
 
 // One output mode each (w4a4_gemm_<mode>.hip).
@@ -90,6 +96,16 @@ hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream);
+
+// The asymmetric mode: zeros [K/64][M] from quartz_quantize_act, wsums
+// [K/64][N] from launch_weight_group_sums.
+hipError_t launch_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
+                                   const uint16_t* scales, const int8_t* zeros,
+                                   const uint8_t* w_packed, const int16_t* wsums,
+                                   const uint16_t* bias, uint16_t* y, int64_t M, int64_t N,
+                                   int64_t K, int64_t ldy, int lzs_group, int epilogue,
+                                   const GemmSchedule& sch, void* workspace, hipStream_t stream);
 
 // `workspace`: gemm_workspace_bytes(sch) bytes whose counter part is zero
 // (left zero again by the launch); unused unless sch.sk_tiles > 0.  With

@@ -108,6 +108,21 @@ hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags,
     return launch_gemm_static(a, stream);
 }
 
+hipError_t launch_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
+                                   const uint16_t* scales, const int8_t* zeros,
+                                   const uint8_t* w_packed, const int16_t* wsums,
+                                   const uint16_t* bias, uint16_t* y, int64_t M, int64_t N,
+                                   int64_t K, int64_t ldy, int lzs_group, int epilogue,
+                                   const GemmSchedule& sch, void* workspace, hipStream_t stream)
+{
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    GemmLaunch a{codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
+                 epilogue, sch, nullptr, nullptr, QuantOut{}, 0.0f, zeros, wsums};
+    split_workspace(sch, workspace, a.counters, a.slots);
+    return launch_gemm_asym(a, stream);
+}
+
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream)

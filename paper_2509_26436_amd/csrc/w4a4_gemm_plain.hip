@@ -6,12 +6,12 @@ namespace quartz {
 
 hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, false, false>(a, stream);
+    return launch_mode<false, false, false, false>(a, stream);
 }
 
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<true, false, false>(a, stream);
+    return launch_mode<true, false, false, false>(a, stream);
 }
 
 int gemm_resident_blocks()
@@ -29,7 +29,7 @@ int gemm_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false, false>),
             kThreadsPerBlock, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);

@@ -5,7 +5,7 @@ namespace quartz {
 
 hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, true, false>(a, stream);
+    return launch_mode<false, true, false, false>(a, stream);
 }
 
 }  // namespace quartz

@@ -63,7 +63,7 @@ def test_quantize_validation(lib):
     f = q.quartz_quantize_act
     assert f(A, 4, 128, 128, 32, 16, 0, A, A, A, None, None) == EUNSUP
     assert f(A, 4, 128, 128, 64, 12, 0, A, A, A, None, None) == EUNSUP
-    assert f(A, 4, 128, 128, 64, 16, 1, A, A, A, None, None) == EUNSUP
+    assert f(A, 4, 128, 128, 64, 16, 5, A, A, A, None, None) == EUNSUP
     assert f(A, 4, 100, 100, 64, 16, 0, A, A, A, None, None) == ESHAPE
     assert f(A, -1, 128, 128, 64, 16, 0, A, A, A, None, None) == ESHAPE
     assert f(A, 4, 128, 64, 64, 16, 0, A, A, A, None, None) == ESHAPE
@@ -183,6 +183,35 @@ def test_ldm_entry_validation(lib):
     assert call(ws=A + 4, wsb=1 << 20) == EALIGN
     assert call(M=0) == OK
     assert call(N=0) == OK
+
+
+def test_asym_entry_validation(lib):
+    qa = q.quartz_quantize_act
+    assert qa(A, 8, 128, 128, 64, 16, 2, A, A, A, A, None) == EUNSUP      # unknown mode
+    assert qa(A, 8, 128, 128, 64, 16, 1, A, A, A, None, None) == ENULL    # asym needs zeros
+    assert qa(A, 8, 128, 128, 64, 16, 1, A, A, A, A + 2, None) == EALIGN
+    assert qa(A, 0, 128, 128, 64, 16, 1, A, A, A, None, None) == OK
+    ws = q.quartz_weight_group_sums
+    assert ws(A, 8, 128, 32, A, None) == EUNSUP
+    assert ws(A, 8, 100, 64, A, None) == ESHAPE
+    assert ws(None, 8, 128, 64, A, None) == ENULL
+    assert ws(A, 8, 128, 64, None, None) == ENULL
+    assert ws(A, 8, 128, 64, A + 2, None) == EALIGN
+    assert ws(A, 0, 128, 64, A, None) == OK
+    la = q.quartz_w4a4_linear_asym
+
+    def call(M=8, N=8, K=128, ldy=8, gs=64, lzs=16, epi=0, zeros=A, sums=A, y=A, wsp=None, wsb=0):
+        return la(A, A, A, zeros, A, sums, None, y, M, N, K, ldy, gs, lzs, epi, wsp, wsb, None)
+    assert call(epi=4) == EUNSUP
+    assert call(gs=16) == EUNSUP
+    assert call(K=96) == ESHAPE
+    assert call(ldy=4) == ESHAPE
+    assert call(zeros=None) == ENULL
+    assert call(sums=None) == ENULL
+    assert call(y=None) == ENULL
+    assert call(sums=A + 2) == EALIGN
+    assert call(wsp=A + 4, wsb=1 << 20) == EALIGN
+    assert call(M=0) == OK
 
 
 def test_debug_entry_validation(lib):
