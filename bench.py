@@ -62,7 +62,8 @@ def parse():
     ap.add_argument("--no-batched-mlp", action="store_true",
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--no-ldm", action="store_true",
-                    help="skip the LDM-setting (static activation scale) layer measurement")
+                    help="skip the LDM-setting (static activation scale) and asymmetric-mode "
+                         "layer measurements")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -238,6 +239,46 @@ def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
             "per_layer": out}
 
 
+def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
+    """The asymmetric mode (per-group zero points; one extra fp16 correction
+    MFMA per tile) on the same layers: per layer the quantizer and GEMM times
+    (HIP events on the launch stream, mean over `reps` passes after two
+    untimed ones).  The weight group sums are computed once, outside."""
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    out = []
+    for (x, w, b), L in zip(dev_in, cfg.layers):
+        qa = q.quantize_act(x, gs, mode=q.MODE_ASYMMETRIC)
+        pw = q.pack_weight(w)
+        sums = q.weight_group_sums(pw)
+        ws = q.gemm_workspace(L.M, L.N, L.K, dev)
+        y = q.w4a4_linear_asym(qa, pw, sums, b, L.epilogue, workspace=ws)
+        torch.cuda.synchronize()
+        t = np.zeros(2)
+        for it in range(reps + 2):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record(stream)
+            q.quantize_act(x, gs, out=qa, mode=q.MODE_ASYMMETRIC)
+            ev[1].record(stream)
+            q.w4a4_linear_asym(qa, pw, sums, b, L.epilogue, out=y, workspace=ws)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            if it >= 2:
+                t += np.array([ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])])
+        t = t / reps * 1e3     # us
+        ops = 2.0 * L.M * L.N * L.K
+        out.append({"layer": L.name, "quantize_us": round(t[0], 2), "gemm_us": round(t[1], 2),
+                    "gemm_tflops": round(ops / (t[1] * 1e6), 1),
+                    "gemm_frac": round(ops / (t[1] * 1e6) / PEAK_FP8_TFLOPS, 4)})
+        del qa, pw, sums, ws, y
+    tot_ops = sum(2.0 * L.M * L.N * L.K for L in cfg.layers)
+    tot_us = sum(r["gemm_us"] for r in out)
+    return {"step": "quantize_act (asymmetric) + w4a4_linear_asym (workspace) per layer",
+            "gemm_tflops": round(tot_ops / (tot_us * 1e6), 1),
+            "gemm_frac": round(tot_ops / (tot_us * 1e6) / PEAK_FP8_TFLOPS, 4),
+            "per_layer": out}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -386,6 +427,12 @@ def main():
         ldm = ldm_layers(q, W, torch, np, cfg, dev_in, gs)
         log(f"LDM-setting layers measured in {time.time() - t_l:.1f}s")
 
+    asym = None
+    if not args.no_ldm:
+        t_a = time.time()
+        asym = asym_layers(q, W, torch, np, cfg, dev_in, gs)
+        log(f"asymmetric-mode layers measured in {time.time() - t_a:.1f}s")
+
     mlp = None
     if not args.no_batched_mlp:
         del outs, dev_in, workspaces
@@ -455,6 +502,7 @@ def main():
         "per_layer": per_layer,
         "batched_mlp": mlp,
         "ldm_static": ldm,
+        "asymmetric": asym,
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
