@@ -82,6 +82,12 @@ constexpr int kMathWaves = 8;
 constexpr int kDecodeWaves = 4;
 constexpr int kThreadsPerBlock = 64 * (kMathWaves + kDecodeWaves);
 constexpr int kDecodeThreads = 64 * kDecodeWaves;
+// The static whole-tile kernel's math waves fit in 128 registers, which
+// leaves room for two decode waves per SIMD (16 waves): each decode thread
+// then takes half an activation row and a quarter weight column, and the
+// decode chain of a step is split over twice the waves.
+constexpr int kSplitDecodeWaves = 8;
+constexpr int kSplitThreadsPerBlock = 64 * (kMathWaves + kSplitDecodeWaves);
 constexpr int WAVES_N = 2;
 constexpr int WM = 64;
 constexpr int WN = 64;
@@ -186,7 +192,7 @@ typedef __attribute__((address_space(3))) v4u lds_v4u;
 // correction -z (x) W (one more fp16 outer-product MFMA, exact), so it yields
 // P_g - z W_g, the group product of the activations s (d - z).
 template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC, bool ASYM>
-__global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
+__global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
@@ -247,16 +253,25 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
     // ------------------------------------------------------ decode waves
     if (decoder) {
         static_assert(kDecodeThreads == BM && kDecodeThreads == 2 * BN, "decode roles");
+        static_assert(64 * kSplitDecodeWaves == 2 * BM && 64 * kSplitDecodeWaves == 4 * BN,
+                      "split decode roles");
+        // STATIC whole-tile kernels: thread d decodes half ah of A row d / 2
+        // and quarter bq of B column d / 4; otherwise all of A row d and half
+        // bh of column d / 2 (the split kernels' partial-sum code needs more
+        // than 128 registers)
+        constexpr bool kSplit = STATIC && !SPLIT;
         const int d = tid - kMathWaves * 64;      // decode thread index
-        const int dr = d & (BM - 1);              // A row
-        const int bc = (d >> 1) & (BN - 1);       // B column
-        const int bh = d & 1;                     // B half
+        const int dr = kSplit ? (d >> 1) & (BM - 1) : d & (BM - 1);   // A row
+        const int ah = kSplit ? d & 1 : 0;                             // A half
+        const int bc = kSplit ? (d >> 2) & (BN - 1) : (d >> 1) & (BN - 1);   // B column
+        const int bh = kSplit ? d & 3 : d & 1;                         // B half / quarter
         const int swc = d & (BN - 1);             // column whose s_w this thread loads
         const int G = (int)(K / 64);
         const int64_t panels = (N + kPanel - 1) / kPanel;
-        const uint32_t a_off = (uint32_t)(dr * 32);
+        const uint32_t a_off = (uint32_t)(dr * 32 + ah * 16);
         const uint32_t f_off = (uint32_t)(dr * FB);
-        const uint32_t b_off = (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * 16);
+        const uint32_t b_off =
+            (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * (kSplit ? 8 : 16));
         const uint32_t sw_off =
             (uint32_t)((swc / kPanel) * G * kChunkBytes + kChunkCodeBytes + (swc % kPanel) * 2);
 
@@ -303,10 +318,18 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
             const Rsrc rf = make_rsrc(flags + ((int64_t)g * M + m0) * FB, f_bytes);
             const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
             r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off, 0, 0));
-            r.a1 = __builtin_bit_cast(uint4,
+            if constexpr (kSplit)
+                r.a1 = make_uint4(0, 0, 0, 0);
+            else
+                r.a1 = __builtin_bit_cast(uint4,
                                       __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
             r.f = load_flags_raw<GS>(rf, f_off);
-            r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+            if constexpr (kSplit) {
+                const uint2 b2 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rb, (int)b_off, 0, 0));
+                r.b = make_uint4(b2.x, b2.y, 0, 0);
+            } else {
+                r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+            }
             if constexpr (kGroupScales) {   // the integer and static paths have none
                 const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
                 r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
@@ -340,16 +363,28 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
         };
         // decode one group into LDS buffer `buf`
         auto stage = [&](const Raw& r, int buf) {
-            const uint2 fr = flags_dwords<GS>(r.f);
+            uint2 fr = flags_dwords<GS>(r.f);
+            if constexpr (kSplit) {
+                // the half row's flags first: half ah starts at word 4 ah,
+                // flag 4 ah / (G_s / 8)
+                if constexpr (GS == 8) {
+                    fr = ah ? uint2{fr.y, 0u} : fr;
+                } else if constexpr (GS == 16) {
+                    fr.x >>= 16 * ah;
+                } else if constexpr (GS == 32) {
+                    fr.x >>= 8 * ah;
+                }
+            }
             const uint32_t a[8] = {r.a0.x, r.a0.y, r.a0.z, r.a0.w, r.a1.x, r.a1.y, r.a1.z, r.a1.w};
             constexpr int kWordsPerFlag = GS / 8;
+            constexpr int kChunks = kSplit ? 2 : 4;   // 16-byte fp8 chunks of the row this thread writes
             Fp8Table t = fp8_table_raw<0>(fr.x, fr.y);
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
+            for (int c = 0; c < kChunks; ++c) {
                 uint2 w[2];
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    const int wi = 2 * c + h;           // word index 0..7
+                    const int wi = 2 * c + h;           // word index within the thread's words
                     if (wi % kWordsPerFlag == 0 && wi > 0) {
                         switch (wi / kWordsPerFlag) {      // flag index, 1..7
                         case 1: t = fp8_table_raw<1>(fr.x, fr.y); break;
@@ -363,15 +398,20 @@ __global__ __launch_bounds__(kThreadsPerBlock) void w4a4_gemm_kernel(
                     }
                     w[h] = decode_nibbles_fp8(a[wi], t);
                 }
-                *reinterpret_cast<uint4*>(As[buf] + swz(dr, c)) = make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
+                *reinterpret_cast<uint4*>(As[buf] + swz(dr, kSplit ? 2 * ah + c : c)) =
+                    make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
             }
             const Fp8Table tw{kTabLo, kTabHi};
             const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
             const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
-            const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
-            const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
-            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
-            *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
+            if constexpr (kSplit) {
+                *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
+            } else {
+                const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
+                const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
+                *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
+                *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
+            }
             if constexpr (kGroupScales) {
                 sas[buf][dr] = r.sa;
                 if (d < BN)
@@ -1130,7 +1170,8 @@ using bool_c = std::integral_constant<bool, B>;
 template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM>
 hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
 {
-    const dim3 grid((unsigned)a.sch.blocks), block(kThreadsPerBlock);
+    const dim3 grid((unsigned)a.sch.blocks);
+    const dim3 block(STATIC && a.sch.sk_tiles == 0 ? kSplitThreadsPerBlock : kThreadsPerBlock);
     auto go = [&](auto gs, auto gelu, auto split) {
         w4a4_gemm_kernel<decltype(gs)::value, I32OUT, decltype(gelu)::value, decltype(split)::value,
                          QOUT, STATIC, ASYM><<<grid, block, 0, stream>>>(
