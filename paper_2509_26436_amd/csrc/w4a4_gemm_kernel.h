@@ -950,9 +950,12 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
             // khalf = 1 rows in the second), so every store covers a full 128-byte
             // row segment; the pair is rounded to bf16 (RNE) by one conversion.
             // Stores go through one buffer range per wave (its 64 rows from its
-            // first column): the row offset is wave-uniform (a scalar operand),
-            // rows past M fall outside the range and are dropped, and lanes
-            // whose column is past N get an offset outside it.
+            // first column), with the whole offset, row included, in the lane
+            // operand: the bounds check covers that operand and the immediate
+            // only, never the scalar one.  Rows past M then fall outside the
+            // range and are dropped, and lanes whose column is past N start
+            // at 2^31, outside it for every row (the range is at most 2^31
+            // bytes: 64 rows of at most 2^25).
             static_assert(TN == 2, "the swap pairs the two column tiles");
             set_out_scale();
             const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
@@ -982,10 +985,10 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                     const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
                     const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
                     const uint32_t row0 = (uint32_t)(i * 32 + 8 * (r >> 2) + (r & 3));
-                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)pk, out_r, (int)voff,
-                                                          (int)(row0 * row_bytes), 0);
-                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(pk >> 16), out_r, (int)voff,
-                                                          (int)((row0 + 4) * row_bytes), 0);
+                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)pk, out_r,
+                                                          (int)(voff + row0 * row_bytes), 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(pk >> 16), out_r,
+                                                          (int)(voff + (row0 + 4) * row_bytes), 0, 0);
                 }
             }
         }
