@@ -120,7 +120,7 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
     """The batched FLUX MLP at M = 18432 (4 images x 4608 tokens) as one pipeline:
     quantize x -> fc1 3072->12288 with the GELU epilogue -> quantize -> fc2
     12288->3072.  Per layer: mean quantize and GEMM time over `reps` passes
-    (HIP events on the launch stream), and the end-to-end time against the
+    (timed_chain), and the end-to-end time against the
     sum of the two roofline times (quantize bytes at 8 TB/s + GEMM ops at the
     fp8 dense peak).  Then the same pipeline with fc2's input quantized in
     fc1's epilogue, its time, and whether fc2's output is bit-identical."""
@@ -140,42 +140,21 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
     y2 = q.w4a4_linear(qa2, pw2, b2, 0, workspace=ws2)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    t = np.zeros(4)
-    for it in range(reps + 2):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-        ev[0].record(stream)
-        q.quantize_act(x1, lzs_group=gs, out=qa1)
-        ev[1].record(stream)
-        q.w4a4_linear(qa1, pw1, b1, 1, out=y1, workspace=ws1)
-        ev[2].record(stream)
-        q.quantize_act(y1, lzs_group=gs, out=qa2)
-        ev[3].record(stream)
-        q.w4a4_linear(qa2, pw2, b2, 0, out=y2, workspace=ws2)
-        ev[4].record(stream)
-        torch.cuda.synchronize()
-        if it >= 2:
-            t += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(4)])
-    t = t / reps * 1e3        # us
+    t = timed_chain(torch, np, stream,
+                    [lambda: q.quantize_act(x1, lzs_group=gs, out=qa1),
+                     lambda: q.w4a4_linear(qa1, pw1, b1, 1, out=y1, workspace=ws1),
+                     lambda: q.quantize_act(y1, lzs_group=gs, out=qa2),
+                     lambda: q.w4a4_linear(qa2, pw2, b2, 0, out=y2, workspace=ws2)], reps)
     # the same pipeline with fc2's input quantized in fc1's epilogue
     # (quartz_w4a4_linear_quantize): no bf16 fc1 output, no separate quantize
     qa2f = q.w4a4_linear_quantize(qa1, pw1, b1, 1, gs, workspace=ws1)
     y2f = q.w4a4_linear(qa2f, pw2, b2, 0, workspace=ws2)
     torch.cuda.synchronize()
     same = bool(torch.equal(y2f.view(torch.int16), y2.view(torch.int16)))
-    tf = np.zeros(3)
-    for it in range(reps + 2):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        ev[0].record(stream)
-        q.quantize_act(x1, lzs_group=gs, out=qa1)
-        ev[1].record(stream)
-        q.w4a4_linear_quantize(qa1, pw1, b1, 1, gs, out=qa2f, workspace=ws1)
-        ev[2].record(stream)
-        q.w4a4_linear(qa2f, pw2, b2, 0, out=y2f, workspace=ws2)
-        ev[3].record(stream)
-        torch.cuda.synchronize()
-        if it >= 2:
-            tf += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(3)])
-    tf = tf / reps * 1e3      # us
+    tf = timed_chain(torch, np, stream,
+                     [lambda: q.quantize_act(x1, lzs_group=gs, out=qa1),
+                      lambda: q.w4a4_linear_quantize(qa1, pw1, b1, 1, gs, out=qa2f, workspace=ws1),
+                      lambda: q.w4a4_linear(qa2f, pw2, b2, 0, out=y2f, workspace=ws2)], reps)
     fused = {"step": "quantize + fc1 (GELU; its epilogue quantizes the output for fc2) + fc2",
              "quantize_us": round(tf[0], 2), "fc1_quantize_us": round(tf[1], 2),
              "fc2_gemm_us": round(tf[2], 2), "end_to_end_us": round(tf.sum(), 2),
@@ -198,11 +177,31 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
             "fused_quantize": fused}
 
 
+def timed_chain(torch, np, stream, calls, reps):
+    """Mean HIP-event time (us) of each launch in `calls` over `reps` passes of
+    the whole chain, queued back to back after two untimed passes with one
+    synchronization at the end: every launch but the very first follows
+    another kernel, as inside a step, so no timed launch starts from an idle
+    queue."""
+    evs = []
+    for _ in range(reps + 2):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+        ev[0].record(stream)
+        for k, call in enumerate(calls):
+            call()
+            ev[k + 1].record(stream)
+        evs.append(ev)
+    torch.cuda.synchronize()
+    t = np.zeros(len(calls))
+    for ev in evs[2:]:
+        t += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(len(calls))])
+    return t / reps * 1e3
+
+
 def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
     """The LDM setting (static per-tensor activation scale, per-channel weight
     scales; the K loop is pure integer MFMA) on the same layers: per layer the
-    static quantizer and GEMM times (HIP events on the launch stream, mean over
-    `reps` passes after two untimed ones).  The static scale is fixed once from
+    static quantizer and GEMM times (timed_chain).  The static scale is fixed once from
     the synthetic tensor (max |x| / 127, outside the timed region)."""
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream()
@@ -214,18 +213,10 @@ def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
         ws = q.gemm_workspace(L.M, L.N, L.K, dev)
         y = q.w4a4_linear_static(qa, pw, s, b, L.epilogue, workspace=ws)
         torch.cuda.synchronize()
-        t = np.zeros(2)
-        for it in range(reps + 2):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            ev[0].record(stream)
-            q.quantize_act_static(x, s, gs, out=qa)
-            ev[1].record(stream)
-            q.w4a4_linear_static(qa, pw, s, b, L.epilogue, out=y, workspace=ws)
-            ev[2].record(stream)
-            torch.cuda.synchronize()
-            if it >= 2:
-                t += np.array([ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])])
-        t = t / reps * 1e3     # us
+        t = timed_chain(torch, np, stream,
+                        [lambda: q.quantize_act_static(x, s, gs, out=qa),
+                         lambda: q.w4a4_linear_static(qa, pw, s, b, L.epilogue, out=y, workspace=ws)],
+                        reps)
         ops = 2.0 * L.M * L.N * L.K
         out.append({"layer": L.name, "quantize_us": round(t[0], 2), "gemm_us": round(t[1], 2),
                     "gemm_tflops": round(ops / (t[1] * 1e6), 1),
@@ -242,8 +233,7 @@ def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
 def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
     """The asymmetric mode (per-group zero points; one extra fp16 correction
     MFMA per tile) on the same layers: per layer the quantizer and GEMM times
-    (HIP events on the launch stream, mean over `reps` passes after two
-    untimed ones).  The weight group sums are computed once, outside."""
+    (timed_chain).  The weight group sums are computed once, outside."""
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream()
     out = []
@@ -254,18 +244,10 @@ def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
         ws = q.gemm_workspace(L.M, L.N, L.K, dev)
         y = q.w4a4_linear_asym(qa, pw, sums, b, L.epilogue, workspace=ws)
         torch.cuda.synchronize()
-        t = np.zeros(2)
-        for it in range(reps + 2):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            ev[0].record(stream)
-            q.quantize_act(x, gs, out=qa, mode=q.MODE_ASYMMETRIC)
-            ev[1].record(stream)
-            q.w4a4_linear_asym(qa, pw, sums, b, L.epilogue, out=y, workspace=ws)
-            ev[2].record(stream)
-            torch.cuda.synchronize()
-            if it >= 2:
-                t += np.array([ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])])
-        t = t / reps * 1e3     # us
+        t = timed_chain(torch, np, stream,
+                        [lambda: q.quantize_act(x, gs, out=qa, mode=q.MODE_ASYMMETRIC),
+                         lambda: q.w4a4_linear_asym(qa, pw, sums, b, L.epilogue, out=y, workspace=ws)],
+                        reps)
         ops = 2.0 * L.M * L.N * L.K
         out.append({"layer": L.name, "quantize_us": round(t[0], 2), "gemm_us": round(t[1], 2),
                     "gemm_tflops": round(ops / (t[1] * 1e6), 1),
