@@ -62,8 +62,8 @@ def parse():
     ap.add_argument("--no-batched-mlp", action="store_true",
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--no-ldm", action="store_true",
-                    help="skip the LDM-setting (static activation scale) and asymmetric-mode "
-                         "layer measurements")
+                    help="skip the LDM-setting (static activation scale), asymmetric-mode "
+                         "and implicit-GEMM convolution measurements")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -261,6 +261,52 @@ def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
             "per_layer": out}
 
 
+def conv_layers(q, W, torch, np, gs, reps=10):
+    """The SDXL UNet 3 x 3 convolutions (config 5) as implicit GEMMs: per layer
+    the feature map's quantizer and the convolution (quartz_w4a4_conv3x3,
+    workspace entry point), then the same in the LDM setting (static
+    quantizer, quartz_w4a4_conv3x3_static); times by timed_chain.  The
+    quantizer reads the H x W x C map once (the im2col matrix would be 9x
+    larger and is never formed)."""
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    cfg = W.CONFIGS[5]
+    to = lambda a: torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+    out = []
+    for li, L in enumerate(cfg.layers):
+        C, H = L.K // 9, int(round(L.M ** 0.5))
+        fm = to(W.make_feature_map(5, li)).reshape(L.M, C)
+        w, b = to(W.make_w(5, li)), to(W.make_bias(5, li))
+        ws = q.gemm_workspace(L.M, L.N, L.K, dev)
+        pw = q.pack_weight(w)
+        qa = q.quantize_act(fm, gs)
+        y = q.w4a4_conv3x3(qa, pw, 1, H, H, b, 0, workspace=ws)
+        t = timed_chain(torch, np, stream,
+                        [lambda: q.quantize_act(fm, gs, out=qa),
+                         lambda: q.w4a4_conv3x3(qa, pw, 1, H, H, b, 0, out=y, workspace=ws)], reps)
+        s = float(fm.abs().max().float().item()) / 127.0
+        pwc = q.pack_weight_per_channel(w)
+        qs = q.quantize_act_static(fm, s, gs)
+        ts = timed_chain(torch, np, stream,
+                         [lambda: q.quantize_act_static(fm, s, gs, out=qs),
+                          lambda: q.w4a4_conv3x3_static(qs, pwc, s, 1, H, H, b, 0, out=y, workspace=ws)],
+                         reps)
+        ops = 2.0 * L.M * L.N * L.K
+        qbytes = L.M * C * (2 + 0.5 + 1.0 / gs + 2.0 / 64)
+        out.append({"layer": L.name, "M": L.M, "C": C, "N": L.N,
+                    "quantize_us": round(t[0], 2), "quantize_gbps": round(qbytes / (t[0] * 1e3), 1),
+                    "conv_us": round(t[1], 2), "conv_tflops": round(ops / (t[1] * 1e6), 1),
+                    "static_quantize_us": round(ts[0], 2), "static_conv_us": round(ts[1], 2),
+                    "static_conv_tflops": round(ops / (ts[1] * 1e6), 1)})
+        del fm, w, b, ws, pw, qa, y, pwc, qs
+    tot_ops = sum(2.0 * L.M * L.N * L.K for L in cfg.layers)
+    return {"workload": cfg.name + " (implicit GEMM)", "lzs_group": gs,
+            "step": "quantize_act of the feature map + w4a4_conv3x3 per layer, then the static pair",
+            "conv_tflops": round(tot_ops / (sum(r["conv_us"] for r in out) * 1e6), 1),
+            "static_conv_tflops": round(tot_ops / (sum(r["static_conv_us"] for r in out) * 1e6), 1),
+            "per_layer": out}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -415,6 +461,12 @@ def main():
         asym = asym_layers(q, W, torch, np, cfg, dev_in, gs)
         log(f"asymmetric-mode layers measured in {time.time() - t_a:.1f}s")
 
+    conv = None
+    if not args.no_ldm:
+        t_c = time.time()
+        conv = conv_layers(q, W, torch, np, gs)
+        log(f"implicit-GEMM convolutions measured in {time.time() - t_c:.1f}s")
+
     mlp = None
     if not args.no_batched_mlp:
         del outs, dev_in, workspaces
@@ -485,6 +537,7 @@ def main():
         "batched_mlp": mlp,
         "ldm_static": ldm,
         "asymmetric": asym,
+        "conv3x3": conv,
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }

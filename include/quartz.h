@@ -304,6 +304,51 @@ quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                    hipStream_t stream);
 
 /*
+ * 3 x 3 convolution (stride 1, padding 1) of the UNet backbones evaluated in
+ * Section 5 (LDM, SD v1.4, SDXL-Turbo), as the W4A4 layer on its im2col
+ * matrix: row m = (image * H + h) * W + w is output pixel (h, w) of an image,
+ * and K = 9 C runs over the taps (kh, kw) and the C input channels, c
+ * fastest, with zero padding outside the image.  The im2col matrix is never
+ * formed: with C % 64 == 0 every 64-group of an im2col row is the 64
+ * channels of one input pixel (or zero padding), and a group's scale, FLAGs
+ * and codes depend on its 64 values only, so quantizing the feature map
+ * once gives the codes of every im2col row; the GEMM reads them at the
+ * pixel each tap points to.  The result equals quartz_w4a4_linear_ws (or
+ * quartz_w4a4_linear_static) on the quantized im2col matrix, bit for bit.
+ *
+ * quartz_w4a4_conv3x3: the per-group setting.
+ *   codes, flags, scales  outputs of quartz_quantize_act for the feature map
+ *                         x [images * H * W][C] (NHWC, K = C), symmetric mode.
+ *   w_packed   quartz_pack_weight of the weight [N][9 C], K ordered
+ *              (kh, kw, c) with c fastest.
+ *   bias_bf16, y_bf16 [images * H * W][ldy], epilogue, workspace,
+ *   workspace_bytes   as for quartz_w4a4_linear_ws, with M = images * H * W
+ *              and K = 9 C (the same workspace size query applies).
+ *   images >= 0, H, W >= 1, C > 0 with C % 64 == 0, images * H * W < 2^26,
+ *   9 C <= 2^20: QUARTZ_ERR_SHAPE otherwise; other errors as for
+ *   quartz_w4a4_linear_ws.
+ *
+ * quartz_w4a4_conv3x3_static: the LDM setting: codes and flags of
+ *   quartz_quantize_act_static for the feature map with act_scale, w_packed
+ *   of quartz_pack_weight_per_channel for the weight [N][9 C]; otherwise as
+ *   quartz_w4a4_conv3x3 (equal to quartz_w4a4_linear_static on the im2col
+ *   matrix).
+ */
+quartz_status quartz_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,
+                                  const uint16_t* scales, const void* w_packed,
+                                  const void* bias_bf16, void* y_bf16, int64_t images, int64_t H,
+                                  int64_t W, int64_t C, int64_t N, int64_t ldy,
+                                  int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+quartz_status quartz_w4a4_conv3x3_static(const uint8_t* codes, const uint8_t* flags,
+                                         float act_scale, const void* w_packed,
+                                         const void* bias_bf16, void* y_bf16, int64_t images,
+                                         int64_t H, int64_t W, int64_t C, int64_t N, int64_t ldy,
+                                         int32_t lzs_group, int32_t epilogue, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream);
+
+/*
  * quartz_w4a4_linear_schedule (host only, needs no GPU): the GEMM work
  * schedule for a persistent grid of at most `blocks` workgroups (the entry
  * points use the device's compute-unit count), with (split = 1, as

@@ -22,10 +22,11 @@ __all__ = [
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
     "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
+    "quartz_w4a4_conv3x3", "quartz_w4a4_conv3x3_static",
     "quartz_status_string", "QuantizedAct", "PackedWeight",
     "quantize_act", "pack_weight", "w4a4_linear", "w4a4_linear_quantize", "gemm_workspace",
     "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "weight_group_sums",
-    "w4a4_linear_asym", "linear_schedule",
+    "w4a4_linear_asym", "linear_schedule", "w4a4_conv3x3", "w4a4_conv3x3_static",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
 ]
 
@@ -45,7 +46,7 @@ EXPORTED_SYMBOLS = (
     "quartz_w4a4_linear_schedule", "quartz_unpack_weight", "quartz_w4a4_gemm_i32",
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
     "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
-    "quartz_status_string",
+    "quartz_w4a4_conv3x3", "quartz_w4a4_conv3x3_static", "quartz_status_string",
 )
 
 
@@ -102,6 +103,12 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_linear_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32,
                                                 I32, I32, P, P, P, P, P, ctypes.c_size_t, P]
     lib.quartz_w4a4_linear_quantize.restype = I32
+    lib.quartz_w4a4_conv3x3.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I32, I32,
+                                        I32, P, SZ, P]
+    lib.quartz_w4a4_conv3x3.restype = I32
+    lib.quartz_w4a4_conv3x3_static.argtypes = [P, P, F32, P, P, P, I64, I64, I64, I64, I64, I64,
+                                               I32, I32, P, SZ, P]
+    lib.quartz_w4a4_conv3x3_static.restype = I32
     lib.quartz_w4a4_linear_schedule.argtypes = [I64, I64, I64, I32, I32, P, P, I64]
     lib.quartz_w4a4_linear_schedule.restype = I64
     lib.quartz_unpack_weight.argtypes = [P, I64, I64, I32, P, P]
@@ -187,6 +194,21 @@ def quartz_w4a4_linear_asym(codes, flags, scales, zeros, w_packed, w_sums, bias,
     return load().quartz_w4a4_linear_asym(codes, flags, scales, zeros, w_packed, w_sums, bias, y,
                                           M, N, K, ldy, group_size, lzs_group, epilogue,
                                           workspace, workspace_bytes, stream)
+
+
+def quartz_w4a4_conv3x3(codes, flags, scales, w_packed, bias, y, images, H, W, C, N, ldy,
+                        group_size, lzs_group, epilogue, workspace, workspace_bytes, stream) -> int:
+    return load().quartz_w4a4_conv3x3(codes, flags, scales, w_packed, bias, y, images, H, W, C, N,
+                                      ldy, group_size, lzs_group, epilogue, workspace,
+                                      workspace_bytes, stream)
+
+
+def quartz_w4a4_conv3x3_static(codes, flags, act_scale, w_packed, bias, y, images, H, W, C, N,
+                               ldy, lzs_group, epilogue, workspace, workspace_bytes,
+                               stream) -> int:
+    return load().quartz_w4a4_conv3x3_static(codes, flags, act_scale, w_packed, bias, y, images,
+                                             H, W, C, N, ldy, lzs_group, epilogue, workspace,
+                                             workspace_bytes, stream)
 
 
 def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
@@ -437,6 +459,53 @@ def w4a4_linear_asym(a: QuantizedAct, w: PackedWeight, w_sums, bias=None,
                                  out.stride(0), GROUP, a.lzs_group, epilogue, _ptr(workspace),
                                  nbytes, _stream_handle(stream))
     _check(st, "quartz_w4a4_linear_asym")
+    return out
+
+
+def _conv_args(a: QuantizedAct, w: PackedWeight, images: int, H: int, W: int, bias, out):
+    torch = _torch()
+    C = a.K
+    if a.M != images * H * W:
+        raise ValueError("the quantized feature map must have images * H * W rows")
+    if w.K != 9 * C:
+        raise ValueError("the weight must have K = 9 C (taps (kh, kw), channels fastest)")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out is None:
+        out = torch.empty((a.M, w.N), dtype=torch.bfloat16, device=a.codes.device)
+    return C, out
+
+
+def w4a4_conv3x3(a: QuantizedAct, w: PackedWeight, images: int, H: int, W: int, bias=None,
+                 epilogue: int = EPI_NONE, out=None, stream=None, workspace=None):
+    """3 x 3 convolution, stride 1, padding 1, as an implicit GEMM
+    (quartz_w4a4_conv3x3): ``a`` = quantize_act of the NHWC feature map viewed as
+    [images * H * W, C], ``w`` = pack_weight of the weight [N, 9 C] ordered
+    (kh, kw, c); returns y bf16 [images * H * W, N] (the workspace from
+    ``gemm_workspace(images * H * W, N, 9 C)``)."""
+    C, out = _conv_args(a, w, images, H, W, bias, out)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_w4a4_conv3x3(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(w.data),
+                             _ptr(bias), _ptr(out), images, H, W, C, w.N, out.stride(0), GROUP,
+                             a.lzs_group, epilogue, _ptr(workspace), nbytes,
+                             _stream_handle(stream))
+    _check(st, "quartz_w4a4_conv3x3")
+    return out
+
+
+def w4a4_conv3x3_static(a: QuantizedAct, w: PackedWeight, act_scale: float, images: int, H: int,
+                        W: int, bias=None, epilogue: int = EPI_NONE, out=None, stream=None,
+                        workspace=None):
+    """The LDM-setting convolution (quartz_w4a4_conv3x3_static): ``a`` =
+    quantize_act_static of the feature map with ``act_scale``, ``w`` =
+    pack_weight_per_channel of the weight [N, 9 C]."""
+    C, out = _conv_args(a, w, images, H, W, bias, out)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_w4a4_conv3x3_static(_ptr(a.codes), _ptr(a.flags), float(act_scale), _ptr(w.data),
+                                    _ptr(bias), _ptr(out), images, H, W, C, w.N, out.stride(0),
+                                    a.lzs_group, epilogue, _ptr(workspace), nbytes,
+                                    _stream_handle(stream))
+    _check(st, "quartz_w4a4_conv3x3_static")
     return out
 
 

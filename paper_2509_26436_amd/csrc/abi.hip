@@ -15,6 +15,9 @@ constexpr int64_t kMaxRowGroups = int64_t(1) << 28;
 // leading dimension of the activations and of the output (elements): 64 bf16
 // rows of it stay below 2^31 bytes (one buffer range per wave of output rows)
 constexpr int64_t kMaxLd = int64_t(1) << 24;
+// pixels of one implicit convolution (images * H * W): the GEMM addresses a
+// channel block's codes by pixel with 32-bit offsets (32 bytes per pixel)
+constexpr int64_t kMaxConvPixels = int64_t(1) << 26;
 
 // sizes that every entry point accepts: rows >= 0, 0 <= K <= kMaxK, K % 64 == 0
 // and rows * K / 64 <= kMaxRowGroups
@@ -436,6 +439,72 @@ quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
     return from_hip(quartz::launch_w4a4_gemm_i32(codes, flags,
                                                  static_cast<const uint8_t*>(w_packed), acc_out, M,
                                                  N, K, lzs_group, stream));
+}
+
+static quartz_status conv_impl(const uint8_t* codes, const uint8_t* flags,
+                               const uint16_t* scales, float act_scale, bool is_static,
+                               const void* w_packed, const void* bias_bf16, void* y_bf16,
+                               int64_t images, int64_t H, int64_t W, int64_t C, int64_t N,
+                               int64_t ldy, int32_t group_size, int32_t lzs_group,
+                               int32_t epilogue, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream)
+{
+    if ((epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH) ||
+        (is_static && !std::isfinite(act_scale)))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (images < 0 || H <= 0 || W <= 0 || C <= 0 || C % 64 != 0 || N < 0 ||
+        H >= kMaxConvPixels || W >= kMaxConvPixels || H > kMaxConvPixels / W ||
+        (images > 0 && images > (kMaxConvPixels - 1) / (H * W)) || C > kMaxK / 9)
+        return QUARTZ_ERR_SHAPE;
+    const int64_t M = images * H * W;
+    const int64_t K = 9 * C;
+    quartz_status st = check_gemm(codes, flags, w_packed, M, N, K, group_size, lzs_group);
+    if (st != QUARTZ_OK)
+        return st;
+    if (ldy < N || ldy > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (M == 0 || N == 0)
+        return QUARTZ_OK;
+    if ((!is_static && !scales) || !y_bf16)
+        return QUARTZ_ERR_NULL;
+    if ((!is_static && !aligned16(scales)) || !aligned16(y_bf16) ||
+        (bias_bf16 && !aligned16(bias_bf16)) || (workspace && !aligned16(workspace)))
+        return QUARTZ_ERR_ALIGN;
+    const quartz::GemmSchedule sch =
+        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+    if (sch.blocks <= 0)
+        return QUARTZ_ERR_HIP;
+    if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    return from_hip(quartz::launch_w4a4_conv3x3(
+        codes, flags, is_static ? nullptr : scales, act_scale,
+        static_cast<const uint8_t*>(w_packed), static_cast<const uint16_t*>(bias_bf16),
+        static_cast<uint16_t*>(y_bf16), images, H, W, C, N, ldy, lzs_group, epilogue, sch,
+        workspace, stream));
+}
+
+quartz_status quartz_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,
+                                  const uint16_t* scales, const void* w_packed,
+                                  const void* bias_bf16, void* y_bf16, int64_t images, int64_t H,
+                                  int64_t W, int64_t C, int64_t N, int64_t ldy,
+                                  int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    return conv_impl(codes, flags, scales, 0.0f, false, w_packed, bias_bf16, y_bf16, images, H,
+                     W, C, N, ldy, group_size, lzs_group, epilogue, workspace, workspace_bytes,
+                     stream);
+}
+
+quartz_status quartz_w4a4_conv3x3_static(const uint8_t* codes, const uint8_t* flags,
+                                         float act_scale, const void* w_packed,
+                                         const void* bias_bf16, void* y_bf16, int64_t images,
+                                         int64_t H, int64_t W, int64_t C, int64_t N, int64_t ldy,
+                                         int32_t lzs_group, int32_t epilogue, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream)
+{
+    return conv_impl(codes, flags, nullptr, act_scale, true, w_packed, bias_bf16, y_bf16, images,
+                     H, W, C, N, ldy, 64, lzs_group, epilogue, workspace, workspace_bytes,
+                     stream);
 }
 
 }  // extern "C"

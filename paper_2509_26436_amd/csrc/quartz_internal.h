@@ -70,6 +70,18 @@ struct QuantOut {
     int32_t lzs;         // LZS subgroup size of the output: 8, 16, 32 or 64
 };
 
+// Geometry of a 3 x 3 convolution (stride 1, padding 1) run as an implicit
+// GEMM: rows are output pixels m = (image * H + h) * W + w, the K-group g is
+// tap t = g / cg (kh = t / 3, kw = t % 3) and channel block g % cg of the
+// pixel (h + kh - 1, w + kw - 1), zero outside the image.  div_magic =
+// floor(2^32 / cg) + 1 gives g / cg = mulhi(g, div_magic) for every g < 2^14
+// (unused when cg == 1).  cg == 0: a plain GEMM.
+struct ConvGeom {
+    int32_t H, W;
+    int32_t cg;            // C / 64
+    uint32_t div_magic;
+};
+
 // Arguments of one GEMM launch (see the kernel template in w4a4_gemm_kernel.h).
 struct GemmLaunch {
     const uint8_t* codes;
@@ -89,6 +101,7 @@ struct GemmLaunch {
     float act_scale;
     const int8_t* zeros;      // asymmetric mode only
     const int16_t* wsums;
+    ConvGeom conv;            // implicit 3 x 3 convolution only
 };
 
 // One output mode each (w4a4_gemm_<mode>.hip).
@@ -97,6 +110,20 @@ hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_conv(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_conv_static(const GemmLaunch& a, hipStream_t stream);
+
+// 3 x 3 convolution (stride 1, padding 1) as an implicit GEMM: codes, flags
+// and scales of quartz_quantize_act for the feature map [images * H * W][C]
+// (scales == nullptr: the static setting with act_scale and a per-channel
+// packed weight), w_packed of the weight [N][9 C] with K ordered (kh, kw, c),
+// y [images * H * W][ldy].
+hipError_t launch_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,
+                               const uint16_t* scales, float act_scale, const uint8_t* w_packed,
+                               const uint16_t* bias, uint16_t* y, int64_t images, int64_t H,
+                               int64_t W, int64_t C, int64_t N, int64_t ldy, int lzs_group,
+                               int epilogue, const GemmSchedule& sch, void* workspace,
+                               hipStream_t stream);
 
 // The asymmetric mode: zeros [K/64][M] from quartz_quantize_act, wsums
 // [K/64][N] from launch_weight_group_sums.

@@ -123,6 +123,25 @@ hipError_t launch_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
     return launch_gemm_asym(a, stream);
 }
 
+hipError_t launch_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,
+                               const uint16_t* scales, float act_scale, const uint8_t* w_packed,
+                               const uint16_t* bias, uint16_t* y, int64_t images, int64_t H,
+                               int64_t W, int64_t C, int64_t N, int64_t ldy, int lzs_group,
+                               int epilogue, const GemmSchedule& sch, void* workspace,
+                               hipStream_t stream)
+{
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    const int64_t M = images * H * W;
+    const int32_t cg = (int32_t)(C / kGroup);
+    const ConvGeom conv{(int32_t)H, (int32_t)W, cg,
+                        cg > 1 ? (uint32_t)((uint64_t(1) << 32) / (uint64_t)cg + 1) : 0u};
+    GemmLaunch a{codes, flags, scales, w_packed, bias, y, nullptr, M, N, 9 * C, ldy, lzs_group,
+                 epilogue, sch, nullptr, nullptr, QuantOut{}, act_scale, nullptr, nullptr, conv};
+    split_workspace(sch, workspace, a.counters, a.slots);
+    return scales ? launch_gemm_conv(a, stream) : launch_gemm_conv_static(a, stream);
+}
+
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream)

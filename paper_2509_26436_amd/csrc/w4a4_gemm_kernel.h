@@ -191,14 +191,22 @@ typedef __attribute__((address_space(3))) v4u lds_v4u;
 // weight group sums W[g][n]: the fp8 MFMA of each tile starts from the
 // correction -z (x) W (one more fp16 outer-product MFMA, exact), so it yields
 // P_g - z W_g, the group product of the activations s (d - z).
-template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC, bool ASYM>
+// CONV instantiations are a 3 x 3 convolution (stride 1, padding 1) as an
+// implicit GEMM (ConvGeom): codes, flags and scales are those of the feature
+// map [M][C], and the A row of output pixel m for K-group g is the row of the
+// pixel shifted by g's tap, read from channel block g % cg, or zero where the
+// tap falls outside the image.  Every 64-group of an im2col row lies within
+// one tap (C % 64 == 0), and a group's codes, FLAGs and scale depend on its
+// 64 values only, so these are exactly the codes of the im2col matrix.
+template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC, bool ASYM,
+          bool CONV = false>
 __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
     uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout, float act_scale,
-    const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums)
+    const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums, ConvGeom conv)
 {
     // per-group scales are staged and applied only by the per-group kernels
     constexpr bool kGroupScales = !I32OUT && !STATIC;
@@ -268,8 +276,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
         const int swc = d & (BN - 1);             // column whose s_w this thread loads
         const int G = (int)(K / 64);
         const int64_t panels = (N + kPanel - 1) / kPanel;
-        const uint32_t a_off = (uint32_t)(dr * 32 + ah * 16);
-        const uint32_t f_off = (uint32_t)(dr * FB);
         const uint32_t b_off =
             (uint32_t)((bc / kPanel) * G * kChunkBytes + (bc % kPanel) * 32 + bh * (kSplit ? 8 : 16));
         const uint32_t sw_off =
@@ -282,16 +288,24 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
         int fg = 0, fend = 0;
         bool fdone = false;
         int64_t m0 = 0, panel0 = 0;
-        uint32_t a_bytes = 0, f_bytes = 0, s_bytes = 0, b_bytes = 0;
+        uint32_t a_bytes = 0, s_bytes = 0, b_bytes = 0;
+        // CONV: image row and column of this thread's output pixel m0 + dr
+        // (M < 2^26, so 32-bit arithmetic holds)
+        int conv_h = 0, conv_w = 0;
         auto set_ranges = [&] {
             m0 = (int64_t)fc.tm * BM;
             panel0 = (int64_t)fc.tn * (BN / kPanel);
             const int64_t rows = min(M - m0, (int64_t)BM);
             a_bytes = (uint32_t)(rows * 32);
-            f_bytes = (uint32_t)(rows * FB);
             s_bytes = (uint32_t)(rows * 2);
             const int64_t blk_panels = min(panels - panel0, (int64_t)kPanelsPerBlock);
             b_bytes = (uint32_t)((blk_panels - 1) * G * kChunkBytes + kChunkBytes);
+            if constexpr (CONV) {
+                const uint32_t m = (uint32_t)m0 + (uint32_t)dr;
+                const uint32_t q = m / (uint32_t)conv.W;
+                conv_w = (int)(m - q * (uint32_t)conv.W);
+                conv_h = (int)(q % (uint32_t)conv.H);
+            }
         };
         if (!cursor_begin(fresh_schedule(), blk, fc))
             return;
@@ -314,16 +328,36 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
         // since the stage a step writes is never read by another step.
         auto fetch_next = [&](Raw& r) {
             const int g = min(fg, fc.sg.g1 - 1);
-            const Rsrc ra = make_rsrc(codes + ((int64_t)g * M + m0) * 32, a_bytes);
-            const Rsrc rf = make_rsrc(flags + ((int64_t)g * M + m0) * FB, f_bytes);
+            // A rows of group g: a plane of the K-group-major arrays, its first
+            // row, the rows the buffer ranges cover, and this thread's row in
+            // it (in == false: offset 2^31, outside every range, reads zero)
+            int64_t plane = g, row0 = m0;
+            uint32_t range_rows = a_bytes / 32, lrow = (uint32_t)dr;
+            bool in = true;
+            if constexpr (CONV) {
+                // the channel block's whole plane, addressed by the pixel
+                // that g's tap shifts this output pixel to
+                const uint32_t tap = conv.cg == 1 ? (uint32_t)g : __umulhi((uint32_t)g, conv.div_magic);
+                const int dh = (int)(tap / 3u) - 1, dw = (int)(tap % 3u) - 1;
+                plane = g - (int)tap * conv.cg;
+                row0 = 0;
+                range_rows = (uint32_t)M;
+                lrow = (uint32_t)((int)m0 + dr + dh * conv.W + dw);
+                in = (uint32_t)(conv_h + dh) < (uint32_t)conv.H && (uint32_t)(conv_w + dw) < (uint32_t)conv.W;
+            }
+            const int64_t prow = plane * M + row0;
+            const Rsrc ra = make_rsrc(codes + prow * 32, range_rows * 32u);
+            const Rsrc rf = make_rsrc(flags + prow * FB, range_rows * (uint32_t)FB);
+            const uint32_t ao = in ? lrow * 32u + (uint32_t)(ah * 16) : 0x80000000u;
+            const uint32_t fo = in ? lrow * (uint32_t)FB : 0x80000000u;
             const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
-            r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off, 0, 0));
+            r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)ao, 0, 0));
             if constexpr (kSplit)
                 r.a1 = make_uint4(0, 0, 0, 0);
             else
                 r.a1 = __builtin_bit_cast(uint4,
-                                      __builtin_amdgcn_raw_buffer_load_b128(ra, (int)a_off + 16, 0, 0));
-            r.f = load_flags_raw<GS>(rf, f_off);
+                                      __builtin_amdgcn_raw_buffer_load_b128(ra, (int)ao + 16, 0, 0));
+            r.f = load_flags_raw<GS>(rf, fo);
             if constexpr (kSplit) {
                 const uint2 b2 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rb, (int)b_off, 0, 0));
                 r.b = make_uint4(b2.x, b2.y, 0, 0);
@@ -331,8 +365,8 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
             }
             if constexpr (kGroupScales) {   // the integer and static paths have none
-                const Rsrc rs = make_rsrc(scales + (int64_t)g * M + m0, s_bytes);
-                r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, (int)(dr * 2), 0, 0);
+                const Rsrc rs = make_rsrc(scales + prow, range_rows * 2u);
+                r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? (int)(lrow * 2u) : (int)0x80000000u, 0, 0);
                 r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
             } else {
                 r.sa = 0;
@@ -1170,16 +1204,16 @@ template <bool B>
 using bool_c = std::integral_constant<bool, B>;
 
 // Launch of one output mode, every G_s / epilogue / split combination of it.
-template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM>
+template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM, bool CONV = false>
 hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.sch.blocks);
     const dim3 block(STATIC && a.sch.sk_tiles == 0 ? kSplitThreadsPerBlock : kThreadsPerBlock);
     auto go = [&](auto gs, auto gelu, auto split) {
         w4a4_gemm_kernel<decltype(gs)::value, I32OUT, decltype(gelu)::value, decltype(split)::value,
-                         QOUT, STATIC, ASYM><<<grid, block, 0, stream>>>(
+                         QOUT, STATIC, ASYM, CONV><<<grid, block, 0, stream>>>(
             a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.yi, a.M, a.N, a.K, a.ldy, a.sch,
-            a.counters, a.slots, a.qout, a.act_scale, a.zeros, a.wsums);
+            a.counters, a.slots, a.qout, a.act_scale, a.zeros, a.wsums, a.conv);
     };
     auto with_split = [&](auto gs, auto gelu) {
         if (!I32OUT && a.sch.sk_tiles > 0)

@@ -152,34 +152,56 @@ def make_x(config: int, layer_index: int, rows: int | None = None) -> np.ndarray
     return to_bf16_bits(x)
 
 
+def _conv_shape(kind):
+    """(C, H) of an im2col_silu_c<C>_h<H> layer (square feature map H x H)."""
+    parts = kind.split("_")
+    return int(parts[2][1:]), int(parts[3][1:])
+
+
+def _feature_map(config, layer_index, img_rows, H, C):
+    """The first img_rows rows of the layer's H x H x C feature map (NHWC,
+    float64): SiLU(Laplace(0, 1)) with 0.5% of the C input channels x30."""
+    g = rng(config, layer_index, 0)
+    z = g.laplace(0.0, 1.0, size=(img_rows, H, C))
+    fmap = z / (1.0 + np.exp(-z))
+    fmap[:, :, _outlier_cols(config, layer_index, C, 0.005)] *= 30.0
+    return fmap
+
+
+def im2col3x3(fmap: np.ndarray, rows: int | None = None) -> np.ndarray:
+    """im2col of a 3 x 3 convolution, stride 1, padding 1, of one feature map
+    [Hs, W, C] (any dtype): row r = output pixel (r // W, r % W), K = 9 C
+    ordered (kh, kw, c) with c fastest; taps outside the map (or past its Hs
+    rows) read zero.  ``rows`` truncates to the first output pixels."""
+    Hs, W, C = fmap.shape
+    M = Hs * W if rows is None else rows
+    out = np.zeros((M, 9 * C), dtype=fmap.dtype)
+    oy, ox = np.divmod(np.arange(M), W)
+    for kh in range(3):
+        for kw in range(3):
+            iy, ix = oy + kh - 1, ox + kw - 1
+            ok = (iy >= 0) & (iy < Hs) & (ix >= 0) & (ix < W)
+            t = kh * 3 + kw
+            out[ok, t * C:(t + 1) * C] = fmap[iy[ok], ix[ok]]
+    return out
+
+
+def make_feature_map(config: int, layer_index: int, img_rows: int | None = None) -> np.ndarray:
+    """The NHWC feature map [img_rows][W][C] of a config-5 layer as bf16 bits;
+    make_x(config, layer) is its im2col (same values, same leading rows)."""
+    L = CONFIGS[config].layers[layer_index]
+    C, H = _conv_shape(L.x_kind)
+    return to_bf16_bits(_feature_map(config, layer_index, H if img_rows is None else img_rows, H, C))
+
+
 def _im2col_silu(config, layer_index, M, K, kind):
     """3x3 conv (padding 1) as GEMM: rows are output pixels, K = 9*C ordered
     (kh, kw, c) with c fastest; the feature map is SiLU(Laplace(0, 1)) with
     0.5% of the C input channels x30; border taps read zero padding."""
-    parts = kind.split("_")
-    C = int(parts[2][1:])
-    H = int(parts[3][1:])
+    C, H = _conv_shape(kind)
     assert K == 9 * C
-    g = rng(config, layer_index, 0)
-    rows_needed = M
-    n_img_rows = min(H, (rows_needed + H - 1) // H + 1)
-    z = g.laplace(0.0, 1.0, size=(n_img_rows, H, C))
-    fmap = z / (1.0 + np.exp(-z))
-    fmap[:, :, _outlier_cols(config, layer_index, C, 0.005)] *= 30.0
-    out = np.zeros((M, K))
-    for r in range(M):
-        oy, ox = divmod(r, H)
-        for kh in range(3):
-            iy = oy + kh - 1
-            if iy < 0 or iy >= n_img_rows or iy >= H:
-                continue
-            for kw in range(3):
-                ix = ox + kw - 1
-                if ix < 0 or ix >= H:
-                    continue
-                t = kh * 3 + kw
-                out[r, t * C:(t + 1) * C] = fmap[iy, ix]
-    return out
+    n_img_rows = min(H, (M + H - 1) // H + 1)
+    return im2col3x3(_feature_map(config, layer_index, n_img_rows, H, C), rows=M)
 
 
 def make_w(config: int, layer_index: int, rows: int | None = None) -> np.ndarray:
