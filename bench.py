@@ -307,6 +307,42 @@ def conv_layers(q, W, torch, np, gs, reps=10):
             "per_layer": out}
 
 
+def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=5):
+    """Cold-cache variant of each layer's quantizer and GEMM: a 512 MiB write
+    (twice the 256 MB Infinity Cache, far beyond L2) before each timed launch,
+    so no input is served from a cache that a previous launch warmed; times by
+    timed_chain (the flushes are timed too and dropped)."""
+    stream = torch.cuda.current_stream()
+    scratch = torch.empty((512 << 20,), dtype=torch.uint8, device=torch.device("cuda", 0))
+    flush = lambda: scratch.fill_(1)
+    res = []
+    for (x, w, b), (qa, pw, y), ws, L in zip(dev_in, outs, workspaces, cfg.layers):
+        t = timed_chain(torch, np, stream,
+                        [flush, lambda: q.quantize_act(x, lzs_group=gs, out=qa),
+                         flush, lambda: q.w4a4_linear(qa, pw, b, L.epilogue, out=y, workspace=ws)],
+                        reps)
+        qb, _, _ = layer_bytes(L, gs)
+        ops = 2.0 * L.M * L.N * L.K
+        res.append({"layer": L.name, "quantize_us": round(t[1], 2),
+                    "quantize_gbps": round(qb / (t[1] * 1e3), 1),
+                    "gemm_us": round(t[3], 2), "gemm_tflops": round(ops / (t[3] * 1e6), 1)})
+    del scratch
+    return {"flush": "512 MiB device write before each timed launch", "per_layer": res}
+
+
+def gpu_clocks():
+    """Current shader and memory clocks as rocm-smi reports them (a child
+    process reading the driver's counters; None if unavailable)."""
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                             text=True, timeout=30).stdout
+        card = next(iter(json.loads(out).values()))
+        return {k: v for k, v in card.items() if "sclk" in k or "mclk" in k or "fclk" in k}
+    except Exception:
+        return None
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -449,6 +485,9 @@ def main():
     torch.cuda.synchronize()
     q_stream_gbps = qrounds * qbytes.sum() / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
+    cold = cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs)
+    clocks = gpu_clocks()
+
     ldm = None
     if not args.no_ldm:
         t_l = time.time()
@@ -538,6 +577,8 @@ def main():
         "ldm_static": ldm,
         "asymmetric": asym,
         "conv3x3": conv,
+        "cold_cache": cold,
+        "gpu_clocks": clocks,
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
