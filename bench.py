@@ -62,8 +62,9 @@ def parse():
     ap.add_argument("--no-batched-mlp", action="store_true",
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--no-ldm", action="store_true",
-                    help="skip the LDM-setting (static activation scale), asymmetric-mode "
-                         "and implicit-GEMM convolution measurements")
+                    help="skip the secondary sections: LDM setting (static activation scale), "
+                         "asymmetric mode, implicit-GEMM convolutions, cold cache and the "
+                         "clocks under load (the profiling runs use this)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -343,6 +344,26 @@ def gpu_clocks():
         return None
 
 
+def clocks_under_load(torch, launch, launch_us, seconds=3.0):
+    """rocm-smi clock readings taken while `launch` (one GEMM) runs back to
+    back for about `seconds`: a thread samples while the main thread keeps
+    the queue full."""
+    import threading
+    samples = []
+
+    def sampler():
+        for _ in range(3):
+            samples.append(gpu_clocks())
+
+    th = threading.Thread(target=sampler)
+    th.start()
+    for _ in range(max(1, int(seconds * 1e6 / launch_us))):
+        launch()
+    torch.cuda.synchronize()
+    th.join()
+    return samples
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -485,8 +506,15 @@ def main():
     torch.cuda.synchronize()
     q_stream_gbps = qrounds * qbytes.sum() / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
-    cold = cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs)
-    clocks = gpu_clocks()
+    cold = clocks = load_clocks = None
+    if not args.no_ldm:
+        cold = cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs)
+        clocks = gpu_clocks()
+        (x0, w0, b0), (qa0, pw0, y0) = dev_in[0], outs[0]
+        load_clocks = clocks_under_load(
+            torch, lambda: q.w4a4_linear(qa0, pw0, b0, layers[0].epilogue, out=y0,
+                                         workspace=workspaces[0]),
+            per_layer[0]["gemm_us"])
 
     ldm = None
     if not args.no_ldm:
@@ -578,7 +606,7 @@ def main():
         "asymmetric": asym,
         "conv3x3": conv,
         "cold_cache": cold,
-        "gpu_clocks": clocks,
+        "gpu_clocks": {"after_run": clocks, "during_gemm": load_clocks},
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
