@@ -63,8 +63,8 @@ def parse():
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--no-ldm", action="store_true",
                     help="skip the secondary sections: LDM setting (static activation scale), "
-                         "asymmetric mode, implicit-GEMM convolutions, cold cache and the "
-                         "clocks under load (the profiling runs use this)")
+                         "asymmetric mode, implicit-GEMM convolutions, cold cache, the G_s "
+                         "sweep and the clocks under load (the profiling runs use this)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -331,6 +331,27 @@ def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=5):
     return {"flush": "512 MiB device write before each timed launch", "per_layer": res}
 
 
+def gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces, reps=10):
+    """The LZS subgroup sweep of Table 1 on the FLUX qkv layer: quantizer and
+    GEMM at G_s = 8, 16, 32 and 64 (timed_chain); the paper's numbers are
+    A100 latencies, context only."""
+    stream = torch.cuda.current_stream()
+    (x, w, b), (qa, pw, y), ws, L = dev_in[0], outs[0], workspaces[0], cfg.layers[0]
+    res = []
+    for g in (8, 16, 32, 64):
+        qg = q.quantize_act(x, lzs_group=g)
+        t = timed_chain(torch, np, stream,
+                        [lambda: q.quantize_act(x, lzs_group=g, out=qg),
+                         lambda: q.w4a4_linear(qg, pw, b, L.epilogue, out=y, workspace=ws)], reps)
+        qb = L.M * L.K * (2 + 0.5 + 1.0 / g + 2.0 / 64)
+        ops = 2.0 * L.M * L.N * L.K
+        res.append({"lzs_group": g, "quantize_us": round(t[0], 2),
+                    "quantize_gbps": round(qb / (t[0] * 1e3), 1), "gemm_us": round(t[1], 2),
+                    "gemm_tflops": round(ops / (t[1] * 1e6), 1)})
+        del qg
+    return {"layer": L.name, "M": L.M, "K": L.K, "N": L.N, "per_lzs_group": res}
+
+
 def gpu_clocks():
     """Current shader and memory clocks as rocm-smi reports them (a child
     process reading the driver's counters; None if unavailable)."""
@@ -506,9 +527,10 @@ def main():
     torch.cuda.synchronize()
     q_stream_gbps = qrounds * qbytes.sum() / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
-    cold = clocks = load_clocks = None
+    cold = clocks = load_clocks = sweep = None
     if not args.no_ldm:
         cold = cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs)
+        sweep = gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces)
         clocks = gpu_clocks()
         (x0, w0, b0), (qa0, pw0, y0) = dev_in[0], outs[0]
         load_clocks = clocks_under_load(
@@ -606,6 +628,7 @@ def main():
         "asymmetric": asym,
         "conv3x3": conv,
         "cold_cache": cold,
+        "lzs_group_sweep": sweep,
         "gpu_clocks": {"after_run": clocks, "during_gemm": load_clocks},
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
