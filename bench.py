@@ -6,15 +6,19 @@ transformer block at 4096 image + 512 text tokens (M = 4608): QKV 3072->9216,
 out 3072->3072, MLP fc1 3072->12288 and fc2 12288->3072, seeded synthetic
 bf16 activations / weights / bias (workloads.py), LZS subgroup G_s = 16.
 
-One step = one pass of the whole hot path over the block: for every layer,
-the weight pre-pack (RTN int4 + fp16 group scales), the activation quantizer
-(Stage 1 + LZS) and the W4A4 GEMM (fp8 MFMA, per-group dequant, bias).  All
-inputs are resident in HBM before the timed region.
+One step = one pass of the whole hot path over the block: the weight
+pre-pack (RTN int4 + fp16 group scales) of the four layers, then for every
+layer the activation quantizer (Stage 1 + LZS) and the W4A4 GEMM (fp8 MFMA,
+per-group dequant, bias).  All inputs are resident in HBM before the timed
+region.
 
 Prints ONE JSON line (stdout).  value = GEMM tera-ops (2 M N K summed over the
-layers) per second of whole steps.  roofline = the GEMM kernel (the dominant
-one): algorithmic ops / its average launch duration, from HIP events recorded
-on the launch stream inside the timed steps, against the fp8 dense MFMA peak.
+layers) per second of whole steps, from K steps with no event between the
+launches.  roofline = the GEMM kernel (the dominant one): algorithmic ops /
+its average launch duration, from HIP events recorded on the launch stream
+around every launch of K more steps run right after the timed ones (each
+event is a barrier in the queue, so those steps are not the ones
+ms_per_step is taken from), against the fp8 dense MFMA peak.
 cpu_baseline = the CPU oracle on a bounded sample of the same workload (all
 weights, the first --cpu-rows rows of every layer), on this host's cores.
 roofline.traffic = HBM bytes per GEMM launch from the FETCH_SIZE / WRITE_SIZE
@@ -443,38 +447,50 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(events=None):
-        for li, ((x, w, b), (qa, pw, y), ws, L) in enumerate(zip(dev_in, outs, workspaces,
-                                                                 layers)):
+        # the four weight packs, then quantize + GEMM layer by layer; with
+        # `events` (per layer: pack start, pack end, quantize start, quantize
+        # end, GEMM end) every launch is bracketed
+        items = list(zip(dev_in, outs, workspaces, layers))
+        for li, ((x, w, b), (qa, pw, y), ws, L) in enumerate(items):
             ev = events[li] if events is not None else None
             if ev: ev[0].record(stream)
             q.quartz_pack_weight(q._ptr(w), L.N, L.K, 64, q._ptr(pw.data), q._ptr(pw.scales),
                                  q._stream_handle())
             if ev: ev[1].record(stream)
-            q.quantize_act(x, lzs_group=gs, out=qa)
+        for li, ((x, w, b), (qa, pw, y), ws, L) in enumerate(items):
+            ev = events[li] if events is not None else None
             if ev: ev[2].record(stream)
-            q.w4a4_linear(qa, pw, b, L.epilogue, out=y, workspace=ws)
+            q.quantize_act(x, lzs_group=gs, out=qa)
             if ev: ev[3].record(stream)
+            q.w4a4_linear(qa, pw, b, L.epilogue, out=y, workspace=ws)
+            if ev: ev[4].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    ev_all = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
-              for _ in range(args.steps)]
+    # the K timed steps: nothing between the launches but the launches
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     start.record(stream)
     for s in range(args.steps):
-        step(ev_all[s])
+        step()
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
 
-    # per-kernel durations from the events of the timed steps
+    # then K more steps with an event pair around every launch, for the
+    # per-kernel durations (each event is a barrier in the queue, so these
+    # steps are slower as a whole and do not enter ms_per_step)
+    ev_all = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in layers]
+              for _ in range(args.steps)]
+    for s in range(args.steps):
+        step(ev_all[s])
+    torch.cuda.synchronize()
     t_pack = np.zeros(len(layers))
     t_quant = np.zeros(len(layers))
     t_gemm = np.zeros(len(layers))
@@ -482,8 +498,8 @@ def main():
         for li in range(len(layers)):
             e = ev_all[s][li]
             t_pack[li] += e[0].elapsed_time(e[1])
-            t_quant[li] += e[1].elapsed_time(e[2])
-            t_gemm[li] += e[2].elapsed_time(e[3])
+            t_quant[li] += e[2].elapsed_time(e[3])
+            t_gemm[li] += e[3].elapsed_time(e[4])
     t_pack /= args.steps
     t_quant /= args.steps
     t_gemm /= args.steps
@@ -602,7 +618,8 @@ def main():
             "workload": cfg.name,
             "layers": [f"{L.name} M={L.M} K={L.K} N={L.N}" for L in layers],
             "group_size": 64, "lzs_group": gs,
-            "step": "pack_weight + quantize_act + w4a4_linear (workspace entry point) per layer",
+            "step": "pack_weight of the 4 layers, then quantize_act + w4a4_linear (workspace "
+                    "entry point) per layer",
         },
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_FP8_TFLOPS,
@@ -614,7 +631,7 @@ def main():
         "quantize_roofline": {
             "bound": "hbm", "achieved": round(quant_gbps, 1), "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(quant_gbps / PEAK_HBM_GBPS, 4),
-            "per": "launch inside the timed steps (HIP events around each launch)",
+            "per": "launch inside the instrumented steps (HIP events around each launch)",
         },
         "quantize_sustained": {
             "bound": "hbm", "achieved": round(q_stream_gbps, 1), "peak": PEAK_HBM_GBPS,
