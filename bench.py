@@ -57,7 +57,10 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=50,
+                    help="untimed steps before the timed ones (the GPU needs a few tens of "
+                         "milliseconds of load to reach its steady clock: 5 steps leave the "
+                         "timed steps ~10 %% slower)")
     ap.add_argument("--config", type=int, default=3, help="workload config index (workloads.py)")
     ap.add_argument("--lzs-group", type=int, default=16)
     ap.add_argument("--cpu-rows", type=int, default=1536,
