@@ -148,3 +148,37 @@ def test_conv_config5_full_size(layer):
     wq, sw = oracle.quantize_weight(wb)
     y64, S = oracle.linear_f64(a_ref, wq, sw, bias_b, epilogue=0)
     _check(y[torch.from_numpy(rows).cuda()], y64, S, L.K, 0)
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2])
+def test_conv_static_config5_full_size(layer):
+    """The LDM setting of a config-5 layer at full size (workspace entry point,
+    G_s = 16, static scale max |x| / 127 of the map): bit for bit equal to the
+    explicit static GEMM on the host-built im2col matrix, and sampled pixels
+    (border and interior rows) against the oracle."""
+    import torch
+    q = _q()
+    cfg = 5
+    L = W.CONFIGS[cfg].layers[layer]
+    C, H = L.K // 9, int(round(L.M ** 0.5))
+    print(f"static conv full size layer {layer}: {H}x{H}x{C} -> {L.N}", flush=True)
+    fm = W.make_feature_map(cfg, layer)
+    s = float(np.float32(np.abs(W.bf16_bits_to_f32(fm)).max() / 127.0))
+    wb, bias_b = W.make_w(cfg, layer), W.make_bias(cfg, layer)
+    pw, bias = q.pack_weight_per_channel(to_dev_bf16(wb)), to_dev_bf16(bias_b)
+    ws = q.gemm_workspace(L.M, L.N, L.K, "cuda")
+    qa = q.quantize_act_static(to_dev_bf16(fm.reshape(L.M, C)), s, 16)
+    y = q.w4a4_conv3x3_static(qa, pw, s, 1, H, H, bias, 0, workspace=ws)
+    cols = W.make_x(cfg, layer)
+    qc = q.quantize_act_static(to_dev_bf16(cols), s, 16)
+    y_explicit = q.w4a4_linear_static(qc, pw, s, bias, 0, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y_explicit.view(torch.int16))
+    mid = (H // 2) * H
+    rows = np.unique(np.concatenate([np.arange(0, 6), np.arange(H - 3, H + 3), [mid - 1, mid, mid + H - 1],
+                                     np.arange(L.M - 6, L.M),
+                                     np.linspace(0, L.M - 1, 40).astype(np.int64)]))
+    a_ref = oracle.quantize_act_static(np.ascontiguousarray(cols[rows]), s, 16)
+    wq, sw = oracle.quantize_weight_per_channel(wb)
+    y64, S = oracle.linear_static_f64(a_ref, s, wq, sw, bias_b, 0)
+    _check(y[torch.from_numpy(rows).cuda()], y64, S, L.K, 0)
