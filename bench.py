@@ -72,6 +72,8 @@ def parse():
                     help="skip the secondary sections: LDM setting (static activation scale), "
                          "asymmetric mode, implicit-GEMM convolutions, cold cache, the G_s "
                          "sweep and the clocks under load (the profiling runs use this)")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="do not start rocm-smi (a child process) for the clock readings")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the known-size "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -550,12 +552,13 @@ def main():
     if not args.no_ldm:
         cold = cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs)
         sweep = gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces)
-        clocks = gpu_clocks()
-        (x0, w0, b0), (qa0, pw0, y0) = dev_in[0], outs[0]
-        load_clocks = clocks_under_load(
-            torch, lambda: q.w4a4_linear(qa0, pw0, b0, layers[0].epilogue, out=y0,
-                                         workspace=workspaces[0]),
-            per_layer[0]["gemm_us"])
+        if not args.no_clocks:
+            clocks = gpu_clocks()
+            (x0, w0, b0), (qa0, pw0, y0) = dev_in[0], outs[0]
+            load_clocks = clocks_under_load(
+                torch, lambda: q.w4a4_linear(qa0, pw0, b0, layers[0].epilogue, out=y0,
+                                             workspace=workspaces[0]),
+                per_layer[0]["gemm_us"])
 
     ldm = None
     if not args.no_ldm:
