@@ -398,8 +398,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the per-GPU share would be benchmarked as its own shape); use --gpus 1",
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(a per-GPU share would be benchmarked as its own shape); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
