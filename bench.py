@@ -593,18 +593,33 @@ def main():
         rows = args.cpu_rows
         t_c = time.perf_counter()
         sample_ops = 0.0
+        t_q = 0.0
+        q_bytes = 0.0
         for li, L in enumerate(layers):
             xb, wb, bb = host[li]
             wq, sw = oracle.quantize_weight(wb)
+            t0 = time.perf_counter()
             a = oracle.quantize_act(xb[:rows], lzs_group=gs)
+            t_q += time.perf_counter() - t0
+            q_bytes += layer_bytes(L, gs)[0] * rows / L.M
             oracle.linear_f64(a, wq, sw, bb, epilogue=L.epilogue)
             sample_ops += 2.0 * rows * L.N * L.K
         t_c = time.perf_counter() - t_c
+        cpu_model = None
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
         cpu = {"value": round(sample_ops / t_c / 1e12, 6), "unit": "TOPS",
                "cores": oracle.num_threads(), "kind": "oracle",
                "sample": (f"weight pack of all {len(layers)} layers + quantize and linear of the "
                           f"first {rows} of {layers[0].M} rows of every layer; "
-                          f"{t_c:.1f}s of CPU time")}
+                          f"{t_c:.1f}s of CPU time"),
+               "quantize_gbps": round(q_bytes / t_q / 1e9, 3),
+               "host": {"cpu_model": cpu_model, "nproc": os.cpu_count()}}
         log(f"cpu oracle sample: {t_c:.1f}s")
 
     result = {
