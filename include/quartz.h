@@ -119,9 +119,12 @@ quartz_status quartz_pack_weight(const void* w_bf16, int64_t N, int64_t K, int32
  * computed exactly (|P_g| <= 112 * 7 * 64 < 2^24); the scales and the sum
  * over groups are applied in fp32, act is the identity or GELU (tanh form).
  *
- *   codes, flags, scales, zeros   outputs of quartz_quantize_act for the same
- *                                 M, K, lzs_group (zeros may be NULL; the
- *                                 symmetric mode never needs it).
+ *   codes, flags, scales, zeros   outputs of quartz_quantize_act in
+ *                                 QUARTZ_MODE_SYMMETRIC for the same M, K,
+ *                                 lzs_group (zeros is not read and may be
+ *                                 NULL).  Codes of QUARTZ_MODE_ASYMMETRIC
+ *                                 need quartz_w4a4_linear_asym: their zero
+ *                                 points are not applied here.
  *   w_packed    output of quartz_pack_weight for N, K.
  *   bias_bf16   bf16 [N] or NULL.
  *   y_bf16      bf16 [M][ldy], N <= ldy <= 2^24.
@@ -293,7 +296,10 @@ quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* fla
  * quartz_unpack_weight: int8 [N][K] weight codes wq recovered from w_packed.
  * quartz_w4a4_gemm_i32: the exact integer accumulator
  *   acc[m][n] = sum_k (c[m,k] * 2^FLAG) * wq[n,k]   (int32 [M][N], row-major),
- * i.e. the sum of the per-group integer MMA results before any scaling.
+ * i.e. the sum of the per-group integer MMA results before any scaling
+ * (Section 4.4's s32 accumulation): each group product is exact and the
+ * groups are added in int32, so acc is exact for every K accepted
+ * (|acc| <= 784 K <= 784 * 2^20 < 2^31).
  */
 quartz_status quartz_unpack_weight(const void* w_packed, int64_t N, int64_t K,
                                    int32_t group_size, int8_t* wq_out, hipStream_t stream);

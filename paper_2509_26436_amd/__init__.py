@@ -28,6 +28,7 @@ __all__ = [
     "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "weight_group_sums",
     "w4a4_linear_asym", "linear_schedule", "w4a4_conv3x3", "w4a4_conv3x3_static",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
+    "MODE_SYMMETRIC", "MODE_ASYMMETRIC", "MODE_STATIC",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -36,6 +37,8 @@ _LIB_PATH = os.path.join(_HERE, "libquartz.so")
 QUARTZ_OK = 0
 MODE_SYMMETRIC = 0
 MODE_ASYMMETRIC = 1
+# binding-side tag of activations from quantize_act_static (no per-group scales)
+MODE_STATIC = 2
 EPI_NONE = 0
 EPI_GELU_TANH = 1
 GROUP = 64
@@ -258,6 +261,20 @@ class QuantizedAct:
     M: int
     K: int
     lzs_group: int
+    mode: int = MODE_SYMMETRIC   # MODE_SYMMETRIC, MODE_ASYMMETRIC or MODE_STATIC
+
+
+_LAYER_FOR_MODE = {MODE_SYMMETRIC: "w4a4_linear / w4a4_linear_quantize / w4a4_conv3x3",
+                   MODE_ASYMMETRIC: "w4a4_linear_asym",
+                   MODE_STATIC: "w4a4_linear_static / w4a4_conv3x3_static"}
+
+
+def _need_mode(a: "QuantizedAct", mode: int, what: str):
+    """Each layer decodes one quantizer mode: symmetric codes fed to the
+    asymmetric layer (or the reverse) would give wrong outputs silently."""
+    if a.mode != mode:
+        raise ValueError(f"{what} needs activations quantized in mode {mode}, got mode {a.mode}; "
+                         f"use {_LAYER_FOR_MODE.get(a.mode, 'the matching layer')}")
 
 
 @dataclass
@@ -286,7 +303,9 @@ def quantize_act(x, lzs_group: int = 16, with_zeros: bool = False, stream=None,
             scales=torch.empty((G, M), dtype=torch.int16, device=dev),
             zeros=(torch.empty((G, M), dtype=torch.int8, device=dev)
                    if with_zeros or mode == MODE_ASYMMETRIC else None),
-            M=M, K=K, lzs_group=lzs_group)
+            M=M, K=K, lzs_group=lzs_group, mode=mode)
+    else:
+        out.mode = mode
     st = quartz_quantize_act(_ptr(x), M, K, ldx, GROUP, lzs_group, mode,
                              _ptr(out.codes), _ptr(out.flags), _ptr(out.scales), _ptr(out.zeros),
                              _stream_handle(stream))
@@ -321,6 +340,7 @@ def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI
     """Returns y bf16 [M, N] (or writes ``out``, a bf16 [M, >=N] view with unit column stride).
     With ``workspace`` (from ``gemm_workspace``) the call is quartz_w4a4_linear_ws."""
     torch = _torch()
+    _need_mode(a, MODE_SYMMETRIC, "w4a4_linear")
     if a.K != w.K:
         raise ValueError("K mismatch between activations and weights")
     if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
@@ -361,6 +381,7 @@ def w4a4_linear_quantize(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: 
     QuantizedAct with M = a.M rows and K = w.N (w.N % 64 == 0), equal to
     ``quantize_act(w4a4_linear(a, w, ...), out_lzs_group)``."""
     torch = _torch()
+    _need_mode(a, MODE_SYMMETRIC, "w4a4_linear_quantize")
     if a.K != w.K:
         raise ValueError("K mismatch between activations and weights")
     if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
@@ -390,7 +411,9 @@ def quantize_act_static(x, scale: float, lzs_group: int = 16, stream=None,
         out = QuantizedAct(
             codes=torch.empty((G, M, 32), dtype=torch.uint8, device=x.device),
             flags=torch.empty((G, M, GROUP // lzs_group), dtype=torch.uint8, device=x.device),
-            scales=None, zeros=None, M=M, K=K, lzs_group=lzs_group)
+            scales=None, zeros=None, M=M, K=K, lzs_group=lzs_group, mode=MODE_STATIC)
+    else:
+        out.mode = MODE_STATIC
     st = quartz_quantize_act_static(_ptr(x), M, K, x.stride(0), float(scale), lzs_group,
                                     _ptr(out.codes), _ptr(out.flags), _stream_handle(stream))
     _check(st, "quartz_quantize_act_static")
@@ -418,6 +441,7 @@ def w4a4_linear_static(a: QuantizedAct, w: PackedWeight, act_scale: float, bias=
     """LDM-setting layer (quartz_w4a4_linear_static): ``a`` from quantize_act_static with
     ``act_scale``, ``w`` from pack_weight_per_channel; returns y bf16 [M, N]."""
     torch = _torch()
+    _need_mode(a, MODE_STATIC, "w4a4_linear_static")
     if a.K != w.K:
         raise ValueError("K mismatch between activations and weights")
     if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
@@ -447,6 +471,7 @@ def w4a4_linear_asym(a: QuantizedAct, w: PackedWeight, w_sums, bias=None,
     """Asymmetric-mode layer (quartz_w4a4_linear_asym): ``a`` from quantize_act with
     ``mode=MODE_ASYMMETRIC``, ``w_sums`` from weight_group_sums(w)."""
     torch = _torch()
+    _need_mode(a, MODE_ASYMMETRIC, "w4a4_linear_asym")
     if a.K != w.K or a.zeros is None:
         raise ValueError("need asymmetric activations with zero points and matching K")
     if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
@@ -483,6 +508,7 @@ def w4a4_conv3x3(a: QuantizedAct, w: PackedWeight, images: int, H: int, W: int, 
     [images * H * W, C], ``w`` = pack_weight of the weight [N, 9 C] ordered
     (kh, kw, c); returns y bf16 [images * H * W, N] (the workspace from
     ``gemm_workspace(images * H * W, N, 9 C)``)."""
+    _need_mode(a, MODE_SYMMETRIC, "w4a4_conv3x3")
     C, out = _conv_args(a, w, images, H, W, bias, out)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = quartz_w4a4_conv3x3(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(w.data),
@@ -499,6 +525,7 @@ def w4a4_conv3x3_static(a: QuantizedAct, w: PackedWeight, act_scale: float, imag
     """The LDM-setting convolution (quartz_w4a4_conv3x3_static): ``a`` =
     quantize_act_static of the feature map with ``act_scale``, ``w`` =
     pack_weight_per_channel of the weight [N, 9 C]."""
+    _need_mode(a, MODE_STATIC, "w4a4_conv3x3_static")
     C, out = _conv_args(a, w, images, H, W, bias, out)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = quartz_w4a4_conv3x3_static(_ptr(a.codes), _ptr(a.flags), float(act_scale), _ptr(w.data),

@@ -295,9 +295,9 @@ hipError_t launch_pack(const uint16_t* w, int64_t N, int64_t K, uint8_t* w_packe
     const int64_t panels = (N + kPanel - 1) / kPanel;
     const int64_t gpairs = (K / 64 + kGroupsPerItem - 1) / kGroupsPerItem;
     const int64_t items = panels * (kPanel / 8) * gpairs;
-    // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
+    // up to 32 waves per compute unit, each walking the items with a grid stride
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock,
-                               (int64_t)(256 * 32 / kWavesPerBlock));
+                               (int64_t)device_compute_units() * 32 / kWavesPerBlock);
     pack_weight_kernel<PER_CHANNEL><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
         w, N, K, panels, w_packed, w_scales);
     return hipGetLastError();

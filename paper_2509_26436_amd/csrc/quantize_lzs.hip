@@ -270,8 +270,8 @@ hipError_t launch_gs(const uint16_t* x, int64_t M, int64_t K, int64_t ldx, uint8
     const int64_t G = K / 64;
     const int64_t quads = (G + kGroupsPerItem - 1) / kGroupsPerItem;
     const int64_t items = (M + 7) / 8 * quads;
-    // up to 32 waves per CU on 256 CUs, each walking the items with a grid stride
-    const int64_t max_blocks = 256 * 32 / kWavesPerBlock;
+    // up to 32 waves per compute unit, each walking the items with a grid stride
+    const int64_t max_blocks = (int64_t)device_compute_units() * 32 / kWavesPerBlock;
     const int64_t blocks = min((items + kWavesPerBlock - 1) / kWavesPerBlock, max_blocks);
     quantize_act_kernel<GS, MODE><<<dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0, stream>>>(
         x, M, G, ldx, quads, items, codes, flags, scales, zeros, r_static);

@@ -59,6 +59,10 @@ GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool spl
 size_t gemm_workspace_bytes(const GemmSchedule& s);
 int gemm_resident_blocks();
 
+// Compute units of the current device (queried once per device and cached;
+// 256 if the query fails): the grid-stride kernels size their grids by it.
+int device_compute_units();
+
 // Destination of an output quantized for the next layer (its K is this
 // layer's N): the arrays of quartz_quantize_act with M rows and N / 64
 // groups; codes == nullptr means a plain bf16 output.

@@ -600,11 +600,17 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     static_assert(TM == 2 && TN == 2, "prefetch order assumes 2 x 2 tiles");
     v16f p_next, p_last, s_last;       // product of the next tile; last tile's P and S
     const v16f zero = {};
+    // I32OUT: acc holds int32 bit patterns and each exact group product is
+    // converted and added in int32, so the sum over K stays exact beyond 2^24
+    // (|P_g| <= 50176 converts exactly; |sum| <= 784 K < 2^31 for K <= 2^20).
+    auto add_i32 = [](float a, float p) {
+        return __int_as_float(__float_as_int(a) + (int)p);
+    };
     auto fma_tile = [&](int i, int j, const v16f& p, const v16f& sc) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             if constexpr (I32OUT)
-                acc[i][j][r] += p[r];
+                acc[i][j][r] = add_i32(acc[i][j][r], p[r]);
             else
                 acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
         }
@@ -654,7 +660,7 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
 #pragma unroll
         for (int r = r0; r < r0 + 8; ++r) {
             if constexpr (I32OUT)
-                acc[i][j][r] += p[r];
+                acc[i][j][r] = add_i32(acc[i][j][r], p[r]);
             else
                 acc[i][j][r] = fmaf(p[r], sc[r], acc[i][j][r]);
         }
@@ -973,7 +979,7 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                     for (int r = 0; r < 16; ++r) {
                         const int64_t row = (int64_t)cur.tm * BM + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
                         if (row < M)
-                            yi[row * N + col] = (int32_t)out[i][j][r];
+                            yi[row * N + col] = __float_as_int(out[i][j][r]);
                     }
                 }
             }

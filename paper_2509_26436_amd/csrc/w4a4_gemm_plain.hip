@@ -14,6 +14,27 @@ hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream)
     return launch_mode<true, false, false, false>(a, stream);
 }
 
+int device_compute_units()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 256;
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices];
+    if (dev < kMaxDevices) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0)
+            return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        return 256;
+    if (dev < kMaxDevices)
+        cache[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
 int gemm_resident_blocks()
 {
     int dev = 0;

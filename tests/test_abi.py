@@ -229,3 +229,30 @@ def test_product_path_does_not_touch_the_oracle():
             if fn.endswith((".py", ".hip", ".h", ".cpp")):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in text.lower(), fn
+
+
+def test_layers_reject_activations_of_another_mode():
+    """The tensor helpers refuse codes of a quantizer mode the layer does not
+    decode (asymmetric codes into the symmetric layer would drop their zero
+    points silently); checked before anything reaches the library."""
+    import torch
+    G, M, K = 2, 4, 128
+    def act(mode):
+        return q.QuantizedAct(codes=torch.zeros((G, M, 32), dtype=torch.uint8),
+                              flags=torch.zeros((G, M, 4), dtype=torch.uint8),
+                              scales=torch.zeros((G, M), dtype=torch.int16),
+                              zeros=torch.zeros((G, M), dtype=torch.int8),
+                              M=M, K=K, lzs_group=16, mode=mode)
+    w = q.PackedWeight(data=torch.zeros(8, dtype=torch.uint8), scales=None, N=64, K=K)
+    calls = {
+        q.MODE_SYMMETRIC: [lambda a: q.w4a4_linear(a, w), lambda a: q.w4a4_linear_quantize(a, w)],
+        q.MODE_ASYMMETRIC: [lambda a: q.w4a4_linear_asym(a, w, None)],
+        q.MODE_STATIC: [lambda a: q.w4a4_linear_static(a, w, 1.0)],
+    }
+    for want, fns in calls.items():
+        for other in calls:
+            if other == want:
+                continue
+            for fn in fns:
+                with pytest.raises(ValueError, match="mode"):
+                    fn(act(other))

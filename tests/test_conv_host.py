@@ -38,6 +38,37 @@ def test_im2col_against_a_plain_loop():
                 np.testing.assert_array_equal(cols[r, (3 * kh + kw) * 2:(3 * kh + kw + 1) * 2], want)
 
 
+@pytest.mark.parametrize("H,Wd,C", [(1, 1, 3), (3, 4, 2), (5, 7, 64), (6, 3, 128)])
+def test_im2col_against_torch_unfold(H, Wd, C):
+    """The host im2col against torch.nn.functional.unfold (kernel 3, padding 1):
+    unfold orders K as (c, kh, kw), so its columns are permuted to (kh, kw, c)
+    with c fastest, the order the convolution layers use."""
+    import torch
+    fm = np.random.Generator(np.random.PCG64(1000 + H * Wd * C)).normal(size=(H, Wd, C))
+    cols = W.im2col3x3(fm)
+    t = torch.from_numpy(np.ascontiguousarray(fm.transpose(2, 0, 1)))[None]      # [1][C][H][W]
+    u = torch.nn.functional.unfold(t, kernel_size=3, padding=1)[0]             # [C*9][H*W]
+    ref = u.reshape(C, 3, 3, H * Wd).permute(3, 1, 2, 0).reshape(H * Wd, 9 * C).numpy()
+    np.testing.assert_array_equal(cols, ref)
+
+
+def test_im2col_gemm_equals_torch_conv2d():
+    """The (kh, kw, c) im2col matrix times the weight [N][9 C] laid out the same
+    way equals torch's float64 conv2d (stride 1, padding 1) of the map: the
+    convention the implicit GEMM and the oracle's input share is the usual
+    convolution, not just the builder's own loop."""
+    import torch
+    rng = np.random.Generator(np.random.PCG64(1001))
+    H, Wd, C, N = 5, 6, 64, 7
+    fm = rng.normal(size=(H, Wd, C))
+    wt = rng.normal(size=(N, C, 3, 3))                          # torch layout [N][C][kh][kw]
+    w_rows = wt.transpose(0, 2, 3, 1).reshape(N, 9 * C)         # [N][(kh, kw, c)]
+    y = W.im2col3x3(fm) @ w_rows.T                              # [H*W][N]
+    ref = torch.nn.functional.conv2d(torch.from_numpy(np.ascontiguousarray(fm.transpose(2, 0, 1)))[None],
+                                     torch.from_numpy(wt), padding=1)[0]       # [N][H][W]
+    np.testing.assert_allclose(y, ref.permute(1, 2, 0).reshape(H * Wd, N).numpy(), rtol=1e-12, atol=1e-12)
+
+
 def _gathered(per_pixel, images, H, Wd, C, zero):
     """Rows of the im2col matrix built from a per-pixel, per-channel-block array
     [C/64][images*H*W][...] by tap, `zero` where the tap leaves the image."""
