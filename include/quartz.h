@@ -176,6 +176,34 @@ quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * quartz_w4a4_linear_noalloc: quartz_w4a4_linear_ws for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments as quartz_w4a4_linear,
+ * same results as quartz_w4a4_linear_ws with a workspace (the same schedule
+ * and split, hence bit-identical outputs), but the stream-K partial sums and
+ * counters live in a scratch array the library holds in device memory on
+ * every GPU it runs on, until the process ends:
+ *   - its size is quartz_w4a4_linear_noalloc_max_bytes() (64 MiB + 64 KiB,
+ *     the workspace of a persistent grid of up to 256 workgroups); a shape
+ *     whose workspace (quartz_w4a4_linear_workspace_bytes) is larger returns
+ *     QUARTZ_ERR_WORKSPACE and launches nothing;
+ *   - nothing is allocated: no hipMalloc, hipFree or allocating library call;
+ *   - each call first clears the counters with a small kernel on `stream`
+ *     (no memset node, so the call may be captured into a graph);
+ *   - every call on one GPU shares that GPU's array: calls that overlap in
+ *     time on one GPU (two streams, two threads) race and give wrong results.
+ * Errors as for quartz_w4a4_linear_ws.
+ */
+quartz_status quartz_w4a4_linear_noalloc(const uint8_t* codes, const uint8_t* flags,
+                                         const uint16_t* scales, const int8_t* zeros,
+                                         const void* w_packed, const void* bias_bf16, void* y_bf16,
+                                         int64_t M, int64_t N, int64_t K, int64_t ldy,
+                                         int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                         hipStream_t stream);
+
+size_t quartz_w4a4_linear_noalloc_max_bytes(void);
+
+/*
  * W4A4 linear layer whose output is quantized on the fly for the next layer
  * (Appendix C applies the 4-bit compression on the fly; Eq. 1 and Eq. 2 as
  * for quartz_quantize_act): the bf16 values quartz_w4a4_linear_ws would

@@ -23,6 +23,7 @@ __all__ = [
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
     "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
     "quartz_w4a4_conv3x3", "quartz_w4a4_conv3x3_static",
+    "quartz_w4a4_linear_noalloc", "quartz_w4a4_linear_noalloc_max_bytes", "w4a4_linear_noalloc",
     "quartz_status_string", "QuantizedAct", "PackedWeight",
     "quantize_act", "pack_weight", "w4a4_linear", "w4a4_linear_quantize", "gemm_workspace",
     "quantize_act_static", "pack_weight_per_channel", "w4a4_linear_static", "weight_group_sums",
@@ -50,6 +51,7 @@ EXPORTED_SYMBOLS = (
     "quartz_w4a4_linear_quantize", "quartz_quantize_act_static", "quartz_pack_weight_per_channel",
     "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
     "quartz_w4a4_conv3x3", "quartz_w4a4_conv3x3_static", "quartz_status_string",
+    "quartz_w4a4_linear_noalloc", "quartz_w4a4_linear_noalloc_max_bytes",
 )
 
 
@@ -90,6 +92,11 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_linear_ws.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32, I32,
                                           P, SZ, P]
     lib.quartz_w4a4_linear_ws.restype = I32
+    lib.quartz_w4a4_linear_noalloc.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I32, I32,
+                                               I32, P]
+    lib.quartz_w4a4_linear_noalloc.restype = I32
+    lib.quartz_w4a4_linear_noalloc_max_bytes.argtypes = []
+    lib.quartz_w4a4_linear_noalloc_max_bytes.restype = SZ
     F32 = ctypes.c_float
     lib.quartz_quantize_act_static.argtypes = [P, I64, I64, I64, F32, I32, P, P, P]
     lib.quartz_quantize_act_static.restype = I32
@@ -160,6 +167,16 @@ def quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, 
     return load().quartz_w4a4_linear_ws(codes, flags, scales, zeros, w_packed, bias, y, M, N, K,
                                         ldy, group_size, lzs_group, epilogue, workspace,
                                         workspace_bytes, stream)
+
+
+def quartz_w4a4_linear_noalloc(codes, flags, scales, zeros, w_packed, bias, y, M, N, K, ldy,
+                               group_size, lzs_group, epilogue, stream) -> int:
+    return load().quartz_w4a4_linear_noalloc(codes, flags, scales, zeros, w_packed, bias, y, M, N,
+                                             K, ldy, group_size, lzs_group, epilogue, stream)
+
+
+def quartz_w4a4_linear_noalloc_max_bytes() -> int:
+    return int(load().quartz_w4a4_linear_noalloc_max_bytes())
 
 
 def quartz_w4a4_linear_quantize(codes, flags, scales, zeros, w_packed, bias, M, N, K,
@@ -360,6 +377,28 @@ def w4a4_linear(a: QuantizedAct, w: PackedWeight, bias=None, epilogue: int = EPI
                                    workspace.numel() * workspace.element_size(),
                                    _stream_handle(stream))
         _check(st, "quartz_w4a4_linear_ws")
+    return out
+
+
+def w4a4_linear_noalloc(a: QuantizedAct, w: PackedWeight, out, bias=None,
+                        epilogue: int = EPI_NONE, stream=None):
+    """quartz_w4a4_linear_noalloc into the caller's ``out`` (bf16 [M, >=N] with unit
+    column stride): the split layer of ``w4a4_linear(..., workspace=...)`` using the
+    library's device scratch array, so this call allocates nothing."""
+    torch = _torch()
+    _need_mode(a, MODE_SYMMETRIC, "w4a4_linear_noalloc")
+    if a.K != w.K:
+        raise ValueError("K mismatch between activations and weights")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != w.N):
+        raise ValueError("bias must be bf16 [N]")
+    if out.dtype != torch.bfloat16 or out.dim() != 2 or out.stride(1) != 1 or \
+            out.shape[0] != a.M or out.shape[1] < w.N:
+        raise ValueError("out must be a bf16 [M, >=N] tensor with unit column stride")
+    st = quartz_w4a4_linear_noalloc(_ptr(a.codes), _ptr(a.flags), _ptr(a.scales), _ptr(a.zeros),
+                                    _ptr(w.data), _ptr(bias), _ptr(out), a.M, w.N, a.K,
+                                    out.stride(0), GROUP, a.lzs_group, epilogue,
+                                    _stream_handle(stream))
+    _check(st, "quartz_w4a4_linear_noalloc")
     return out
 
 

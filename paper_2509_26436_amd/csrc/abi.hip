@@ -215,7 +215,8 @@ static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
                                  const void* bias_bf16, void* y_bf16, int64_t M, int64_t N,
                                  int64_t K, int64_t ldy, int32_t group_size, int32_t lzs_group,
                                  int32_t epilogue, void* workspace, size_t workspace_bytes,
-                                 const quartz::QuantOut* qout, hipStream_t stream)
+                                 const quartz::QuantOut* qout, hipStream_t stream,
+                                 bool use_scratch = false)
 {
     if (epilogue != QUARTZ_EPI_NONE && epilogue != QUARTZ_EPI_GELU_TANH)
         return QUARTZ_ERR_UNSUPPORTED;
@@ -236,10 +237,22 @@ static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
         (qout && (!aligned16(qout->codes) || !aligned16(qout->flags) ||
                   !aligned16(qout->scales) || (qout->zeros && !aligned16(qout->zeros)))))
         return QUARTZ_ERR_ALIGN;
-    const quartz::GemmSchedule sch =
-        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+    const quartz::GemmSchedule sch = quartz::gemm_schedule(
+        M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr || use_scratch);
     if (sch.blocks <= 0)
         return QUARTZ_ERR_HIP;          // no usable device
+    if (use_scratch) {
+        // the device's own scratch array in place of a workspace: nothing is
+        // allocated; its counters are cleared by a kernel on this stream
+        workspace_bytes = quartz::noalloc_scratch_bytes();
+        if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+            return QUARTZ_ERR_WORKSPACE;
+        if (quartz::noalloc_scratch(&workspace) != hipSuccess)
+            return QUARTZ_ERR_HIP;
+        if (quartz::clear_noalloc_counters(workspace, quartz::gemm_counter_bytes(sch), stream) !=
+            hipSuccess)
+            return QUARTZ_ERR_HIP;
+    }
     if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
         return QUARTZ_ERR_WORKSPACE;
     return from_hip(quartz::launch_w4a4_linear(
@@ -279,6 +292,23 @@ quartz_status quartz_w4a4_linear_ws(const uint8_t* codes, const uint8_t* flags,
     return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
                        group_size, lzs_group, epilogue, workspace, workspace_bytes, nullptr,
                        stream);
+}
+
+quartz_status quartz_w4a4_linear_noalloc(const uint8_t* codes, const uint8_t* flags,
+                                         const uint16_t* scales, const int8_t* zeros,
+                                         const void* w_packed, const void* bias_bf16, void* y_bf16,
+                                         int64_t M, int64_t N, int64_t K, int64_t ldy,
+                                         int32_t group_size, int32_t lzs_group, int32_t epilogue,
+                                         hipStream_t stream)
+{
+    (void)zeros;
+    return linear_impl(codes, flags, scales, w_packed, bias_bf16, y_bf16, M, N, K, ldy,
+                       group_size, lzs_group, epilogue, nullptr, 0, nullptr, stream, true);
+}
+
+size_t quartz_w4a4_linear_noalloc_max_bytes(void)
+{
+    return quartz::noalloc_scratch_bytes();
 }
 
 quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags,

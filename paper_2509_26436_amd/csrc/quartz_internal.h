@@ -58,6 +58,15 @@ hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, i
 GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split);
 size_t gemm_workspace_bytes(const GemmSchedule& s);
 int gemm_resident_blocks();
+// bytes of the workspace's counter part (its start); the slots follow it
+size_t gemm_counter_bytes(const GemmSchedule& s);
+
+// The device scratch array of quartz_w4a4_linear_noalloc (scratch.hip): its
+// size, its address on the current device (resolved once per device), and
+// the fill kernel that zeroes its first counter_bytes on `stream`.
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void** ptr);
+hipError_t clear_noalloc_counters(void* ptr, size_t counter_bytes, hipStream_t stream);
 
 // Compute units of the current device (queried once per device and cached;
 // 256 if the query fails): the grid-stride kernels size their grids by it.

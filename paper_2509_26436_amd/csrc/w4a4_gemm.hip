@@ -64,6 +64,11 @@ GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool spl
     return s;
 }
 
+size_t gemm_counter_bytes(const GemmSchedule& s)
+{
+    return s.sk_tiles > 0 ? counter_bytes(s) : 0;
+}
+
 size_t gemm_workspace_bytes(const GemmSchedule& s)
 {
     if (s.sk_tiles == 0)
