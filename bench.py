@@ -43,6 +43,7 @@ if ROOT not in sys.path:
 
 PEAK_FP8_TFLOPS = 5000.0      # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+SETTLE_S = 0.25               # untimed load before the timed steps (clock settling)
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
                 for f in ("w4a4_gemm_kernel.h", "w4a4_gemm.hip", "w4a4_gemm_plain.hip",
@@ -126,10 +127,10 @@ def layer_bytes(L, gs):
     return quant, pack, gemm
 
 
-def batched_mlp(q, W, torch, np, gs, reps=5):
+def batched_mlp(q, W, torch, np, gs, reps=20):
     """The batched FLUX MLP at M = 18432 (4 images x 4608 tokens) as one pipeline:
     quantize x -> fc1 3072->12288 with the GELU epilogue -> quantize -> fc2
-    12288->3072.  Per layer: mean quantize and GEMM time over `reps` passes
+    12288->3072.  Per layer: median quantize and GEMM time over `reps` passes
     (timed_chain), and the end-to-end time against the
     sum of the two roofline times (quantize bytes at 8 TB/s + GEMM ops at the
     fp8 dense peak).  Then the same pipeline with fc2's input quantized in
@@ -188,8 +189,8 @@ def batched_mlp(q, W, torch, np, gs, reps=5):
 
 
 def timed_chain(torch, np, stream, calls, reps):
-    """Mean HIP-event time (us) of each launch in `calls` over `reps` passes of
-    the whole chain, queued back to back after two untimed passes with one
+    """Median HIP-event time (us) of each launch in `calls` over `reps` passes
+    of the whole chain, queued back to back after two untimed passes with one
     synchronization at the end: every launch but the very first follows
     another kernel, as inside a step, so no timed launch starts from an idle
     queue."""
@@ -202,13 +203,73 @@ def timed_chain(torch, np, stream, calls, reps):
             ev[k + 1].record(stream)
         evs.append(ev)
     torch.cuda.synchronize()
-    t = np.zeros(len(calls))
-    for ev in evs[2:]:
-        t += np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(len(calls))])
-    return t / reps * 1e3
+    t = np.array([[ev[k].elapsed_time(ev[k + 1]) for k in range(len(calls))] for ev in evs[2:]])
+    return np.median(t, axis=0) * 1e3
 
 
-def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
+def copy_ceiling_us(torch, np, stream, moved_bytes, reps=20):
+    """Median time (us) of a plain device-to-device copy that moves
+    `moved_bytes` in all (half read, half written), launched back to back
+    (timed_chain), and the bytes it moves: the measured ceiling a streaming
+    kernel of that size is compared with."""
+    n = max(256, int(moved_bytes // 2) // 256 * 256)
+    src = torch.empty(n, dtype=torch.uint8, device=torch.device("cuda", 0))
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    t = timed_chain(torch, np, stream, [lambda: dst.copy_(src)], reps)[0]
+    del src, dst
+    return float(t), 2 * n
+
+
+def config_layers(q, W, torch, np, config, gs, reps=20):
+    """The other workloads of the benchmark set, layer by layer (the single
+    256 x 1152 -> 1152 linear; the PixArt-Sigma 1024px block): per layer the
+    quantizer (GB/s, fraction of the HBM peak and of a same-size device copy
+    timed in the same run) and the GEMM through the workspace entry point
+    (TFLOP/s, fraction of the fp8 peak), medians of `reps` launches
+    (timed_chain); config 1 also without bias."""
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    cfg = W.CONFIGS[config]
+    to = lambda a: torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+    out = []
+    for li, L in enumerate(cfg.layers):
+        x, w, b = to(W.make_x(config, li)), to(W.make_w(config, li)), to(W.make_bias(config, li))
+        qa = q.quantize_act(x, gs)
+        pw = q.pack_weight(w)
+        ws = q.gemm_workspace(L.M, L.N, L.K, dev)
+        y = q.w4a4_linear(qa, pw, b, L.epilogue, workspace=ws)
+        calls = [lambda: q.quantize_act(x, gs, out=qa),
+                 lambda: q.w4a4_linear(qa, pw, b, L.epilogue, out=y, workspace=ws)]
+        if config == 1:
+            calls.append(lambda: q.w4a4_linear(qa, pw, None, L.epilogue, out=y, workspace=ws))
+        t = timed_chain(torch, np, stream, calls, reps)
+        qb, _, _ = layer_bytes(L, gs)
+        tc, moved = copy_ceiling_us(torch, np, stream, qb, reps)
+        ops = 2.0 * L.M * L.N * L.K
+        r = {"layer": L.name, "M": L.M, "K": L.K, "N": L.N,
+             "quantize_us": round(t[0], 2), "quantize_gbps": round(qb / (t[0] * 1e3), 1),
+             "quantize_frac": round(qb / (t[0] * 1e3) / PEAK_HBM_GBPS, 4),
+             "copy_us": round(tc, 2), "copy_gbps": round(moved / (tc * 1e3), 1),
+             "quantize_copy_frac": round(tc / t[0] * qb / moved, 4),
+             "gemm_us": round(t[1], 2), "gemm_tflops": round(ops / (t[1] * 1e6), 1),
+             "gemm_frac": round(ops / (t[1] * 1e6) / PEAK_FP8_TFLOPS, 4)}
+        if config == 1:
+            r["gemm_no_bias_us"] = round(t[2], 2)
+            r["gemm_no_bias_tflops"] = round(ops / (t[2] * 1e6), 1)
+        out.append(r)
+        del x, w, b, qa, pw, ws, y
+    tot_ops = sum(2.0 * L.M * L.N * L.K for L in cfg.layers)
+    tot_us = sum(r["gemm_us"] for r in out)
+    return {"workload": cfg.name, "lzs_group": gs,
+            "step": "quantize_act + w4a4_linear (workspace entry point) per layer"
+                    + ("; the GEMM again without bias" if config == 1 else ""),
+            "gemm_tflops": round(tot_ops / (tot_us * 1e6), 1),
+            "gemm_frac": round(tot_ops / (tot_us * 1e6) / PEAK_FP8_TFLOPS, 4),
+            "per_layer": out}
+
+
+def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=20):
     """The LDM setting (static per-tensor activation scale, per-channel weight
     scales; the K loop is pure integer MFMA) on the same layers: per layer the
     static quantizer and GEMM times (timed_chain).  The static scale is fixed once from
@@ -240,7 +301,7 @@ def ldm_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
             "per_layer": out}
 
 
-def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
+def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=20):
     """The asymmetric mode (per-group zero points; one extra fp16 correction
     MFMA per tile) on the same layers: per layer the quantizer and GEMM times
     (timed_chain).  The weight group sums are computed once, outside."""
@@ -271,7 +332,7 @@ def asym_layers(q, W, torch, np, cfg, dev_in, gs, reps=10):
             "per_layer": out}
 
 
-def conv_layers(q, W, torch, np, gs, reps=10):
+def conv_layers(q, W, torch, np, gs, reps=20):
     """The SDXL UNet 3 x 3 convolutions (config 5) as implicit GEMMs: per layer
     the feature map's quantizer and the convolution (quartz_w4a4_conv3x3,
     workspace entry point), then the same in the LDM setting (static
@@ -317,7 +378,7 @@ def conv_layers(q, W, torch, np, gs, reps=10):
             "per_layer": out}
 
 
-def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=5):
+def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=20):
     """Cold-cache variant of each layer's quantizer and GEMM: a 512 MiB write
     (twice the 256 MB Infinity Cache, far beyond L2) before each timed launch,
     so no input is served from a cache that a previous launch warmed; times by
@@ -340,7 +401,7 @@ def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=5):
     return {"flush": "512 MiB device write before each timed launch", "per_layer": res}
 
 
-def gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces, reps=10):
+def gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces, reps=20):
     """The LZS subgroup sweep of Table 1 on the FLUX qkv layer: quantizer and
     GEMM at G_s = 8, 16, 32 and 64 (timed_chain); the paper's numbers are
     A100 latencies, context only."""
@@ -450,6 +511,7 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
+    t_warm0 = time.perf_counter()
 
     def step(events=None):
         # the four weight packs, then quantize + GEMM layer by layer; with
@@ -473,6 +535,16 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # Clock settling, part of the protocol: the GPU needs a few tens of
+    # milliseconds of sustained load to reach its steady clock, so untimed
+    # steps continue until SETTLE_S of work have run since the first warmup
+    # step (at least the W warmup steps; reported as "settle").
+    settle_steps = 0
+    while time.perf_counter() - t_warm0 < SETTLE_S:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
+        settle_steps += 10
 
     # the K timed steps: nothing between the launches but the launches
     start = torch.cuda.Event(enable_timing=True)
@@ -496,18 +568,15 @@ def main():
     for s in range(args.steps):
         step(ev_all[s])
     torch.cuda.synchronize()
-    t_pack = np.zeros(len(layers))
-    t_quant = np.zeros(len(layers))
-    t_gemm = np.zeros(len(layers))
-    for s in range(args.steps):
-        for li in range(len(layers)):
-            e = ev_all[s][li]
-            t_pack[li] += e[0].elapsed_time(e[1])
-            t_quant[li] += e[2].elapsed_time(e[3])
-            t_gemm[li] += e[3].elapsed_time(e[4])
-    t_pack /= args.steps
-    t_quant /= args.steps
-    t_gemm /= args.steps
+    # per launch: [step][layer] durations in ms; the means are what the
+    # roofline divides by (the rocprofv3 statistics report averages), the
+    # medians are reported beside them
+    def durations(a, b):
+        return np.array([[ev_all[s][li][a].elapsed_time(ev_all[s][li][b])
+                          for li in range(len(layers))] for s in range(args.steps)])
+    d_pack, d_quant, d_gemm = durations(0, 1), durations(2, 3), durations(3, 4)
+    t_pack, t_quant, t_gemm = d_pack.mean(0), d_quant.mean(0), d_gemm.mean(0)
+    m_quant, m_gemm = np.median(d_quant, 0), np.median(d_gemm, 0)
 
     ops = np.array([2.0 * L.M * L.N * L.K for L in layers])
     qbytes = np.array([layer_bytes(L, gs)[0] for L in layers])
@@ -515,7 +584,11 @@ def main():
     gbytes = np.array([layer_bytes(L, gs)[2] for L in layers])
     value = ops.sum() / (ms_per_step * 1e-3) / 1e12
     gemm_tflops = ops.sum() / (t_gemm.sum() * 1e-3) / 1e12
+    gemm_tflops_median = ops.sum() / (m_gemm.sum() * 1e-3) / 1e12
     quant_gbps = qbytes.sum() / (t_quant.sum() * 1e-3) / 1e9
+    quant_gbps_median = qbytes.sum() / (m_quant.sum() * 1e-3) / 1e9
+    # the same bytes moved by a plain device copy, timed in this run
+    copies = [copy_ceiling_us(torch, np, stream, qb) for qb in qbytes]
     pack_gbps = pbytes.sum() / (t_pack.sum() * 1e-3) / 1e9
 
     per_layer = []
@@ -523,9 +596,16 @@ def main():
         per_layer.append({
             "layer": L.name, "M": L.M, "K": L.K, "N": L.N,
             "gemm_us": round(t_gemm[li] * 1e3, 2),
+            "gemm_us_median": round(m_gemm[li] * 1e3, 2),
             "gemm_tflops": round(ops[li] / (t_gemm[li] * 1e-3) / 1e12, 1),
+            "gemm_frac": round(ops[li] / (t_gemm[li] * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4),
             "quantize_us": round(t_quant[li] * 1e3, 2),
+            "quantize_us_median": round(m_quant[li] * 1e3, 2),
             "quantize_gbps": round(qbytes[li] / (t_quant[li] * 1e-3) / 1e9, 1),
+            "copy_us": round(copies[li][0], 2),
+            "copy_gbps": round(copies[li][1] / (copies[li][0] * 1e3), 1),
+            "quantize_copy_frac": round(copies[li][0] / (m_quant[li] * 1e3)
+                                        * qbytes[li] / copies[li][1], 4),
             "pack_us": round(t_pack[li] * 1e3, 2),
             "pack_gbps": round(pbytes[li] / (t_pack[li] * 1e-3) / 1e9, 1),
         })
@@ -578,6 +658,14 @@ def main():
         conv = conv_layers(q, W, torch, np, gs)
         log(f"implicit-GEMM convolutions measured in {time.time() - t_c:.1f}s")
 
+    others = {}
+    if not args.no_ldm:
+        t_o = time.time()
+        for c in (1, 2):
+            if c != args.config:
+                others[f"config{c}"] = config_layers(q, W, torch, np, c, gs)
+        log(f"configs 1 and 2 measured in {time.time() - t_o:.1f}s")
+
     mlp = None
     if not args.no_batched_mlp:
         del outs, dev_in, workspaces
@@ -629,6 +717,9 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"steps": settle_steps, "seconds": SETTLE_S,
+                   "why": "untimed steps after the warmup until SETTLE_S of load have run, so "
+                          "the timed steps see the GPU's steady clock"},
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -645,6 +736,7 @@ def main():
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_FP8_TFLOPS,
             "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
+            "achieved_median": round(gemm_tflops_median, 1),
             "traffic": traffic,
             "algorithmic_bytes": round(float(gbytes.mean())),
             "per": f"GEMM launch, mean over the {len(layers)} layers",
@@ -652,7 +744,12 @@ def main():
         "quantize_roofline": {
             "bound": "hbm", "achieved": round(quant_gbps, 1), "peak": PEAK_HBM_GBPS,
             "unit": "GB/s", "frac": round(quant_gbps / PEAK_HBM_GBPS, 4),
-            "per": "launch inside the instrumented steps (HIP events around each launch)",
+            "achieved_median": round(quant_gbps_median, 1),
+            "copy_frac": round(sum(c[0] for c in copies) / (m_quant.sum() * 1e3)
+                               * qbytes.sum() / sum(c[1] for c in copies), 4),
+            "per": "launch inside the instrumented steps (HIP events around each launch); "
+                   "copy_frac: median quantizer time against a device copy moving the same "
+                   "bytes, timed in this run",
         },
         "quantize_sustained": {
             "bound": "hbm", "achieved": round(q_stream_gbps, 1), "peak": PEAK_HBM_GBPS,
@@ -661,6 +758,7 @@ def main():
         },
         "pack_gbps": round(pack_gbps, 1),
         "per_layer": per_layer,
+        **others,
         "batched_mlp": mlp,
         "ldm_static": ldm,
         "asymmetric": asym,
