@@ -89,6 +89,10 @@ def _load():
     lib.qo_weight_group_sums.restype = I32
     lib.qo_linear_asym_f64.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I32, I32, P, P]
     lib.qo_linear_asym_f64.restype = I32
+    lib.qo_quantize_f32.argtypes = [P, I64, I64, I64, I32, P, P, P]
+    lib.qo_quantize_f32.restype = I32
+    lib.qo_softmax_rows.argtypes = [P, I64, I64, I64, P]
+    lib.qo_softmax_rows.restype = I32
     lib.qo_round_bf16.argtypes = [P, I64, P]
     lib.qo_round_bf16.restype = None
     lib.qo_num_threads.argtypes = []
@@ -418,3 +422,79 @@ def linear_asym_f64(a: ActQuant, wq: np.ndarray, sw: np.ndarray, bias_bits=None,
     if rc != 0:
         raise ValueError("oracle linear_asym_f64: invalid arguments")
     return y, s
+
+
+# ------------------------------------------------ LZS attention (reading R11)
+
+def quantize_f32(x: np.ndarray, lzs_group: int = 16) -> ActQuant:
+    """The activation quantizer on binary32 inputs x [M][K] (float32): the
+    form it takes on the softmax output."""
+    x = _c(x, np.float32)
+    M, K = x.shape
+    c = np.empty((M, K), np.int8)
+    flags = np.empty((M, K // lzs_group), np.uint8)
+    scales = np.empty((M, K // 64), np.uint16)
+    rc = _load().qo_quantize_f32(_ptr(x), M, K, K, lzs_group, _ptr(c), _ptr(flags), _ptr(scales))
+    if rc != 0:
+        raise ValueError("oracle quantize_f32: invalid arguments")
+    return ActQuant(None, c, flags, scales, np.zeros((M, K // 64), np.int8), lzs_group)
+
+
+def softmax_rows(S: np.ndarray) -> np.ndarray:
+    """Row softmax of float64 scores, in double, returned as float32."""
+    S = _c(S, np.float64)
+    M, N = S.shape
+    P = np.empty((M, N), np.float32)
+    if _load().qo_softmax_rows(_ptr(S), M, N, N, _ptr(P)) != 0:
+        raise ValueError("oracle softmax_rows: invalid arguments")
+    return P
+
+
+def _as_operand(a: ActQuant):
+    """An LZS-quantized activation used as the second operand of a product:
+    its decoded integers c * 2^FLAG (in [-112, 112], so int8) and its fp16
+    group scales, in the (wq, sw) form linear_f64 takes."""
+    d = a.decoded()
+    return d.astype(np.int8), a.scales
+
+
+def attn_scores_f64(q: ActQuant, k: ActQuant, scale: float, rows=None, cols=None):
+    """Scores of one head, S = (Q~ K~^T) * scale with Q~, K~ the quantized
+    queries [Lq][d] and keys [Lk][d]: per (i, j) the exact integer products of
+    the two 64-groups along d times s_q s_k, summed in double.  With rows /
+    cols (index arrays of equal length) only those entries.  Returns (S, A)
+    with A = sum_g |s_q s_k P_g| * |scale| (the accumulation's scale)."""
+    kd, ks = _as_operand(k)
+    if rows is None:
+        S, A = linear_f64(q, kd, ks, None)
+    else:
+        S, A = linear_f64_sampled(q, kd, ks, None, rows, cols)
+    return S * scale, A * abs(scale)
+
+
+def attn_pv_f64(p: ActQuant, vt: ActQuant, rows=None, cols=None):
+    """Output of one head from the quantized softmax output P~ [Lq][Lk] and the
+    quantized transposed values V~^T [d][Lk] (quantized along the keys):
+    O = P~ V~, per (i, c) the exact integer products of the 64-key groups
+    times s_p s_v, summed in double.  Returns (O, A) as attn_scores_f64."""
+    vd, vs = _as_operand(vt)
+    if rows is None:
+        return linear_f64(p, vd, vs, None)
+    return linear_f64_sampled(p, vd, vs, None, rows, cols)
+
+
+def lzs_attention_f64(qb, kb, vb, lzs_group: int = 16):
+    """One head of LZS attention (reading R11) on bf16 inputs q, k, v [L][d]:
+    quantize Q and K along d and V^T along the keys, scores in double, row
+    softmax, the softmax output rounded to binary32 and quantized like an
+    activation, then O = P~ V~ in double.  Returns (O, parts) with the
+    intermediate quantities."""
+    d = qb.shape[1]
+    qa = quantize_act(qb, lzs_group)
+    ka = quantize_act(kb, lzs_group)
+    vta = quantize_act(np.ascontiguousarray(np.asarray(vb).T), lzs_group)
+    S, _ = attn_scores_f64(qa, ka, 1.0 / np.sqrt(d))
+    P = softmax_rows(S)
+    pa = quantize_f32(P, lzs_group)
+    O, A = attn_pv_f64(pa, vta)
+    return O, {"q": qa, "k": ka, "vt": vta, "S": S, "P": P, "p": pa, "A": A}

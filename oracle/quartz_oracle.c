@@ -705,6 +705,80 @@ int qo_linear_static_f64(const int8_t* c, const uint8_t* flags, float s, const i
     return QO_OK;
 }
 
+/* -------------------------------------------- LZS attention (reading R11) */
+
+/*
+ * The activation quantizer (Eq. 1 under R1/R2, then Eq. 2 and the right
+ * shift per subgroup) applied to binary32 inputs instead of bf16 ones: the
+ * form it takes on the softmax output, which is computed in binary32.  Per
+ * 64-group: alpha = max |x|, s16 = fp16(alpha / 127), r = 1/s,
+ * q = clamp(rne(fp32(x r)), -127, 127).  Outputs as qo_quantize_act
+ * (row-major c [M][K], flags [M][K/lzs_group], scales [M][K/64]).
+ */
+int qo_quantize_f32(const float* x, int64_t M, int64_t K, int64_t ldx, int lzs_group, int8_t* c,
+                    uint8_t* flags, uint16_t* scales)
+{
+    if (lzs_group < 1 || 64 % lzs_group != 0 || K % 64 != 0 || ldx < K)
+        return QO_EINVAL;
+    const int64_t G = K / 64, S = K / lzs_group;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+        for (int64_t g = 0; g < G; ++g) {
+            const float* xg = x + m * ldx + g * 64;
+            float alpha = 0.0f;
+            for (int k = 0; k < 64; ++k) {
+                float a = fabsf(xg[k]);
+                if (a > alpha)
+                    alpha = a;
+            }
+            uint16_t s16 = qo_f32_to_f16_rne_sat(alpha / 127.0f);
+            float sv = qo_f16_to_f32(s16);
+            float r = (sv == 0.0f) ? 0.0f : 1.0f / sv;
+            int8_t q[64];
+            for (int k = 0; k < 64; ++k) {
+                double v = qo_rne((double)(xg[k] * r));
+                if (v > 127.0)
+                    v = 127.0;
+                if (v < -127.0)
+                    v = -127.0;
+                q[k] = (int8_t)v;
+            }
+            scales[m * G + g] = s16;
+            for (int j = 0; j < 64 / lzs_group; ++j) {
+                int64_t sub = g * (64 / lzs_group) + j;
+                flags[m * S + sub] = (uint8_t)qo_lzs_subgroup(q + j * lzs_group, lzs_group,
+                                                               c + m * K + g * 64 + j * lzs_group);
+            }
+        }
+    }
+    return QO_OK;
+}
+
+/*
+ * Row softmax of scores S [M][lds] (N columns) in double:
+ *   P[i][j] = exp(S[i][j] - max_j S[i][j]) / sum_j exp(S[i][j] - max_j S[i][j]),
+ * stored as binary32 (round to nearest) in P [M][N].
+ */
+int qo_softmax_rows(const double* S, int64_t M, int64_t N, int64_t lds, float* P)
+{
+    if (N <= 0 || lds < N)
+        return QO_EINVAL;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < M; ++i) {
+        const double* row = S + i * lds;
+        double mx = row[0];
+        for (int64_t j = 1; j < N; ++j)
+            if (row[j] > mx)
+                mx = row[j];
+        double sum = 0.0;
+        for (int64_t j = 0; j < N; ++j)
+            sum += exp(row[j] - mx);
+        for (int64_t j = 0; j < N; ++j)
+            P[i * N + j] = (float)(exp(row[j] - mx) / sum);
+    }
+    return QO_OK;
+}
+
 /*
  * bf16 bit patterns (round to nearest even) of n float64 values: the bf16
  * output a layer stores for its float64 results, elementwise.
