@@ -383,6 +383,85 @@ quartz_status quartz_w4a4_conv3x3_static(const uint8_t* codes, const uint8_t* fl
                                          size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * LZS attention: the attention setting of the paper's hardware appendix
+ * (Table 8: heads x 128, G_s 8 / 16 / 32), read as follows (the paper leaves
+ * the operation open): per head, O = softmax(Q K^T / sqrt(d)) V, non-causal,
+ * where Q, K, V and the softmax output are all activations and so each goes
+ * through the activation quantizer (Eq. 1, Eq. 2) -- Q and K per token along
+ * d, V^T per channel along the keys, the softmax output P (computed in fp32)
+ * per query row in 64-key groups -- and both products are exact per-group
+ * integer products with the two fp16 group scales applied in fp32, as in the
+ * linear layer (Section 4.4).  S is kept in fp32 between the products.
+ *
+ * quartz_quantize_vt: V^T quantized along the keys.
+ *   v_bf16   bf16 [heads * L][ldv]: row h * L + j is key j of head h, d channels.
+ *   codes    u8  [L/64][heads * d][32]   (row h * d + c: channel c of head h)
+ *   flags    u8  [L/64][heads * d][64/lzs_group],  scales u16 [L/64][heads * d]
+ *   L % 64 == 0, d % 64 == 0, d <= ldv, ldv % 8 == 0.
+ *
+ * quartz_attn_scores: one head's scores, s[i][j] = scale * sum over the
+ * 64-groups of d of s_q s_k P_g (fp32), i < Lq, j < Lk, row stride lds >= Lk.
+ *   q_*   quartz_quantize_act outputs for queries with K = d; the head's rows
+ *         are rows q_row0 .. q_row0 + Lq - 1 of planes of q_plane rows (the M
+ *         of that call); k_* likewise for the keys.
+ *
+ * quartz_softmax_quantize: s fp32 [M][lds] (N columns, N % 64 == 0) ->
+ *   P = exp(s - rowmax) / rowsum in fp32, then quartz_quantize_act's Stage 1
+ *   and Stage 2 on the fp32 values of P with K = N: codes [N/64][M][32],
+ *   flags [N/64][M][64/lzs_group], scales [N/64][M].
+ *
+ * quartz_attn_pv: one head's output o[i][c] = bf16(sum over 64-key groups of
+ *   s_p s_v P_g) for i < Lq, c < d (row stride ldo >= d), from the quantized
+ *   softmax output (quartz_softmax_quantize with M = Lq, N = Lk) and V^T
+ *   (quartz_quantize_vt; the head's channels are rows vt_row0 .. + d - 1 of
+ *   planes of vt_plane rows).  workspace / workspace_bytes as for
+ *   quartz_w4a4_linear_ws (size: quartz_attn_pv_workspace_bytes; NULL, 0: no
+ *   split tiles).
+ *
+ * quartz_lzs_attention: all heads end to end.
+ *   q_bf16, k_bf16, v_bf16   bf16 [heads][L][d], contiguous.
+ *   o_bf16   bf16 [L][ldo], ldo >= heads * d: head h in columns h d .. h d + d - 1.
+ *   workspace  quartz_lzs_attention_workspace_bytes(heads, L, d, lzs_group)
+ *              bytes, zero-filled before its first use (every call leaves its
+ *              first part zero again); it holds the quantized Q, K, V^T of all
+ *              heads and one head's fp32 scores and quantized softmax output.
+ *   L % 64 == 0 (L <= 2^16), d % 64 == 0.  The heads run one after another on
+ *   `stream`; calls that share a workspace must not overlap.
+ * Errors as for the other entry points; lzs_group must be 8, 16, 32 or 64.
+ */
+quartz_status quartz_quantize_vt(const void* v_bf16, int64_t heads, int64_t L, int64_t d,
+                                 int64_t ldv, int32_t lzs_group, uint8_t* codes, uint8_t* flags,
+                                 uint16_t* scales, hipStream_t stream);
+
+quartz_status quartz_attn_scores(const uint8_t* q_codes, const uint8_t* q_flags,
+                                 const uint16_t* q_scales, int64_t q_plane, int64_t q_row0,
+                                 const uint8_t* k_codes, const uint8_t* k_flags,
+                                 const uint16_t* k_scales, int64_t k_plane, int64_t k_row0,
+                                 int64_t Lq, int64_t Lk, int64_t d, int32_t lzs_group, float scale,
+                                 float* s, int64_t lds, hipStream_t stream);
+
+quartz_status quartz_softmax_quantize(const float* s, int64_t M, int64_t N, int64_t lds,
+                                      int32_t lzs_group, uint8_t* codes, uint8_t* flags,
+                                      uint16_t* scales, hipStream_t stream);
+
+size_t quartz_attn_pv_workspace_bytes(int64_t Lq, int64_t Lk, int64_t d);
+
+quartz_status quartz_attn_pv(const uint8_t* p_codes, const uint8_t* p_flags,
+                             const uint16_t* p_scales, const uint8_t* vt_codes,
+                             const uint8_t* vt_flags, const uint16_t* vt_scales, int64_t vt_plane,
+                             int64_t vt_row0, int64_t Lq, int64_t Lk, int64_t d,
+                             int32_t lzs_group, void* o_bf16, int64_t ldo, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+size_t quartz_lzs_attention_workspace_bytes(int64_t heads, int64_t L, int64_t d,
+                                            int32_t lzs_group);
+
+quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const void* v_bf16,
+                                   int64_t heads, int64_t L, int64_t d, int32_t lzs_group,
+                                   void* o_bf16, int64_t ldo, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/*
  * quartz_w4a4_linear_schedule (host only, needs no GPU): the GEMM work
  * schedule for a persistent grid of at most `blocks` workgroups (the entry
  * points use the device's compute-unit count), with (split = 1, as

@@ -30,6 +30,10 @@ __all__ = [
     "w4a4_linear_asym", "linear_schedule", "w4a4_conv3x3", "w4a4_conv3x3_static",
     "unpack_weight", "w4a4_gemm_i32", "EXPORTED_SYMBOLS",
     "MODE_SYMMETRIC", "MODE_ASYMMETRIC", "MODE_STATIC",
+    "quartz_quantize_vt", "quartz_attn_scores", "quartz_softmax_quantize",
+    "quartz_attn_pv_workspace_bytes", "quartz_attn_pv", "quartz_lzs_attention_workspace_bytes",
+    "quartz_lzs_attention", "quantize_vt", "attn_scores", "softmax_quantize", "attn_pv",
+    "attention_workspace", "lzs_attention",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -52,6 +56,9 @@ EXPORTED_SYMBOLS = (
     "quartz_w4a4_linear_static", "quartz_weight_group_sums", "quartz_w4a4_linear_asym",
     "quartz_w4a4_conv3x3", "quartz_w4a4_conv3x3_static", "quartz_status_string",
     "quartz_w4a4_linear_noalloc", "quartz_w4a4_linear_noalloc_max_bytes",
+    "quartz_quantize_vt", "quartz_attn_scores", "quartz_softmax_quantize",
+    "quartz_attn_pv_workspace_bytes", "quartz_attn_pv", "quartz_lzs_attention_workspace_bytes",
+    "quartz_lzs_attention",
 )
 
 
@@ -125,6 +132,22 @@ def load() -> ctypes.CDLL:
     lib.quartz_unpack_weight.restype = I32
     lib.quartz_w4a4_gemm_i32.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P]
     lib.quartz_w4a4_gemm_i32.restype = I32
+    lib.quartz_quantize_vt.argtypes = [P, I64, I64, I64, I64, I32, P, P, P, P]
+    lib.quartz_quantize_vt.restype = I32
+    lib.quartz_attn_scores.argtypes = [P, P, P, I64, I64, P, P, P, I64, I64, I64, I64, I64, I32,
+                                       F32, P, I64, P]
+    lib.quartz_attn_scores.restype = I32
+    lib.quartz_softmax_quantize.argtypes = [P, I64, I64, I64, I32, P, P, P, P]
+    lib.quartz_softmax_quantize.restype = I32
+    lib.quartz_attn_pv_workspace_bytes.argtypes = [I64, I64, I64]
+    lib.quartz_attn_pv_workspace_bytes.restype = SZ
+    lib.quartz_attn_pv.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I32, P, I64, P, SZ,
+                                   P]
+    lib.quartz_attn_pv.restype = I32
+    lib.quartz_lzs_attention_workspace_bytes.argtypes = [I64, I64, I64, I32]
+    lib.quartz_lzs_attention_workspace_bytes.restype = SZ
+    lib.quartz_lzs_attention.argtypes = [P, P, P, I64, I64, I64, I32, P, I64, P, SZ, P]
+    lib.quartz_lzs_attention.restype = I32
     lib.quartz_status_string.argtypes = [I32]
     lib.quartz_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -244,6 +267,40 @@ def quartz_w4a4_gemm_i32(codes, flags, w_packed, acc, M, N, K, group_size, lzs_g
                          stream) -> int:
     return load().quartz_w4a4_gemm_i32(codes, flags, w_packed, acc, M, N, K, group_size,
                                        lzs_group, stream)
+
+
+def quartz_quantize_vt(v, heads, L, d, ldv, lzs_group, codes, flags, scales, stream) -> int:
+    return load().quartz_quantize_vt(v, heads, L, d, ldv, lzs_group, codes, flags, scales, stream)
+
+
+def quartz_attn_scores(qc, qf, qs, q_plane, q_row0, kc, kf, ks, k_plane, k_row0, Lq, Lk, d,
+                       lzs_group, scale, s, lds, stream) -> int:
+    return load().quartz_attn_scores(qc, qf, qs, q_plane, q_row0, kc, kf, ks, k_plane, k_row0, Lq,
+                                     Lk, d, lzs_group, scale, s, lds, stream)
+
+
+def quartz_softmax_quantize(s, M, N, lds, lzs_group, codes, flags, scales, stream) -> int:
+    return load().quartz_softmax_quantize(s, M, N, lds, lzs_group, codes, flags, scales, stream)
+
+
+def quartz_attn_pv_workspace_bytes(Lq, Lk, d) -> int:
+    return int(load().quartz_attn_pv_workspace_bytes(Lq, Lk, d))
+
+
+def quartz_attn_pv(pc, pf, ps, vc, vf, vs, vt_plane, vt_row0, Lq, Lk, d, lzs_group, o, ldo,
+                   workspace, workspace_bytes, stream) -> int:
+    return load().quartz_attn_pv(pc, pf, ps, vc, vf, vs, vt_plane, vt_row0, Lq, Lk, d, lzs_group,
+                                 o, ldo, workspace, workspace_bytes, stream)
+
+
+def quartz_lzs_attention_workspace_bytes(heads, L, d, lzs_group) -> int:
+    return int(load().quartz_lzs_attention_workspace_bytes(heads, L, d, lzs_group))
+
+
+def quartz_lzs_attention(q, k, v, heads, L, d, lzs_group, o, ldo, workspace, workspace_bytes,
+                         stream) -> int:
+    return load().quartz_lzs_attention(q, k, v, heads, L, d, lzs_group, o, ldo, workspace,
+                                       workspace_bytes, stream)
 
 
 # ------------------------------------------------------------- tensor helpers
@@ -610,4 +667,101 @@ def w4a4_gemm_i32(a: QuantizedAct, w: PackedWeight, stream=None):
     st = quartz_w4a4_gemm_i32(_ptr(a.codes), _ptr(a.flags), _ptr(w.data), _ptr(out), a.M, w.N,
                               a.K, GROUP, a.lzs_group, _stream_handle(stream))
     _check(st, "quartz_w4a4_gemm_i32")
+    return out
+
+
+# ------------------------------------------------------------- LZS attention
+
+def quantize_vt(v, heads: int, lzs_group: int = 16, stream=None) -> QuantizedAct:
+    """V^T quantized along the keys (quartz_quantize_vt): v bf16 [heads * L, d]
+    (rows head * L + key) -> a QuantizedAct with M = heads * d rows (row
+    head * d + channel) and K = L."""
+    torch = _torch()
+    if v.dtype != torch.bfloat16 or v.dim() != 2 or v.stride(1) != 1 or v.shape[0] % heads:
+        raise ValueError("v must be a bf16 [heads * L, d] tensor with unit column stride")
+    L, d = v.shape[0] // heads, v.shape[1]
+    out = _empty_act(heads * d, L, lzs_group, False, v.device)
+    st = quartz_quantize_vt(_ptr(v), heads, L, d, v.stride(0), lzs_group, _ptr(out.codes),
+                            _ptr(out.flags), _ptr(out.scales), _stream_handle(stream))
+    _check(st, "quartz_quantize_vt")
+    return out
+
+
+def attn_scores(q: QuantizedAct, k: QuantizedAct, q_row0: int, k_row0: int, Lq: int, Lk: int,
+                scale: float, out=None, stream=None):
+    """fp32 scores [Lq, Lk] = scale * Q~ K~^T of one head, the head's rows at
+    q_row0 / k_row0 of the quantized queries / keys of all heads."""
+    torch = _torch()
+    _need_mode(q, MODE_SYMMETRIC, "attn_scores")
+    _need_mode(k, MODE_SYMMETRIC, "attn_scores")
+    if q.K != k.K or q.lzs_group != k.lzs_group:
+        raise ValueError("queries and keys need the same d and G_s")
+    if out is None:
+        out = torch.empty((Lq, Lk), dtype=torch.float32, device=q.codes.device)
+    st = quartz_attn_scores(_ptr(q.codes), _ptr(q.flags), _ptr(q.scales), q.M, q_row0,
+                            _ptr(k.codes), _ptr(k.flags), _ptr(k.scales), k.M, k_row0, Lq, Lk,
+                            q.K, q.lzs_group, float(scale), _ptr(out), out.stride(0),
+                            _stream_handle(stream))
+    _check(st, "quartz_attn_scores")
+    return out
+
+
+def softmax_quantize(s, lzs_group: int = 16, out: QuantizedAct | None = None,
+                     stream=None) -> QuantizedAct:
+    """Row softmax of fp32 scores [M, N] quantized like an activation with K = N."""
+    torch = _torch()
+    if s.dtype != torch.float32 or s.dim() != 2 or s.stride(1) != 1:
+        raise ValueError("s must be a 2-D fp32 tensor with unit column stride")
+    M, N = s.shape
+    if out is None:
+        out = _empty_act(M, N, lzs_group, False, s.device)
+    st = quartz_softmax_quantize(_ptr(s), M, N, s.stride(0), lzs_group, _ptr(out.codes),
+                                 _ptr(out.flags), _ptr(out.scales), _stream_handle(stream))
+    _check(st, "quartz_softmax_quantize")
+    return out
+
+
+def attn_pv(p: QuantizedAct, vt: QuantizedAct, vt_row0: int, d: int, out=None, stream=None,
+            workspace=None):
+    """bf16 [Lq, d] = P~ V~ of one head: p from softmax_quantize, vt from
+    quantize_vt (the head's channels at rows vt_row0 .. vt_row0 + d - 1)."""
+    torch = _torch()
+    if p.K != vt.K or p.lzs_group != vt.lzs_group:
+        raise ValueError("the softmax output and V^T need the same key count and G_s")
+    if out is None:
+        out = torch.empty((p.M, d), dtype=torch.bfloat16, device=p.codes.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = quartz_attn_pv(_ptr(p.codes), _ptr(p.flags), _ptr(p.scales), _ptr(vt.codes),
+                        _ptr(vt.flags), _ptr(vt.scales), vt.M, vt_row0, p.M, p.K, d, p.lzs_group,
+                        _ptr(out), out.stride(0), _ptr(workspace), nbytes, _stream_handle(stream))
+    _check(st, "quartz_attn_pv")
+    return out
+
+
+def attention_workspace(heads: int, L: int, d: int, lzs_group: int, device):
+    """Zero-filled workspace of lzs_attention."""
+    torch = _torch()
+    nbytes = quartz_lzs_attention_workspace_bytes(heads, L, d, lzs_group)
+    if nbytes == 0:
+        raise ValueError("unsupported attention shape")
+    return torch.zeros((nbytes,), dtype=torch.uint8, device=device)
+
+
+def lzs_attention(q, k, v, heads: int, lzs_group: int = 16, out=None, workspace=None, stream=None):
+    """LZS attention of all heads (quartz_lzs_attention): q, k, v bf16
+    [heads * L, d] contiguous (head-major); returns bf16 [L, heads * d]."""
+    torch = _torch()
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or t.dim() != 2 or not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous bf16 [heads * L, d] tensors")
+    L, d = q.shape[0] // heads, q.shape[1]
+    if out is None:
+        out = torch.empty((L, heads * d), dtype=torch.bfloat16, device=q.device)
+    if workspace is None:
+        workspace = attention_workspace(heads, L, d, lzs_group, q.device)
+    st = quartz_lzs_attention(_ptr(q), _ptr(k), _ptr(v), heads, L, d, lzs_group, _ptr(out),
+                              out.stride(0), _ptr(workspace),
+                              workspace.numel() * workspace.element_size(),
+                              _stream_handle(stream))
+    _check(st, "quartz_lzs_attention")
     return out

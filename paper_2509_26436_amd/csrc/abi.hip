@@ -471,6 +471,234 @@ quartz_status quartz_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                                  N, K, lzs_group, stream));
 }
 
+// ------------------------------------------------------------ LZS attention
+
+static bool attn_dims_ok(int64_t L, int64_t d)
+{
+    return L > 0 && d > 0 && L % 64 == 0 && d % 64 == 0 && L <= kMaxK && d <= kMaxK;
+}
+
+quartz_status quartz_quantize_vt(const void* v_bf16, int64_t heads, int64_t L, int64_t d,
+                                 int64_t ldv, int32_t lzs_group, uint8_t* codes, uint8_t* flags,
+                                 uint16_t* scales, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (heads < 0 || !attn_dims_ok(L, d) || ldv < d || ldv > kMaxLd ||
+        !size_ok(heads * d, L) || (heads > 0 && L > kMaxRowGroups / heads))
+        return QUARTZ_ERR_SHAPE;
+    if (ldv % 8 != 0)
+        return QUARTZ_ERR_ALIGN;
+    if (heads == 0)
+        return QUARTZ_OK;
+    if (!v_bf16 || !codes || !flags || !scales)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(v_bf16) || !aligned16(codes) || !aligned16(flags) || !aligned16(scales))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_quantize_vt(static_cast<const uint16_t*>(v_bf16), heads, L, d,
+                                               ldv, lzs_group, codes, flags, scales, stream));
+}
+
+quartz_status quartz_softmax_quantize(const float* s, int64_t M, int64_t N, int64_t lds,
+                                      int32_t lzs_group, uint8_t* codes, uint8_t* flags,
+                                      uint16_t* scales, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (M < 0 || N <= 0 || N % 64 != 0 || !size_ok(M, N) || lds < N || lds > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (lds % 4 != 0)
+        return QUARTZ_ERR_ALIGN;
+    if (M == 0)
+        return QUARTZ_OK;
+    if (!s || !codes || !flags || !scales)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(s) || !aligned16(codes) || !aligned16(flags) || !aligned16(scales))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_softmax_quantize(s, M, N, lds, lzs_group, codes, flags, scales,
+                                                    stream));
+}
+
+// rows [row0, row0 + n) of planes of `plane` rows
+static bool rows_ok(int64_t plane, int64_t row0, int64_t n)
+{
+    return plane > 0 && row0 >= 0 && n >= 0 && row0 <= plane - n && plane <= kMaxRowGroups;
+}
+
+quartz_status quartz_attn_scores(const uint8_t* q_codes, const uint8_t* q_flags,
+                                 const uint16_t* q_scales, int64_t q_plane, int64_t q_row0,
+                                 const uint8_t* k_codes, const uint8_t* k_flags,
+                                 const uint16_t* k_scales, int64_t k_plane, int64_t k_row0,
+                                 int64_t Lq, int64_t Lk, int64_t d, int32_t lzs_group, float scale,
+                                 float* s, int64_t lds, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group) || !std::isfinite(scale))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (Lq < 0 || Lk < 0 || d <= 0 || d % 64 != 0 || d > kMaxK || !rows_ok(q_plane, q_row0, Lq) ||
+        !rows_ok(k_plane, k_row0, Lk) || !size_ok(q_plane, d) || !size_ok(k_plane, d) ||
+        lds < Lk || lds > kMaxLd ||
+        ((Lq + quartz::kGemmBlockRows - 1) / quartz::kGemmBlockRows) *
+                ((Lk + quartz::kGemmBlockCols - 1) / quartz::kGemmBlockCols) > quartz::kMaxGemmTiles)
+        return QUARTZ_ERR_SHAPE;
+    if (Lq == 0 || Lk == 0)
+        return QUARTZ_OK;
+    if (!q_codes || !q_flags || !q_scales || !k_codes || !k_flags || !k_scales || !s)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(q_codes) || !aligned16(q_flags) || !aligned16(q_scales) || !aligned16(k_codes) ||
+        !aligned16(k_flags) || !aligned16(k_scales) || !aligned16(s))
+        return QUARTZ_ERR_ALIGN;
+    return from_hip(quartz::launch_attn_scores(q_codes, q_flags, q_scales, q_plane, q_row0, k_codes,
+                                               k_flags, k_scales, k_plane, k_row0, Lq, Lk, d,
+                                               lzs_group, scale, s, lds, stream));
+}
+
+size_t quartz_attn_pv_workspace_bytes(int64_t Lq, int64_t Lk, int64_t d)
+{
+    if (Lq <= 0 || d <= 0 || Lk <= 0 || Lk % 64 != 0 || !size_ok(Lq, Lk) || !size_ok(d, Lk))
+        return 0;
+    return quartz::gemm_workspace_bytes(
+        quartz::gemm_schedule(Lq, d, Lk, quartz::gemm_resident_blocks(), true));
+}
+
+quartz_status quartz_attn_pv(const uint8_t* p_codes, const uint8_t* p_flags,
+                             const uint16_t* p_scales, const uint8_t* vt_codes,
+                             const uint8_t* vt_flags, const uint16_t* vt_scales, int64_t vt_plane,
+                             int64_t vt_row0, int64_t Lq, int64_t Lk, int64_t d,
+                             int32_t lzs_group, void* o_bf16, int64_t ldo, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (Lq < 0 || d <= 0 || Lk <= 0 || Lk % 64 != 0 || Lk > kMaxK || !size_ok(Lq, Lk) ||
+        !rows_ok(vt_plane, vt_row0, d) || !size_ok(vt_plane, Lk) || ldo < d || ldo > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (Lq == 0)
+        return QUARTZ_OK;
+    if (!p_codes || !p_flags || !p_scales || !vt_codes || !vt_flags || !vt_scales || !o_bf16)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(p_codes) || !aligned16(p_flags) || !aligned16(p_scales) ||
+        !aligned16(vt_codes) || !aligned16(vt_flags) || !aligned16(vt_scales) ||
+        !aligned16(o_bf16) || (workspace && !aligned16(workspace)))
+        return QUARTZ_ERR_ALIGN;
+    const quartz::GemmSchedule sch =
+        quartz::gemm_schedule(Lq, d, Lk, quartz::gemm_resident_blocks(), workspace != nullptr);
+    if (sch.blocks <= 0)
+        return QUARTZ_ERR_HIP;
+    if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    return from_hip(quartz::launch_attn_pv(p_codes, p_flags, p_scales, vt_codes, vt_flags,
+                                           vt_scales, vt_plane, vt_row0, Lq, Lk, d, lzs_group,
+                                           static_cast<uint16_t*>(o_bf16), ldo, sch, workspace,
+                                           stream));
+}
+
+// Workspace of quartz_lzs_attention, in order: the PV split workspace (must
+// start zero-filled; every call leaves it so), Q, K and V^T codes / flags /
+// scales of all heads, the scores of one head, its quantized softmax output.
+namespace {
+struct AttnLayout {
+    size_t split, qc, qf, qs, kc, kf, ks, vc, vf, vs, s, pc, pf, ps, total;
+};
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+AttnLayout attn_layout(int64_t heads, int64_t L, int64_t d, int32_t gs)
+{
+    AttnLayout w{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align256(bytes);
+        return at;
+    };
+    const size_t rows = (size_t)(heads * L);
+    const size_t vrows = (size_t)(heads * d);
+    w.split = take(quartz::gemm_workspace_bytes(
+        quartz::gemm_schedule(L, d, L, quartz::gemm_resident_blocks(), true)));
+    w.qc = take(rows * (size_t)d / 2);
+    w.qf = take(rows * (size_t)d / (size_t)gs);
+    w.qs = take(rows * (size_t)d / 64 * 2);
+    w.kc = take(rows * (size_t)d / 2);
+    w.kf = take(rows * (size_t)d / (size_t)gs);
+    w.ks = take(rows * (size_t)d / 64 * 2);
+    w.vc = take(vrows * (size_t)L / 2);
+    w.vf = take(vrows * (size_t)L / (size_t)gs);
+    w.vs = take(vrows * (size_t)L / 64 * 2);
+    w.s = take((size_t)L * (size_t)L * 4);
+    w.pc = take((size_t)L * (size_t)L / 2);
+    w.pf = take((size_t)L * (size_t)L / (size_t)gs);
+    w.ps = take((size_t)L * (size_t)L / 64 * 2);
+    w.total = off;
+    return w;
+}
+}  // namespace
+
+static bool attention_shape_ok(int64_t heads, int64_t L, int64_t d)
+{
+    return heads >= 0 && attn_dims_ok(L, d) && L <= (int64_t(1) << 16) &&
+           (heads == 0 || (heads <= kMaxRowGroups / L && size_ok(heads * L, d) &&
+                           size_ok(heads * d, L)));
+}
+
+size_t quartz_lzs_attention_workspace_bytes(int64_t heads, int64_t L, int64_t d,
+                                            int32_t lzs_group)
+{
+    if (!lzs_ok(lzs_group) || heads <= 0 || !attention_shape_ok(heads, L, d))
+        return 0;
+    return attn_layout(heads, L, d, lzs_group).total;
+}
+
+quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const void* v_bf16,
+                                   int64_t heads, int64_t L, int64_t d, int32_t lzs_group,
+                                   void* o_bf16, int64_t ldo, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream)
+{
+    if (!lzs_ok(lzs_group))
+        return QUARTZ_ERR_UNSUPPORTED;
+    if (!attention_shape_ok(heads, L, d) || ldo < heads * d || ldo > kMaxLd)
+        return QUARTZ_ERR_SHAPE;
+    if (heads == 0)
+        return QUARTZ_OK;
+    if (!q_bf16 || !k_bf16 || !v_bf16 || !o_bf16 || !workspace)
+        return QUARTZ_ERR_NULL;
+    if (!aligned16(q_bf16) || !aligned16(k_bf16) || !aligned16(v_bf16) || !aligned16(o_bf16) ||
+        !aligned16(workspace))
+        return QUARTZ_ERR_ALIGN;
+    const AttnLayout w = attn_layout(heads, L, d, lzs_group);
+    if (w.total > workspace_bytes)
+        return QUARTZ_ERR_WORKSPACE;
+    uint8_t* base = static_cast<uint8_t*>(workspace);
+    auto u8 = [&](size_t off) { return base + off; };
+    auto u16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+    const int64_t rows = heads * L;
+    hipError_t e = quartz::launch_quantize_act(static_cast<const uint16_t*>(q_bf16), rows, d, d,
+                                               lzs_group, u8(w.qc), u8(w.qf), u16(w.qs), nullptr,
+                                               false, stream);
+    if (e == hipSuccess)
+        e = quartz::launch_quantize_act(static_cast<const uint16_t*>(k_bf16), rows, d, d,
+                                        lzs_group, u8(w.kc), u8(w.kf), u16(w.ks), nullptr, false,
+                                        stream);
+    if (e == hipSuccess)
+        e = quartz::launch_quantize_vt(static_cast<const uint16_t*>(v_bf16), heads, L, d, d,
+                                       lzs_group, u8(w.vc), u8(w.vf), u16(w.vs), stream);
+    const quartz::GemmSchedule pv =
+        quartz::gemm_schedule(L, d, L, quartz::gemm_resident_blocks(), true);
+    const float scale = (float)(1.0 / std::sqrt((double)d));
+    float* S = reinterpret_cast<float*>(base + w.s);
+    for (int64_t h = 0; h < heads && e == hipSuccess; ++h) {
+        e = quartz::launch_attn_scores(u8(w.qc), u8(w.qf), u16(w.qs), rows, h * L, u8(w.kc),
+                                       u8(w.kf), u16(w.ks), rows, h * L, L, L, d, lzs_group,
+                                       scale, S, L, stream);
+        if (e == hipSuccess)
+            e = quartz::launch_softmax_quantize(S, L, L, L, lzs_group, u8(w.pc), u8(w.pf),
+                                                u16(w.ps), stream);
+        if (e == hipSuccess)
+            e = quartz::launch_attn_pv(u8(w.pc), u8(w.pf), u16(w.ps), u8(w.vc), u8(w.vf),
+                                       u16(w.vs), heads * d, h * d, L, L, d, lzs_group,
+                                       static_cast<uint16_t*>(o_bf16) + h * d, ldo, pv,
+                                       u8(w.split), stream);
+    }
+    return from_hip(e);
+}
+
 static quartz_status conv_impl(const uint8_t* codes, const uint8_t* flags,
                                const uint16_t* scales, float act_scale, bool is_static,
                                const void* w_packed, const void* bias_bf16, void* y_bf16,

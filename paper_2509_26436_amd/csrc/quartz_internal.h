@@ -95,6 +95,20 @@ struct ConvGeom {
     uint32_t div_magic;
 };
 
+// The two products of LZS attention (ATTN kernels): B is an LZS-quantized
+// activation, b_codes [G][b_plane][32], b_flags [G][b_plane][64/G_s],
+// b_scales [G][b_plane] with the GEMM's rows n at plane row b_row0 + n; A's
+// rows m are plane row a_row0 + m of planes of a_plane rows.  y32 and scale:
+// the fp32 output of the scores (y32[m][ldy] = acc * scale), else unused.
+struct AttnGeom {
+    const uint8_t* b_codes;
+    const uint8_t* b_flags;
+    const uint16_t* b_scales;
+    int64_t a_plane, a_row0, b_plane, b_row0;
+    float* y32;
+    float scale;
+};
+
 // Arguments of one GEMM launch (see the kernel template in w4a4_gemm_kernel.h).
 struct GemmLaunch {
     const uint8_t* codes;
@@ -115,6 +129,7 @@ struct GemmLaunch {
     const int8_t* zeros;      // asymmetric mode only
     const int16_t* wsums;
     ConvGeom conv;            // implicit 3 x 3 convolution only
+    AttnGeom attn;            // attention products only
 };
 
 // One output mode each (w4a4_gemm_<mode>.hip).
@@ -125,6 +140,8 @@ hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv_static(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_attn_scores(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_gemm_attn_pv(const GemmLaunch& a, hipStream_t stream);
 
 // 3 x 3 convolution (stride 1, padding 1) as an implicit GEMM: codes, flags
 // and scales of quartz_quantize_act for the feature map [images * H * W][C]
@@ -175,6 +192,29 @@ hipError_t launch_pack_weight_per_channel(const uint16_t* w, int64_t N, int64_t 
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream);
+
+// LZS attention (attention.hip): V^T quantized along the keys from V
+// [heads * L][ldv] (rows head * L + key) into codes [L/64][heads * d][32],
+// flags [L/64][heads * d][64/G_s], scales [L/64][heads * d]; the row softmax of
+// S [M][lds] (N columns) quantized into codes [N/64][M][32] ...; and the two
+// products of one head (scores: fp32 s[Lq][lds] = scale * Q~ K~^T; PV: bf16
+// o[Lq][ldo] = P~ V~, with a split workspace as for the linear layer).
+hipError_t launch_quantize_vt(const uint16_t* v, int64_t heads, int64_t L, int64_t d, int64_t ldv,
+                              int lzs_group, uint8_t* codes, uint8_t* flags, uint16_t* scales,
+                              hipStream_t stream);
+hipError_t launch_softmax_quantize(const float* S, int64_t M, int64_t N, int64_t lds, int lzs_group,
+                                   uint8_t* codes, uint8_t* flags, uint16_t* scales,
+                                   hipStream_t stream);
+hipError_t launch_attn_scores(const uint8_t* qc, const uint8_t* qf, const uint16_t* qs,
+                              int64_t q_plane, int64_t q_row0, const uint8_t* kc,
+                              const uint8_t* kf, const uint16_t* ks, int64_t k_plane,
+                              int64_t k_row0, int64_t Lq, int64_t Lk, int64_t d, int lzs_group,
+                              float scale, float* s, int64_t lds, hipStream_t stream);
+hipError_t launch_attn_pv(const uint8_t* pc, const uint8_t* pf, const uint16_t* ps,
+                          const uint8_t* vc, const uint8_t* vf, const uint16_t* vs,
+                          int64_t v_plane, int64_t v_row0, int64_t Lq, int64_t Lk, int64_t d,
+                          int lzs_group, uint16_t* o, int64_t ldo, const GemmSchedule& sch,
+                          void* workspace, hipStream_t stream);
 
 // ------------------------------------------------------------ device helpers
 

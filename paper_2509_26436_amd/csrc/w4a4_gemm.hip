@@ -147,6 +147,36 @@ hipError_t launch_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,
     return scales ? launch_gemm_conv(a, stream) : launch_gemm_conv_static(a, stream);
 }
 
+hipError_t launch_attn_scores(const uint8_t* qc, const uint8_t* qf, const uint16_t* qs,
+                              int64_t q_plane, int64_t q_row0, const uint8_t* kc,
+                              const uint8_t* kf, const uint16_t* ks, int64_t k_plane,
+                              int64_t k_row0, int64_t Lq, int64_t Lk, int64_t d, int lzs_group,
+                              float scale, float* s, int64_t lds, hipStream_t stream)
+{
+    const GemmSchedule sch = gemm_schedule(Lq, Lk, d, gemm_resident_blocks(), false);
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    GemmLaunch a{qc, qf, qs, nullptr, nullptr, nullptr, nullptr, Lq, Lk, d, lds, lzs_group, 0,
+                 sch, nullptr, nullptr, QuantOut{}, 0.0f};
+    a.attn = AttnGeom{kc, kf, ks, q_plane, q_row0, k_plane, k_row0, s, scale};
+    return launch_gemm_attn_scores(a, stream);
+}
+
+hipError_t launch_attn_pv(const uint8_t* pc, const uint8_t* pf, const uint16_t* ps,
+                          const uint8_t* vc, const uint8_t* vf, const uint16_t* vs,
+                          int64_t v_plane, int64_t v_row0, int64_t Lq, int64_t Lk, int64_t d,
+                          int lzs_group, uint16_t* o, int64_t ldo, const GemmSchedule& sch,
+                          void* workspace, hipStream_t stream)
+{
+    if (sch.blocks <= 0)
+        return hipErrorInvalidConfiguration;
+    GemmLaunch a{pc, pf, ps, nullptr, nullptr, o, nullptr, Lq, d, Lk, ldo, lzs_group, 0,
+                 sch, nullptr, nullptr, QuantOut{}, 0.0f};
+    a.attn = AttnGeom{vc, vf, vs, Lq, 0, v_plane, v_row0, nullptr, 0.0f};
+    split_workspace(sch, workspace, a.counters, a.slots);
+    return launch_gemm_attn_pv(a, stream);
+}
+
 hipError_t launch_w4a4_gemm_i32(const uint8_t* codes, const uint8_t* flags,
                                 const uint8_t* w_packed, int32_t* acc, int64_t M, int64_t N,
                                 int64_t K, int lzs_group, hipStream_t stream)

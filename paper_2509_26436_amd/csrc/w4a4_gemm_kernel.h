@@ -153,6 +153,23 @@ __device__ __forceinline__ Fp8Table fp8_table_raw(uint32_t lo, uint32_t hi)
     return t;
 }
 
+// ATTN: the flags of half h of a B row (one activation row of 64 / G_s flag
+// bytes): its first 32 elements are flags [0, 32 / G_s), the second half the
+// rest (G_s = 64: the row's single flag covers both halves).  Returned in the
+// low bytes of a dword, flag k of the half in byte k.
+template <int GS>
+__device__ __forceinline__ uint32_t load_half_flags(Rsrc r, uint32_t row_off, int h)
+{
+    if constexpr (GS == 8)
+        return __builtin_amdgcn_raw_buffer_load_b32(r, (int)(row_off + 4u * (uint32_t)h), 0, 0);
+    else if constexpr (GS == 16)
+        return __builtin_amdgcn_raw_buffer_load_b16(r, (int)(row_off + 2u * (uint32_t)h), 0, 0);
+    else if constexpr (GS == 32)
+        return __builtin_amdgcn_raw_buffer_load_b8(r, (int)(row_off + (uint32_t)h), 0, 0);
+    else
+        return __builtin_amdgcn_raw_buffer_load_b8(r, (int)row_off, 0, 0);
+}
+
 template <int GS>
 __device__ __forceinline__ uint2 flags_dwords(FlagRaw<GS> raw)
 {
@@ -198,15 +215,22 @@ typedef __attribute__((address_space(3))) v4u lds_v4u;
 // tap falls outside the image.  Every 64-group of an im2col row lies within
 // one tap (C % 64 == 0), and a group's codes, FLAGs and scale depend on its
 // 64 values only, so these are exactly the codes of the im2col matrix.
+// ATTN instantiations are the two products of LZS attention: the B operand
+// is itself an LZS-quantized activation (codes, FLAGs and fp16 scales in the
+// quantizer's K-group-major layout, AttnGeom), decoded with its own FLAG
+// tables like A, and A and B address one head's rows inside the arrays of
+// all heads (plane stride and row offset).  With OUT32 the output is fp32,
+// y32 = acc * scale (the scores); otherwise the bf16 output of the layer.
 template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC, bool ASYM,
-          bool CONV = false>
+          bool CONV = false, bool ATTN = false, bool OUT32 = false>
 __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
     uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout, float act_scale,
-    const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums, ConvGeom conv)
+    const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums, ConvGeom conv,
+    AttnGeom attn)
 {
     // per-group scales are staged and applied only by the per-group kernels
     constexpr bool kGroupScales = !I32OUT && !STATIC;
@@ -317,6 +341,7 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
             uint4 a0, a1;
             uint4 b;
             FlagRaw<GS> f;
+            uint32_t fb;             // ATTN: flags of this thread's half B row
             uint16_t sa, sw;
             uint16_t zh, wh;         // ASYM: fp16 bits of -z and of W
         };
@@ -345,12 +370,18 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 lrow = (uint32_t)((int)m0 + dr + dh * conv.W + dw);
                 in = (uint32_t)(conv_h + dh) < (uint32_t)conv.H && (uint32_t)(conv_w + dw) < (uint32_t)conv.W;
             }
-            const int64_t prow = plane * M + row0;
+            const int64_t prow = ATTN ? plane * attn.a_plane + attn.a_row0 + row0 : plane * M + row0;
             const Rsrc ra = make_rsrc(codes + prow * 32, range_rows * 32u);
             const Rsrc rf = make_rsrc(flags + prow * FB, range_rows * (uint32_t)FB);
             const uint32_t ao = in ? lrow * 32u + (uint32_t)(ah * 16) : 0x80000000u;
             const uint32_t fo = in ? lrow * (uint32_t)FB : 0x80000000u;
-            const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
+            // ATTN: B rows n0 .. n0 + BN - 1 of group g's plane of the B
+            // activation arrays (bh_rows of them inside N)
+            const int64_t n0 = panel0 * kPanel;
+            const int64_t bprow = (int64_t)g * attn.b_plane + attn.b_row0 + n0;
+            const uint32_t bh_rows = (uint32_t)min(max(N - n0, (int64_t)0), (int64_t)BN);
+            const Rsrc rb = ATTN ? make_rsrc(attn.b_codes + bprow * 32, bh_rows * 32u)
+                                 : make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
             r.a0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)ao, 0, 0));
             if constexpr (kSplit)
                 r.a1 = make_uint4(0, 0, 0, 0);
@@ -362,15 +393,27 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 const uint2 b2 = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rb, (int)b_off, 0, 0));
                 r.b = make_uint4(b2.x, b2.y, 0, 0);
             } else {
-                r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+                r.b = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    rb, (int)(ATTN ? (uint32_t)(bc * 32 + bh * 16) : b_off), 0, 0));
             }
             if constexpr (kGroupScales) {   // the integer and static paths have none
                 const Rsrc rs = make_rsrc(scales + prow, range_rows * 2u);
                 r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? (int)(lrow * 2u) : (int)0x80000000u, 0, 0);
-                r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
+                if constexpr (ATTN) {
+                    const Rsrc rbs = make_rsrc(attn.b_scales + bprow, bh_rows * 2u);
+                    r.sw = __builtin_amdgcn_raw_buffer_load_b16(rbs, swc * 2, 0, 0);
+                } else {
+                    r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
+                }
             } else {
                 r.sa = 0;
                 r.sw = 0;
+            }
+            if constexpr (ATTN) {
+                const Rsrc rbf = make_rsrc(attn.b_flags + bprow * FB, bh_rows * (uint32_t)FB);
+                r.fb = load_half_flags<GS>(rbf, (uint32_t)(bc * FB), bh);
+            } else {
+                r.fb = 0;
             }
             if constexpr (ASYM) {
                 const Rsrc rz = make_rsrc(zeros + (int64_t)g * M + m0, s_bytes / 2);
@@ -435,10 +478,36 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 *reinterpret_cast<uint4*>(As[buf] + swz(dr, kSplit ? 2 * ah + c : c)) =
                     make_uint4(w[0].x, w[0].y, w[1].x, w[1].y);
             }
+            if constexpr (ATTN) {
+                // the half B row's 4 words with the FLAG tables of its
+                // subgroups (word w: flag w / (G_s / 8) of the half)
+                const uint32_t bw[4] = {r.b.x, r.b.y, r.b.z, r.b.w};
+                uint2 o[4];
+                const Fp8Table t0 = fp8_table_raw<0>(r.fb, 0u);
+                if constexpr (GS == 8) {
+                    o[0] = decode_nibbles_fp8(bw[0], t0);
+                    o[1] = decode_nibbles_fp8(bw[1], fp8_table_raw<1>(r.fb, 0u));
+                    o[2] = decode_nibbles_fp8(bw[2], fp8_table_raw<2>(r.fb, 0u));
+                    o[3] = decode_nibbles_fp8(bw[3], fp8_table_raw<3>(r.fb, 0u));
+                } else if constexpr (GS == 16) {
+                    const Fp8Table t1 = fp8_table_raw<1>(r.fb, 0u);
+                    o[0] = decode_nibbles_fp8(bw[0], t0);
+                    o[1] = decode_nibbles_fp8(bw[1], t0);
+                    o[2] = decode_nibbles_fp8(bw[2], t1);
+                    o[3] = decode_nibbles_fp8(bw[3], t1);
+                } else {
+#pragma unroll
+                    for (int w = 0; w < 4; ++w)
+                        o[w] = decode_nibbles_fp8(bw[w], t0);
+                }
+                *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(o[0].x, o[0].y, o[1].x, o[1].y);
+                *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(o[2].x, o[2].y, o[3].x, o[3].y);
+            }
             const Fp8Table tw{kTabLo, kTabHi};
             const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
             const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
-            if constexpr (kSplit) {
+            if constexpr (ATTN) {
+            } else if constexpr (kSplit) {
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
             } else {
                 const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
@@ -967,6 +1036,24 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     auto store_tile = [&](const v16f (&out)[TM][TN]) {
         if constexpr (QOUT) {
             quantize_out(out);
+        } else if constexpr (OUT32) {
+            // fp32 y32[row][ldy] = acc * scale; lane l holds column l % 32,
+            // so each store instruction writes two rows' 32 consecutive floats
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int64_t col = (int64_t)cur.tn * BN + wn * WN + j * 32 + l32;
+                if (col >= N)
+                    continue;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t row = (int64_t)cur.tm * BM + wm * WM + i * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                        if (row < M)
+                            attn.y32[row * ldy + col] = out[i][j][r] * attn.scale;
+                    }
+                }
+            }
         } else if constexpr (I32OUT) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
@@ -1210,26 +1297,27 @@ template <bool B>
 using bool_c = std::integral_constant<bool, B>;
 
 // Launch of one output mode, every G_s / epilogue / split combination of it.
-template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM, bool CONV = false>
+template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM, bool CONV = false, bool ATTN = false,
+          bool OUT32 = false>
 hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.sch.blocks);
     const dim3 block(STATIC && a.sch.sk_tiles == 0 ? kSplitThreadsPerBlock : kThreadsPerBlock);
     auto go = [&](auto gs, auto gelu, auto split) {
         w4a4_gemm_kernel<decltype(gs)::value, I32OUT, decltype(gelu)::value, decltype(split)::value,
-                         QOUT, STATIC, ASYM, CONV><<<grid, block, 0, stream>>>(
+                         QOUT, STATIC, ASYM, CONV, ATTN, OUT32><<<grid, block, 0, stream>>>(
             a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.yi, a.M, a.N, a.K, a.ldy, a.sch,
-            a.counters, a.slots, a.qout, a.act_scale, a.zeros, a.wsums, a.conv);
+            a.counters, a.slots, a.qout, a.act_scale, a.zeros, a.wsums, a.conv, a.attn);
     };
     auto with_split = [&](auto gs, auto gelu) {
-        if (!I32OUT && a.sch.sk_tiles > 0)
-            go(gs, gelu, bool_c<!I32OUT>());
+        if (!I32OUT && !OUT32 && a.sch.sk_tiles > 0)
+            go(gs, gelu, bool_c<!I32OUT && !OUT32>());
         else
             go(gs, gelu, bool_c<false>());
     };
     auto with_gelu = [&](auto gs) {
-        if (!I32OUT && a.epilogue == 1)
-            with_split(gs, bool_c<!I32OUT>());
+        if (!I32OUT && !ATTN && a.epilogue == 1)
+            with_split(gs, bool_c<!I32OUT && !ATTN>());
         else
             with_split(gs, bool_c<false>());
     };

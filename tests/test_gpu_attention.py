@@ -1,0 +1,280 @@
+"""GPU parity of LZS attention (reading R11) against the oracle, stage by stage
+and end to end, through the C ABI.
+
+  * V^T quantizer: codes, FLAGs and scales bit for bit.
+  * Scores: every fp32 entry within the fp32 accumulation floor of the
+    oracle's float64 value (the oracle's quantized operands are the input).
+  * Softmax + quantization on seeded scores: where floating point decides a
+    code, the GPU's binary32 softmax and the oracle's float64 one can fall on
+    either side of a rounding boundary, so every scale, FLAG and code must be
+    one that some probability within a relative 2^-12 of the oracle's
+    produces (scale, FLAG and code are monotone in it), and almost all of them
+    must equal the oracle's.
+  * PV on the oracle's quantized softmax output and V^T: within the linear
+    layer's output tolerance.
+  * End to end: equal to the composition of the stage entry points bit for
+    bit, and close to the oracle (relative error, and nearly every output
+    within the layer tolerance: the softmax codes may differ as above).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import bf16_bits_to_f64, to_dev_bf16, to_host_u16, y_tolerance
+
+pytestmark = pytest.mark.gpu
+
+EPS = 2.0 ** -12
+
+
+def _q():
+    import paper_2509_26436_amd as q
+    return q
+
+
+def rand_bf16(seed, shape, scale=1.0, outliers=0):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    x = rng.normal(0, scale, shape)
+    if outliers:
+        cols = rng.choice(shape[1], outliers, replace=False)
+        x[:, cols] *= 20.0
+    return W.to_bf16_bits(x)
+
+
+def to_dev(a: oracle.ActQuant):
+    import torch
+    q = _q()
+    M, K = a.c.shape
+    return q.QuantizedAct(codes=torch.from_numpy(a.codes).cuda(),
+                          flags=torch.from_numpy(a.abi_flags).cuda(),
+                          scales=torch.from_numpy(a.abi_scales.view(np.int16)).cuda(),
+                          zeros=None, M=M, K=K, lzs_group=a.lzs_group)
+
+
+def rows_of(a: oracle.ActQuant, r0: int, n: int) -> oracle.ActQuant:
+    return oracle.ActQuant(None, a.c[r0:r0 + n], a.flags[r0:r0 + n], a.scales[r0:r0 + n],
+                           a.zeros[r0:r0 + n], a.lzs_group)
+
+
+def host_act(qa, gs):
+    """A device QuantizedAct back on the host: (c int8 [M][K], flags [M][K/gs], scales u16 [M][K/64])."""
+    G, M, _ = qa.codes.shape
+    c = oracle.unpack_codes(qa.codes.cpu().numpy(), M, G * 64)
+    fl = qa.flags.cpu().numpy().transpose(1, 0, 2).reshape(M, -1)
+    sc = to_host_u16(qa.scales).T.copy()
+    return c, fl, sc
+
+
+@pytest.mark.parametrize("gs", [8, 16, 32, 64])
+@pytest.mark.parametrize("heads,L,d", [(3, 192, 128), (1, 64, 64), (2, 128, 192)])
+def test_quantize_vt_bit_exact(heads, L, d, gs):
+    import torch
+    q = _q()
+    vb = rand_bf16(100 + heads * L + d, (heads * L, d), 1.0, outliers=3)
+    vt = q.quantize_vt(to_dev_bf16(vb), heads, gs)
+    torch.cuda.synchronize()
+    vtb = np.ascontiguousarray(vb.reshape(heads, L, d).transpose(0, 2, 1).reshape(heads * d, L))
+    ref = oracle.quantize_act(vtb, gs)
+    np.testing.assert_array_equal(vt.codes.cpu().numpy(), ref.codes)
+    np.testing.assert_array_equal(vt.flags.cpu().numpy(), ref.abi_flags)
+    np.testing.assert_array_equal(to_host_u16(vt.scales), ref.abi_scales)
+
+
+def _scores_case(heads, L, Lk, d, gs, seed):
+    qb = rand_bf16(seed, (heads * L, d), 1.0, outliers=2)
+    kb = rand_bf16(seed + 1, (heads * Lk, d), 1.0, outliers=2)
+    return oracle.quantize_act(qb, gs), oracle.quantize_act(kb, gs)
+
+
+@pytest.mark.parametrize("gs", [8, 16, 32])
+@pytest.mark.parametrize("L,Lk", [(320, 320), (200, 384), (64, 64)])
+def test_scores_within_fp32_floor(L, Lk, gs):
+    import torch
+    q = _q()
+    heads, d = 2, 128
+    qa, ka = _scores_case(heads, L, Lk, d, gs, 200 + L + Lk)
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    for h in range(heads):
+        S = q.attn_scores(to_dev(qa), to_dev(ka), h * L, h * Lk, L, Lk, scale)
+        torch.cuda.synchronize()
+        S64, A = oracle.attn_scores_f64(rows_of(qa, h * L, L), rows_of(ka, h * Lk, Lk), scale)
+        tol = (4 * (d / 64 + 1) + 2) * 2.0 ** -24 * A + 1e-30
+        err = np.abs(S.cpu().numpy().astype(np.float64) - S64)
+        assert (err <= tol).all(), f"head {h}: worst excess {(err - tol).max():.3e}"
+
+
+def _softmax_ref(S32):
+    from scipy.special import softmax
+    return softmax(S32.astype(np.float64), axis=1)
+
+
+def _check_softmax_codes(S32, qa, gs, min_exact=0.99):
+    """Validity of the GPU's quantized softmax output against the float64
+    softmax of the same fp32 scores (see the module notes)."""
+    M, N = S32.shape
+    G = N // 64
+    P64 = _softmax_ref(S32)
+    c, fl, sc = host_act(qa, gs)
+    ref = oracle.quantize_f32(P64.astype(np.float32), gs)
+    exact = (c == ref.c).mean()
+    assert exact >= min_exact, f"only {exact:.4f} of the codes equal the oracle's"
+    f16 = lambda v: np.float16(v).view(np.uint16).astype(np.int64)
+    for i in range(M):
+        for g in range(G):
+            p = P64[i, 64 * g:64 * g + 64]
+            alpha = p.max()
+            s16 = int(sc[i, g])
+            lo = f16(np.float32(np.float32(alpha * (1 - EPS)) / np.float32(127.0)))
+            hi = f16(np.float32(np.float32(alpha * (1 + EPS)) / np.float32(127.0)))
+            assert lo <= s16 <= hi, (i, g, s16, lo, hi)
+            s = np.float32(np.uint16(s16).view(np.float16))
+            r = np.float32(0.0) if s == 0 else np.float32(np.float32(1.0) / s)
+            qlo = np.minimum(np.rint(np.float32(p * (1 - EPS)).astype(np.float32) * r), 127).astype(np.int64)
+            qhi = np.minimum(np.rint(np.float32(p * (1 + EPS)).astype(np.float32) * r), 127).astype(np.int64)
+            for j in range(64 // gs):
+                sl = slice(j * gs, (j + 1) * gs)
+                f_lo = oracle.lzs_flag(int(np.bitwise_or.reduce(qlo[sl])))
+                f_hi = oracle.lzs_flag(int(np.bitwise_or.reduce(qhi[sl])))
+                f = int(fl[i, g * (64 // gs) + j])
+                assert f_lo <= f <= f_hi, (i, g, j, f, f_lo, f_hi)
+                cc = c[i, 64 * g + j * gs:64 * g + (j + 1) * gs].astype(np.int64)
+                assert ((cc >= (qlo[sl] >> f)) & (cc <= (qhi[sl] >> f))).all(), (i, g, j)
+
+
+def _score_rows(seed, M, N):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    S = rng.normal(0, 3, (M, N))
+    S[0] = 0.5                                   # equal scores
+    S[1, 7] += 40.0                              # one dominant key
+    S[2] = rng.normal(0, 60, N)                  # a peaked row: most groups underflow
+    S[3] = np.linspace(-30, 10, N)               # a smooth ramp across the groups
+    return S.astype(np.float32)
+
+
+@pytest.mark.parametrize("gs", [8, 16, 32, 64])
+def test_softmax_quantize_valid(gs):
+    import torch
+    q = _q()
+    S32 = _score_rows(300 + gs, 70, 448)
+    qa = q.softmax_quantize(torch.from_numpy(S32).cuda(), gs)
+    torch.cuda.synchronize()
+    _check_softmax_codes(S32, qa, gs)
+
+
+def test_softmax_quantize_strided_rows():
+    import torch
+    q = _q()
+    S32 = _score_rows(310, 9, 192)
+    buf = torch.full((9, 256), 1e30, dtype=torch.float32, device="cuda")
+    buf[:, :192] = torch.from_numpy(S32).cuda()
+    qa = q.softmax_quantize(buf[:, :192], 16)
+    torch.cuda.synchronize()
+    _check_softmax_codes(S32, qa, 16)
+
+
+def _pv_case(Lq, Lk, d, heads, gs, seed):
+    S = _score_rows(seed, Lq, Lk).astype(np.float64)
+    pa = oracle.quantize_f32(oracle.softmax_rows(S), gs)
+    vb = rand_bf16(seed + 1, (heads * Lk, d), 1.0, outliers=2)
+    vtb = np.ascontiguousarray(vb.reshape(heads, Lk, d).transpose(0, 2, 1).reshape(heads * d, Lk))
+    return pa, oracle.quantize_act(vtb, gs)
+
+
+@pytest.mark.parametrize("gs", [8, 16, 32])
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("Lq,Lk", [(320, 448), (4608, 576)])
+def test_pv_within_tolerance(Lq, Lk, split, gs):
+    import torch
+    q = _q()
+    heads, d = 2, 128
+    pa, vta = _pv_case(Lq, Lk, d, heads, gs, 400 + Lq + gs)
+    ws = None
+    if split:
+        nbytes = q.quartz_attn_pv_workspace_bytes(Lq, Lk, d)
+        ws = torch.zeros((max(nbytes, 16),), dtype=torch.uint8, device="cuda")
+    out = torch.full((Lq, heads * d), 7.0, dtype=torch.bfloat16, device="cuda")
+    for h in range(heads):
+        q.attn_pv(to_dev(pa), to_dev(vta), h * d, d, out=out[:, h * d:(h + 1) * d], workspace=ws)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, 2, 3, Lq - 1], np.linspace(0, Lq - 1, 40).astype(int)]))
+    for h in range(heads):
+        rr, cc = np.meshgrid(rows, np.arange(d), indexing="ij")
+        O64, A = oracle.attn_pv_f64(pa, rows_of(vta, h * d, d), rr.ravel(), cc.ravel())
+        got = bf16_bits_to_f64(to_host_u16(out[rows.tolist(), h * d:(h + 1) * d].contiguous())).ravel()
+        tol = y_tolerance(O64, A, Lk)
+        err = np.abs(got - O64)
+        assert (err <= tol).all(), f"head {h}: {(err > tol).sum()} outputs out of tolerance"
+
+
+def _staged(q, qb, kb, vb, heads, gs):
+    """The end-to-end output composed from the stage entry points."""
+    import torch
+    L, d = qb.shape[0] // heads, qb.shape[1]
+    qa = q.quantize_act(to_dev_bf16(qb), gs)
+    ka = q.quantize_act(to_dev_bf16(kb), gs)
+    vt = q.quantize_vt(to_dev_bf16(vb), heads, gs)
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    nbytes = q.quartz_attn_pv_workspace_bytes(L, L, d)
+    ws = torch.zeros((max(nbytes, 16),), dtype=torch.uint8, device="cuda")
+    out = torch.empty((L, heads * d), dtype=torch.bfloat16, device="cuda")
+    for h in range(heads):
+        S = q.attn_scores(qa, ka, h * L, h * L, L, L, scale)
+        pa = q.softmax_quantize(S, gs)
+        q.attn_pv(pa, vt, h * d, d, out=out[:, h * d:(h + 1) * d], workspace=ws)
+    return out
+
+
+def _compare_head(O_gpu, O64, A, L):
+    err = np.abs(O_gpu - O64)
+    rel = np.linalg.norm(O_gpu - O64) / np.linalg.norm(O64)
+    within = (err <= y_tolerance(O64, A, L)).mean()
+    assert rel <= 2e-3, f"relative error {rel:.2e}"
+    assert within >= 0.99, f"only {within:.4f} of the outputs within the layer tolerance"
+
+
+@pytest.mark.parametrize("gs", [8, 16, 32])
+def test_attention_end_to_end(gs):
+    import torch
+    q = _q()
+    heads, L, d = 3, 256, 128
+    qb = rand_bf16(500 + gs, (heads * L, d), 1.0, outliers=2)
+    kb = rand_bf16(501 + gs, (heads * L, d), 1.0, outliers=2)
+    vb = rand_bf16(502 + gs, (heads * L, d), 1.0, outliers=2)
+    O = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
+    O2 = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
+    ref = _staged(q, qb, kb, vb, heads, gs)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_host_u16(O), to_host_u16(ref))
+    np.testing.assert_array_equal(to_host_u16(O2), to_host_u16(O))
+    Og = bf16_bits_to_f64(to_host_u16(O))
+    for h in range(heads):
+        O64, parts = oracle.lzs_attention_f64(qb[h * L:(h + 1) * L], kb[h * L:(h + 1) * L],
+                                              vb[h * L:(h + 1) * L], gs)
+        _compare_head(Og[:, h * d:(h + 1) * d], O64, parts["A"], L)
+
+
+def test_attention_full_size_sampled():
+    """Two heads at the FLUX sequence length (4096 image + 512 text tokens),
+    d = 128, G_s = 16; sampled query rows recomputed by the oracle."""
+    import torch
+    q = _q()
+    heads, L, d, gs = 2, 4608, 128, 16
+    qb = rand_bf16(600, (heads * L, d), 1.0, outliers=2)
+    kb = rand_bf16(601, (heads * L, d), 1.0, outliers=2)
+    vb = rand_bf16(602, (heads * L, d), 1.0, outliers=2)
+    O = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
+    torch.cuda.synchronize()
+    Og = bf16_bits_to_f64(to_host_u16(O))
+    rows = np.unique(np.concatenate([[0, 255, 256, L - 1], np.linspace(0, L - 1, 20).astype(int)]))
+    scale = 1.0 / np.sqrt(d)
+    for h in range(heads):
+        sl = slice(h * L, (h + 1) * L)
+        qa = oracle.quantize_act(qb[sl][rows], gs)
+        ka = oracle.quantize_act(kb[sl], gs)
+        vta = oracle.quantize_act(np.ascontiguousarray(vb[sl].T), gs)
+        rr, cc = np.meshgrid(np.arange(rows.size), np.arange(L), indexing="ij")
+        S, _ = oracle.attn_scores_f64(qa, ka, scale, rr.ravel(), cc.ravel())
+        pa = oracle.quantize_f32(oracle.softmax_rows(S.reshape(rows.size, L)), gs)
+        O64, A = oracle.attn_pv_f64(pa, vta)
+        _compare_head(Og[rows, h * d:(h + 1) * d], O64, A, L)
