@@ -67,6 +67,8 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=1536,
                     help="rows per layer in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-attention", action="store_true",
+                    help="skip the LZS attention settings of Table 8")
     ap.add_argument("--no-batched-mlp", action="store_true",
                     help="skip the batched FLUX MLP pipeline measurement (M = 18432)")
     ap.add_argument("--no-ldm", action="store_true",
@@ -401,6 +403,84 @@ def cold_layers(q, torch, np, cfg, dev_in, outs, workspaces, gs, reps=20):
     return {"flush": "512 MiB device write before each timed launch", "per_layer": res}
 
 
+ATTN_L = 4608                  # FLUX.1 joint sequence: 4096 image + 512 text tokens
+ATTN_D = 128
+ATTN_SETTINGS = [(h, gs) for h in (32, 40, 64) for gs in (8, 16, 32)]   # Table 8
+
+
+def attention_bench(q, torch, np, reps=10):
+    """LZS attention (quartz_lzs_attention) in the settings of Table 8:
+    heads x dim 32 x 128, 40 x 128, 64 x 128 at G_s = 8, 16, 32, each at the
+    FLUX sequence length L = 4608 (the table does not give one), seeded
+    normal q, k, v.  Per setting the whole call (timed_chain); ops are the two
+    products, 4 heads L^2 d.  Then the stages of one setting (32 heads,
+    G_s = 16) launched one by one: the Q / K / V^T quantizers over all heads
+    and the scores, softmax + quantize and PV of one head, with their
+    algorithmic bytes (HBM-bound stages) or ops (products)."""
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    L, d = ATTN_L, ATTN_D
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2509)
+    hmax = max(h for h, _ in ATTN_SETTINGS)
+    qkv = [torch.randn((hmax * L, d), generator=gen, device=dev).to(torch.bfloat16) for _ in range(3)]
+    out = torch.empty((L, hmax * d), dtype=torch.bfloat16, device=dev)
+    res = []
+    for heads, gs in ATTN_SETTINGS:
+        qh, kh, vh = (t[: heads * L] for t in qkv)
+        ws = q.attention_workspace(heads, L, d, gs, dev)
+        o = out[:, : heads * d]
+        t = timed_chain(torch, np, stream,
+                        [lambda: q.lzs_attention(qh, kh, vh, heads, gs, out=o, workspace=ws)], reps)[0]
+        ops = 4.0 * heads * L * L * d
+        res.append({"heads": heads, "dim": d, "lzs_group": gs, "L": L, "ms": round(t / 1e3, 4),
+                    "tflops": round(ops / (t * 1e6), 1),
+                    "frac": round(ops / (t * 1e6) / PEAK_FP8_TFLOPS, 4)})
+        del ws
+    # stages of the 32-head, G_s = 16 setting
+    heads, gs = 32, 16
+    qh, kh, vh = (t[: heads * L] for t in qkv)
+    qa = q.quantize_act(qh, gs)
+    ka = q.quantize_act(kh, gs)
+    vt = q.quantize_vt(vh, heads, gs)
+    S = torch.empty((L, L), dtype=torch.float32, device=dev)
+    pa = q.softmax_quantize(S.zero_(), gs)
+    pv_ws = torch.zeros((max(q.quartz_attn_pv_workspace_bytes(L, L, d), 16),), dtype=torch.uint8,
+                        device=dev)
+    o = out[:, :d]
+    scale = float(np.float32(1.0 / np.sqrt(d)))
+    calls = [lambda: q.quantize_act(qh, gs, out=qa), lambda: q.quantize_act(kh, gs, out=ka),
+             lambda: q.quantize_vt(vh, heads, gs),
+             lambda: q.attn_scores(qa, ka, 0, 0, L, L, scale, out=S),
+             lambda: q.softmax_quantize(S, gs, out=pa),
+             lambda: q.attn_pv(pa, vt, 0, d, out=o, workspace=pv_ws)]
+    t = timed_chain(torch, np, stream, calls, reps)
+    act = lambda rows, k: rows * k * (0.5 + 1.0 / gs + 2.0 / 64)     # LZS codes + FLAGs + scales
+    qbytes = heads * L * d * 2 + act(heads * L, d)
+    stages = [
+        {"stage": "quantize Q (all heads)", "us": t[0], "bytes": qbytes},
+        {"stage": "quantize K (all heads)", "us": t[1], "bytes": qbytes},
+        {"stage": "quantize V^T (all heads)", "us": t[2], "bytes": qbytes},
+        {"stage": "scores, one head (fp32 out)", "us": t[3], "ops": 2.0 * L * L * d,
+         "bytes": 2 * act(L, d) + 4.0 * L * L},
+        {"stage": "softmax + quantize, one head", "us": t[4], "bytes": 4.0 * L * L + act(L, L)},
+        {"stage": "PV, one head", "us": t[5], "ops": 2.0 * L * L * d,
+         "bytes": act(L, L) + act(d, L) + 2.0 * L * d},
+    ]
+    for r in stages:
+        r["gbps"] = round(r["bytes"] / (r["us"] * 1e3), 1)
+        if "ops" in r:
+            r["tflops"] = round(r["ops"] / (r["us"] * 1e6), 1)
+        r["us"] = round(float(r["us"]), 2)
+        r["bytes"] = round(r["bytes"])
+    del qkv, out, S, pv_ws
+    return {"workload": f"LZS attention, L = {L}, dim {d}, seeded normal q, k, v",
+            "step": "quartz_lzs_attention: Q, K, V^T quantizers, then per head scores -> "
+                    "softmax + quantize -> PV",
+            "settings": res,
+            "stages_32x128_g16": stages}
+
+
 def gs_sweep(q, torch, np, cfg, dev_in, outs, workspaces, reps=20):
     """The LZS subgroup sweep of Table 1 on the FLUX qkv layer: quantizer and
     GEMM at G_s = 8, 16, 32 and 64 (timed_chain); the paper's numbers are
@@ -666,6 +746,12 @@ def main():
                 others[f"config{c}"] = config_layers(q, W, torch, np, c, gs)
         log(f"configs 1 and 2 measured in {time.time() - t_o:.1f}s")
 
+    attn = None
+    if not args.no_attention:
+        t_at = time.time()
+        attn = attention_bench(q, torch, np)
+        log(f"LZS attention measured in {time.time() - t_at:.1f}s")
+
     mlp = None
     if not args.no_batched_mlp:
         del outs, dev_in, workspaces
@@ -763,6 +849,7 @@ def main():
         "ldm_static": ldm,
         "asymmetric": asym,
         "conv3x3": conv,
+        "attention": attn,
         "cold_cache": cold,
         "lzs_group_sweep": sweep,
         "gpu_clocks": {"after_run": clocks, "during_gemm": load_clocks},

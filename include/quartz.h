@@ -420,13 +420,22 @@ quartz_status quartz_w4a4_conv3x3_static(const uint8_t* codes, const uint8_t* fl
  *
  * quartz_lzs_attention: all heads end to end.
  *   q_bf16, k_bf16, v_bf16   bf16 [heads][L][d], contiguous.
- *   o_bf16   bf16 [L][ldo], ldo >= heads * d: head h in columns h d .. h d + d - 1.
+ *   o_bf16   bf16 [L][ldo], ldo >= heads * d, ldo % 4 == 0: head h in
+ *            columns h d .. h d + d - 1; nothing else of o is written.
  *   workspace  quartz_lzs_attention_workspace_bytes(heads, L, d, lzs_group)
- *              bytes, zero-filled before its first use (every call leaves its
- *              first part zero again); it holds the quantized Q, K, V^T of all
- *              heads and one head's fp32 scores and quantized softmax output.
- *   L % 64 == 0 (L <= 2^16), d % 64 == 0.  The heads run one after another on
- *   `stream`; calls that share a workspace must not overlap.
+ *              bytes.  It holds the quantized Q, K, V^T of all heads and:
+ *              for d = 64 and 128, the same expanded to fp8 e4m3 for the fused
+ *              kernel (two sweeps over the keys per query row, the first for
+ *              the row's max and sum, the second for P, its quantization and
+ *              the PV product; S never leaves registers); for other d, one
+ *              head's fp32 scores and quantized softmax output of the stage
+ *              pipeline above, run head by head, and the PV split workspace,
+ *              which must be zero-filled before its first use (every call
+ *              leaves it zero again).
+ *   L % 64 == 0 (L <= 2^16), d % 64 == 0.  Both paths compute the quantities
+ *   defined above; they differ only in fp32 rounding (the fused kernel's
+ *   exponentials are base-2 hardware exponentials of x log2(e) / sqrt(d)).
+ *   Calls that share a workspace must not overlap.
  * Errors as for the other entry points; lzs_group must be 8, 16, 32 or 64.
  */
 quartz_status quartz_quantize_vt(const void* v_bf16, int64_t heads, int64_t L, int64_t d,

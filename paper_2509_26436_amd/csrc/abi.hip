@@ -592,14 +592,18 @@ quartz_status quartz_attn_pv(const uint8_t* p_codes, const uint8_t* p_flags,
                                            stream));
 }
 
-// Workspace of quartz_lzs_attention, in order: the PV split workspace (must
-// start zero-filled; every call leaves it so), Q, K and V^T codes / flags /
-// scales of all heads, the scores of one head, its quantized softmax output.
+// Workspace of quartz_lzs_attention.  Head dimensions 64 and 128 (the fused
+// kernel): Q, K and V^T codes / flags / scales of all heads, then the three
+// expanded to fp8 e4m3.  Other d (the unfused pipeline), in order: the PV
+// split workspace (must start zero-filled; every call leaves it so), the
+// codes / flags / scales, the scores of one head and its quantized softmax
+// output.
 namespace {
 struct AttnLayout {
-    size_t split, qc, qf, qs, kc, kf, ks, vc, vf, vs, s, pc, pf, ps, total;
+    size_t split, qc, qf, qs, kc, kf, ks, vc, vf, vs, qx, kx, vx, s, pc, pf, ps, total;
 };
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+bool attention_fused(int64_t d) { return d == 64 || d == 128; }
 AttnLayout attn_layout(int64_t heads, int64_t L, int64_t d, int32_t gs)
 {
     AttnLayout w{};
@@ -609,10 +613,12 @@ AttnLayout attn_layout(int64_t heads, int64_t L, int64_t d, int32_t gs)
         off += align256(bytes);
         return at;
     };
+    const bool fused = attention_fused(d);
     const size_t rows = (size_t)(heads * L);
     const size_t vrows = (size_t)(heads * d);
-    w.split = take(quartz::gemm_workspace_bytes(
-        quartz::gemm_schedule(L, d, L, quartz::gemm_resident_blocks(), true)));
+    if (!fused)
+        w.split = take(quartz::gemm_workspace_bytes(
+            quartz::gemm_schedule(L, d, L, quartz::gemm_resident_blocks(), true)));
     w.qc = take(rows * (size_t)d / 2);
     w.qf = take(rows * (size_t)d / (size_t)gs);
     w.qs = take(rows * (size_t)d / 64 * 2);
@@ -622,10 +628,16 @@ AttnLayout attn_layout(int64_t heads, int64_t L, int64_t d, int32_t gs)
     w.vc = take(vrows * (size_t)L / 2);
     w.vf = take(vrows * (size_t)L / (size_t)gs);
     w.vs = take(vrows * (size_t)L / 64 * 2);
-    w.s = take((size_t)L * (size_t)L * 4);
-    w.pc = take((size_t)L * (size_t)L / 2);
-    w.pf = take((size_t)L * (size_t)L / (size_t)gs);
-    w.ps = take((size_t)L * (size_t)L / 64 * 2);
+    if (fused) {
+        w.qx = take(rows * (size_t)d);
+        w.kx = take(rows * (size_t)d);
+        w.vx = take(vrows * (size_t)L);
+    } else {
+        w.s = take((size_t)L * (size_t)L * 4);
+        w.pc = take((size_t)L * (size_t)L / 2);
+        w.pf = take((size_t)L * (size_t)L / (size_t)gs);
+        w.ps = take((size_t)L * (size_t)L / 64 * 2);
+    }
     w.total = off;
     return w;
 }
@@ -660,7 +672,7 @@ quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const
     if (!q_bf16 || !k_bf16 || !v_bf16 || !o_bf16 || !workspace)
         return QUARTZ_ERR_NULL;
     if (!aligned16(q_bf16) || !aligned16(k_bf16) || !aligned16(v_bf16) || !aligned16(o_bf16) ||
-        !aligned16(workspace))
+        !aligned16(workspace) || ldo % 4 != 0)
         return QUARTZ_ERR_ALIGN;
     const AttnLayout w = attn_layout(heads, L, d, lzs_group);
     if (w.total > workspace_bytes)
@@ -679,6 +691,20 @@ quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const
     if (e == hipSuccess)
         e = quartz::launch_quantize_vt(static_cast<const uint16_t*>(v_bf16), heads, L, d, d,
                                        lzs_group, u8(w.vc), u8(w.vf), u16(w.vs), stream);
+    if (attention_fused(d)) {
+        if (e == hipSuccess)
+            e = quartz::launch_expand_fp8(u8(w.qc), u8(w.qf), rows, d, lzs_group, u8(w.qx), stream);
+        if (e == hipSuccess)
+            e = quartz::launch_expand_fp8(u8(w.kc), u8(w.kf), rows, d, lzs_group, u8(w.kx), stream);
+        if (e == hipSuccess)
+            e = quartz::launch_expand_fp8(u8(w.vc), u8(w.vf), heads * d, L, lzs_group, u8(w.vx),
+                                          stream);
+        if (e == hipSuccess)
+            e = quartz::launch_attention_fused(u8(w.qx), u16(w.qs), u8(w.kx), u16(w.ks), u8(w.vx),
+                                               u16(w.vs), heads, L, d, lzs_group,
+                                               static_cast<uint16_t*>(o_bf16), ldo, stream);
+        return from_hip(e);
+    }
     const quartz::GemmSchedule pv =
         quartz::gemm_schedule(L, d, L, quartz::gemm_resident_blocks(), true);
     const float scale = (float)(1.0 / std::sqrt((double)d));

@@ -1,0 +1,355 @@
+// Fused LZS attention (the attention setting of the hardware appendix,
+// Table 8) for head dimensions 64 and 128: the scores never leave registers.
+//
+// Per head, O = softmax(S) V with S = Q~ K~^T / sqrt(d); Q~, K~ quantized per
+// token along d, V~^T per channel along the keys and the binary32 softmax
+// output P per query row in 64-key groups, all by Eq. 1 and Eq. 2, and both
+// products exact per-group integer products with the fp16 group scales
+// applied in fp32 (the same quantities the unfused path materializes).
+//
+// The quantized P of a 64-key group needs the row's final max and sum (its
+// group scale is fp16(max P / 127) of the normalized values), so each query
+// row is swept twice:
+//   pass 1  S of every 64-key chunk, the running max and sum of exp;
+//   pass 2  S again, P = exp(S - max) / sum in binary32, the group scale,
+//           Stage-1 codes, FLAG per subgroup and the truncated LZS values
+//           d = c 2^FLAG, which go straight into the PV matrix product.
+// One wave owns 32 queries of one head and streams every key chunk through
+// registers: no LDS, no barriers.  The operands come from HBM / L2 already
+// decoded to fp8 e4m3 (expand_fp8_kernel: every d = c 2^FLAG is exact in
+// e4m3), since every chunk of K~ and V~^T is read by all L / 32 query waves of
+// its head and decoding it once is cheaper than decoding it L / 32 times.
+//
+// Layout of the score tiles.  The product runs as S^T = K~ Q~^T on
+// v_mfma_f32_32x32x64_f8f6f4 (rows: keys, columns: queries), so lane l holds
+// query l % 32 and 16 keys per 32-key tile.  Row rho of key tile t is fed
+// with key 32 ((rho >> 2) & 1) + 16 t + 4 (rho >> 3) + (rho & 3) of the
+// chunk, which puts keys 32 h + 16 t + r (register r, h = l / 32) in lane l:
+// each half-wave holds 32 consecutive keys of every query, so row maxima,
+// group maxima and the FLAG subgroups (G_s <= 32) are in-lane reductions and
+// a 64-key group takes one exchange between the two half-waves.  The same
+// registers, converted to e4m3 and packed in the byte order the fp8 expansion
+// gives V~^T's keys, are the k-slice of the PV product O^T = V~^T P~^T.
+#include <cmath>
+
+#include "lzs_device.h"
+#include "w4a4_gemm_kernel.h"
+
+namespace quartz {
+
+namespace {
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+// ------------------------------------------------------------ fp8 expansion
+// One (group, row) of a K-group-major LZS activation per thread: its 32 code
+// bytes decoded to 64 e4m3 bytes at out[row][64 g ..] (word w of the group
+// gives bytes 8 w .. 8 w + 7 in the order decode_nibbles_fp8 writes them).
+template <int GS>
+__global__ __launch_bounds__(256) void expand_fp8_kernel(const uint8_t* __restrict__ codes,
+                                                         const uint8_t* __restrict__ flags,
+                                                         int64_t rows, int64_t G,
+                                                         uint8_t* __restrict__ out)
+{
+    constexpr int FB = 64 / GS;
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (t >= rows * G)
+        return;
+    const int64_t g = t / rows, row = t % rows;
+    const uint4 c0 = reinterpret_cast<const uint4*>(codes + t * 32)[0];
+    const uint4 c1 = reinterpret_cast<const uint4*>(codes + t * 32)[1];
+    const uint32_t w[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    FlagRaw<GS> raw;
+    if constexpr (FB == 8)
+        raw = *reinterpret_cast<const uint2*>(flags + t * FB);
+    else if constexpr (FB == 4)
+        raw = *reinterpret_cast<const uint32_t*>(flags + t * FB);
+    else if constexpr (FB == 2)
+        raw = *reinterpret_cast<const uint16_t*>(flags + t * FB);
+    else
+        raw = flags[t];
+    const uint2 f = flags_dwords<GS>(raw);
+    uint32_t o[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        Fp8Table tb;
+        switch (i / (GS / 8)) {
+        case 0: tb = fp8_table_raw<0>(f.x, f.y); break;
+        case 1: tb = fp8_table_raw<1>(f.x, f.y); break;
+        case 2: tb = fp8_table_raw<2>(f.x, f.y); break;
+        case 3: tb = fp8_table_raw<3>(f.x, f.y); break;
+        case 4: tb = fp8_table_raw<4>(f.x, f.y); break;
+        case 5: tb = fp8_table_raw<5>(f.x, f.y); break;
+        case 6: tb = fp8_table_raw<6>(f.x, f.y); break;
+        default: tb = fp8_table_raw<7>(f.x, f.y); break;
+        }
+        const uint2 d = decode_nibbles_fp8(w[i], tb);
+        o[2 * i] = d.x;
+        o[2 * i + 1] = d.y;
+    }
+    uint4* dst = reinterpret_cast<uint4*>(out + row * (64 * G) + 64 * g);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        dst[k] = make_uint4(o[4 * k], o[4 * k + 1], o[4 * k + 2], o[4 * k + 3]);
+}
+
+__device__ __forceinline__ v8i load32(const uint8_t* p)
+{
+    const uint4 a = reinterpret_cast<const uint4*>(p)[0];
+    const uint4 b = reinterpret_cast<const uint4*>(p)[1];
+    return v8i{(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
+}
+
+// operand of the scale outer product (fp16 32x32x16, only k = 0 non-zero):
+// the lower half-wave supplies k = 0 .. 7, the upper one k = 8 .. 15
+__device__ __forceinline__ v8h scale_operand(uint16_t bits, int h)
+{
+    v8h v = {};
+    v[0] = h ? (_Float16)0.0f : __builtin_bit_cast(_Float16, bits);
+    return v;
+}
+
+__device__ __forceinline__ v16f mfma_fp8(const v8i& a, const v8i& b)
+{
+    const v16f zero = {};
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, zero, 0, 0, 0, 0, 0, 0);
+}
+
+__device__ __forceinline__ v16f mfma_outer(const v8h& a, const v8h& b)
+{
+    const v16f zero = {};
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, zero, 0, 0, 0);
+}
+
+__device__ __forceinline__ float xhalf(float v)       // value of lane l ^ 32
+{
+    return __shfl_xor(v, 32, 64);
+}
+
+// One wave: queries q0 .. q0 + 31 of head `head`.  qx / kx: [heads L][64 G]
+// e4m3, qs / ks: [G][heads L] fp16; vx: [heads d][L] e4m3 (V^T), vs:
+// [L / 64][heads d] fp16; o: bf16 [L][ldo], head h at columns h d ...
+template <int GS, int G>
+__global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
+    const uint8_t* __restrict__ qx, const uint16_t* __restrict__ qs,
+    const uint8_t* __restrict__ kx, const uint16_t* __restrict__ ks,
+    const uint8_t* __restrict__ vx, const uint16_t* __restrict__ vs, int64_t heads, int64_t L,
+    float kexp, uint16_t* __restrict__ o, int64_t ldo, int64_t qblocks)
+{
+    constexpr int D = 64 * G;
+    constexpr int TV = D / 32;                 // channel tiles of the PV product
+    // blocks of one head on one XCD (consecutive block ids go round robin
+    // over the 8 XCDs), so its K~ / V~^T chunks are shared in that L2
+    const int64_t total = heads * qblocks;
+    const int64_t bid = blockIdx.x;
+    const int64_t logical = total % 8 == 0 ? (bid % 8) * (total / 8) + bid / 8 : bid;
+    const int64_t head = logical / qblocks;
+    const int64_t q0 = (logical % qblocks) * 128 + (threadIdx.x >> 6) * 32;
+    if (q0 >= L)
+        return;                                  // wave-uniform; no barriers follow
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 31, h = lane >> 5;
+    const int64_t rows = heads * L;
+
+    v8i qop[G];
+    v8h sqop[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        qop[g] = load32(qx + (head * L + q0 + n) * D + 64 * g + 32 * h);
+        sqop[g] = scale_operand(qs[g * rows + head * L + q0 + n], h);
+    }
+    // key of row n of key tile t (within the chunk)
+    const int krow = 32 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+
+    // x (the scores before the 1 / sqrt(d)) of chunk c: x[t][r] belongs to
+    // key 64 c + 32 h + 16 t + r of query q0 + n
+    auto scores = [&](int64_t c, v16f (&x)[2]) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int64_t key = head * L + 64 * c + krow + 16 * t;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const v8i kop = load32(kx + key * D + 64 * g + 32 * h);
+                const v8h skop = scale_operand(ks[g * rows + key], h);
+                const v16f sc = mfma_outer(skop, sqop[g]);
+                const v16f p = mfma_fp8(kop, qop[g]);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    x[t][r] = g == 0 ? p[r] * sc[r] : fmaf(p[r], sc[r], x[t][r]);
+            }
+        }
+    };
+
+    const int64_t chunks = L / 64;
+    // pass 1: per lane the running max and sum of exp over its 32 keys of
+    // every chunk, in the base-2 domain: exp(S - m) = 2^((x - m_x) kexp)
+    float m = -INFINITY, l = 0.0f;
+    for (int64_t c = 0; c < chunks; ++c) {
+        v16f x[2];
+        scores(c, x);
+        float cm = x[0][0];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                cm = fmaxf(cm, x[t][r]);
+        const float mn = fmaxf(m, cm);
+        const float nmk = -mn * kexp;
+        float cs = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                cs += __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk));
+        l = l * __builtin_amdgcn_exp2f((m - mn) * kexp) + cs;
+        m = mn;
+    }
+    {
+        // the two half-waves' keys of the same query (identical result in both)
+        const float mo = xhalf(m), lo = xhalf(l);
+        const float mf = fmaxf(m, mo);
+        l = l * __builtin_amdgcn_exp2f((m - mf) * kexp) + lo * __builtin_amdgcn_exp2f((mo - mf) * kexp);
+        m = mf;
+    }
+    const float inv_l = 1.0f / l;
+    const float nmk = -m * kexp;
+
+    v16f acc[TV];
+#pragma unroll
+    for (int i = 0; i < TV; ++i)
+        acc[i] = v16f{};
+    // pass 2
+    for (int64_t c = 0; c < chunks; ++c) {
+        v16f x[2];
+        scores(c, x);
+        float amax = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                x[t][r] = __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk)) * inv_l;   // P
+                amax = fmaxf(amax, x[t][r]);
+            }
+        const float alpha = fmaxf(amax, xhalf(amax));
+        const _Float16 s16 = (_Float16)(alpha / 127.0f);
+        const uint16_t sbits = __builtin_bit_cast(uint16_t, s16);
+        const float rs = sbits == 0 ? 0.0f : 1.0f / (float)s16;
+        // Stage-1 codes (P >= 0), the max of each subgroup, FLAG, then the
+        // LZS value d = (q >> FLAG) << FLAG as a float
+        float qmax[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // per 8 registers
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                x[t][r] = fminf(__builtin_rintf(x[t][r] * rs), 127.0f);
+                qmax[2 * t + r / 8] = fmaxf(qmax[2 * t + r / 8], x[t][r]);
+            }
+        uint32_t mask[4];
+        if constexpr (GS == 8) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                mask[k] = ~0u << lzs_flag((uint32_t)qmax[k]);
+        } else if constexpr (GS == 16) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+                mask[2 * t] = mask[2 * t + 1] = ~0u << lzs_flag((uint32_t)fmaxf(qmax[2 * t], qmax[2 * t + 1]));
+        } else {
+            float q4 = fmaxf(fmaxf(qmax[0], qmax[1]), fmaxf(qmax[2], qmax[3]));
+            if constexpr (GS == 64)
+                q4 = fmaxf(q4, xhalf(q4));
+            mask[0] = mask[1] = mask[2] = mask[3] = ~0u << lzs_flag((uint32_t)q4);
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                x[t][r] = (float)((uint32_t)x[t][r] & mask[2 * t + r / 8]);
+        // the k-slice of P~^T: dword k of the operand holds keys (relative to
+        // the half-wave) 8 (k / 2) + {0, 4, 1, 5} (k even) or {2, 6, 3, 7}
+        // (k odd), the byte order of the expanded V~^T rows
+        v8i pop;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int t = k >> 2, base = 8 * ((k >> 1) & 1) + 2 * (k & 1);
+            int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[t][base], x[t][base + 4], 0, false);
+            w = __builtin_amdgcn_cvt_pk_fp8_f32(x[t][base + 1], x[t][base + 5], w, true);
+            pop[k] = w;
+        }
+        const v8h spop = scale_operand(sbits, h);
+#pragma unroll
+        for (int i = 0; i < TV; ++i) {
+            const int64_t ch = head * D + 32 * i + n;
+            const v8i vop = load32(vx + ch * L + 64 * c + 32 * h);
+            const v8h svop = scale_operand(vs[c * heads * D + ch], h);
+            const v16f sc = mfma_outer(svop, spop);
+            const v16f p = mfma_fp8(vop, pop);
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][r] = fmaf(p[r], sc[r], acc[i][r]);
+        }
+    }
+    // O^T tile i, register r: channel 32 i + 8 (r / 4) + 4 h + r % 4 of query
+    // q0 + n; four consecutive channels per 8-byte store
+    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    uint16_t* orow = o + (q0 + n) * ldo + head * D;
+#pragma unroll
+    for (int i = 0; i < TV; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const f2 a = {acc[i][4 * j], acc[i][4 * j + 1]};
+            const f2 b = {acc[i][4 * j + 2], acc[i][4 * j + 3]};
+            const uint2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a, bf2)),
+                             __builtin_bit_cast(uint32_t, __builtin_convertvector(b, bf2))};
+            *reinterpret_cast<uint2*>(orow + 32 * i + 8 * j + 4 * h) = v;
+        }
+}
+
+template <int GS>
+hipError_t launch_fused_gs(const uint8_t* qx, const uint16_t* qs, const uint8_t* kx,
+                           const uint16_t* ks, const uint8_t* vx, const uint16_t* vs,
+                           int64_t heads, int64_t L, int64_t d, uint16_t* o, int64_t ldo,
+                           hipStream_t stream)
+{
+    const int64_t qblocks = (L + 127) / 128;
+    const dim3 grid((unsigned)(heads * qblocks)), block(256);
+    const float kexp = (float)(1.4426950408889634 / std::sqrt((double)d));
+    if (d == 64)
+        lzs_attention_fused_kernel<GS, 1><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
+                                                                       kexp, o, ldo, qblocks);
+    else
+        lzs_attention_fused_kernel<GS, 2><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
+                                                                       kexp, o, ldo, qblocks);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_expand_fp8(const uint8_t* codes, const uint8_t* flags, int64_t rows, int64_t K,
+                             int lzs_group, uint8_t* out, hipStream_t stream)
+{
+    const int64_t G = K / 64;
+    const dim3 grid((unsigned)((rows * G + 255) / 256)), block(256);
+    switch (lzs_group) {
+    case 8: expand_fp8_kernel<8><<<grid, block, 0, stream>>>(codes, flags, rows, G, out); break;
+    case 16: expand_fp8_kernel<16><<<grid, block, 0, stream>>>(codes, flags, rows, G, out); break;
+    case 32: expand_fp8_kernel<32><<<grid, block, 0, stream>>>(codes, flags, rows, G, out); break;
+    default: expand_fp8_kernel<64><<<grid, block, 0, stream>>>(codes, flags, rows, G, out); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_fused(const uint8_t* qx, const uint16_t* qs, const uint8_t* kx,
+                                  const uint16_t* ks, const uint8_t* vx, const uint16_t* vs,
+                                  int64_t heads, int64_t L, int64_t d, int lzs_group, uint16_t* o,
+                                  int64_t ldo, hipStream_t stream)
+{
+    switch (lzs_group) {
+    case 8: return launch_fused_gs<8>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
+    case 16: return launch_fused_gs<16>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
+    case 32: return launch_fused_gs<32>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
+    default: return launch_fused_gs<64>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
+    }
+}
+
+}  // namespace quartz

@@ -210,6 +210,14 @@ hipError_t launch_attn_scores(const uint8_t* qc, const uint8_t* qf, const uint16
                               const uint8_t* kf, const uint16_t* ks, int64_t k_plane,
                               int64_t k_row0, int64_t Lq, int64_t Lk, int64_t d, int lzs_group,
                               float scale, float* s, int64_t lds, hipStream_t stream);
+// LZS activation codes K-group-major -> fp8 e4m3 rows out[rows][K]
+hipError_t launch_expand_fp8(const uint8_t* codes, const uint8_t* flags, int64_t rows, int64_t K,
+                             int lzs_group, uint8_t* out, hipStream_t stream);
+// fused LZS attention of all heads (d = 64 or 128) from the expanded operands
+hipError_t launch_attention_fused(const uint8_t* qx, const uint16_t* qs, const uint8_t* kx,
+                                  const uint16_t* ks, const uint8_t* vx, const uint16_t* vs,
+                                  int64_t heads, int64_t L, int64_t d, int lzs_group, uint16_t* o,
+                                  int64_t ldo, hipStream_t stream);
 hipError_t launch_attn_pv(const uint8_t* pc, const uint8_t* pf, const uint16_t* ps,
                           const uint8_t* vc, const uint8_t* vf, const uint16_t* vs,
                           int64_t v_plane, int64_t v_row0, int64_t Lq, int64_t Lk, int64_t d,

@@ -12,9 +12,11 @@ and end to end, through the C ABI.
     must equal the oracle's.
   * PV on the oracle's quantized softmax output and V^T: within the linear
     layer's output tolerance.
-  * End to end: equal to the composition of the stage entry points bit for
-    bit, and close to the oracle (relative error, and nearly every output
-    within the layer tolerance: the softmax codes may differ as above).
+  * End to end (the fused kernel for d = 64 and 128, the stage pipeline
+    otherwise): close to the oracle (relative error, and nearly every output
+    within the layer tolerance: the softmax codes may differ as above); the
+    pipeline also equal to the composition of the stage entry points bit for
+    bit.
 """
 import numpy as np
 import pytest
@@ -233,25 +235,53 @@ def _compare_head(O_gpu, O64, A, L):
     assert within >= 0.99, f"only {within:.4f} of the outputs within the layer tolerance"
 
 
-@pytest.mark.parametrize("gs", [8, 16, 32])
-def test_attention_end_to_end(gs):
+@pytest.mark.parametrize("heads,L,d,gs", [
+    (3, 256, 128, 8), (3, 256, 128, 16), (3, 256, 128, 32), (3, 256, 128, 64),
+    (4, 320, 128, 16),      # a ragged query block (L % 128 = 64); 8 blocks: XCD-grouped order
+    (2, 256, 64, 16), (2, 192, 64, 32),
+    (2, 192, 192, 16),      # d = 192: the unfused pipeline
+])
+def test_attention_end_to_end(heads, L, d, gs):
+    """quartz_lzs_attention against the oracle head by head; for d = 64 and
+    128 it runs the fused kernel, otherwise the unfused pipeline, which must
+    equal the composition of the stage entry points bit for bit.  Either way
+    a second call gives the same bits."""
     import torch
     q = _q()
-    heads, L, d = 3, 256, 128
-    qb = rand_bf16(500 + gs, (heads * L, d), 1.0, outliers=2)
-    kb = rand_bf16(501 + gs, (heads * L, d), 1.0, outliers=2)
-    vb = rand_bf16(502 + gs, (heads * L, d), 1.0, outliers=2)
+    qb = rand_bf16(500 + gs + d, (heads * L, d), 1.0, outliers=2)
+    kb = rand_bf16(501 + gs + d, (heads * L, d), 1.0, outliers=2)
+    vb = rand_bf16(502 + gs + d, (heads * L, d), 1.0, outliers=2)
     O = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
     O2 = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
-    ref = _staged(q, qb, kb, vb, heads, gs)
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(to_host_u16(O), to_host_u16(ref))
     np.testing.assert_array_equal(to_host_u16(O2), to_host_u16(O))
+    if d not in (64, 128):
+        ref = _staged(q, qb, kb, vb, heads, gs)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_host_u16(O), to_host_u16(ref))
     Og = bf16_bits_to_f64(to_host_u16(O))
     for h in range(heads):
         O64, parts = oracle.lzs_attention_f64(qb[h * L:(h + 1) * L], kb[h * L:(h + 1) * L],
                                               vb[h * L:(h + 1) * L], gs)
         _compare_head(Og[:, h * d:(h + 1) * d], O64, parts["A"], L)
+
+
+def test_attention_strided_output_and_guard():
+    """ldo > heads * d: the columns between the heads' outputs and the rows'
+    tails stay untouched (fused path)."""
+    import torch
+    q = _q()
+    heads, L, d, gs = 2, 128, 128, 16
+    qb = rand_bf16(520, (heads * L, d), 1.0)
+    kb = rand_bf16(521, (heads * L, d), 1.0)
+    vb = rand_bf16(522, (heads * L, d), 1.0)
+    ref = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
+    buf = torch.full((L, heads * d + 40), 3.0, dtype=torch.bfloat16, device="cuda")
+    out = buf[:, :heads * d]
+    q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs, out=out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_host_u16(out.contiguous()), to_host_u16(ref))
+    assert (buf[:, heads * d:] == 3.0).all()
 
 
 def test_attention_full_size_sampled():
