@@ -14,6 +14,10 @@
 //   pass 2  S again, P = exp(S - max) / sum in binary32, the group scale,
 //           Stage-1 codes, FLAG per subgroup and the truncated LZS values
 //           d = c 2^FLAG, which go straight into the PV matrix product.
+// The codes are rne(e R) with e = exp(S - max) and R = (1 / sum) (1 / s):
+// one binary32 rounding fewer than rne(P r) with P rounded first, so a code
+// can differ from the unfused path's only where P r lies within an ulp of a
+// rounding boundary.
 // One wave owns 32 queries of one head and streams every key chunk through
 // registers: no LDS, no barriers.  The operands come from HBM / L2 already
 // decoded to fp8 e4m3 (expand_fp8_kernel: every d = c 2^FLAG is exact in
@@ -126,9 +130,29 @@ __device__ __forceinline__ float xhalf(float v)       // value of lane l ^ 32
     return __shfl_xor(v, 32, 64);
 }
 
-// One wave: queries q0 .. q0 + 31 of head `head`.  qx / kx: [heads L][64 G]
-// e4m3, qs / ks: [G][heads L] fp16; vx: [heads d][L] e4m3 (V^T), vs:
-// [L / 64][heads d] fp16; o: bf16 [L][ldo], head h at columns h d ...
+// LDS staging of one 64-key chunk, in the order the MFMA lanes read it, so
+// that every operand read is one conflict-free ds_read_b128 per 16 bytes:
+//   K~   [t][g][j][lane][16 B]: lane (rho, h) of key tile t holds bytes
+//        64 g + 32 h + 16 j .. of key kappa(t, rho) (see krow below);
+//   V~^T [i][j][lane][16 B]: lane (n, h) holds bytes 32 h + 16 j .. of the
+//        chunk's 64 keys of channel 32 i + n;
+//   the key scales [t][g][rho] and the channel scales [D] (fp16).
+template <int G>
+struct AttnStage {
+    static constexpr int D = 64 * G;
+    static constexpr int kK = 64 * D;               // K~ bytes
+    static constexpr int kV = D * 64;               // V~^T bytes
+    static constexpr int kSk = 64 * G * 2;
+    static constexpr int kSv = D * 2;
+    static constexpr int kBytes = kK + kV + kSk + kSv;
+    static constexpr int kKItems = kK / 16 / 256;   // 16-byte pieces per thread
+    static constexpr int kVItems = kV / 16 / 256;
+};
+
+// One block: 4 waves, queries qb * 128 + 32 w .. + 31 of head `head`, which
+// share the staged chunks.  qx / kx: [heads L][64 G] e4m3, qs / ks:
+// [G][heads L] fp16; vx: [heads d][L] e4m3 (V^T), vs: [L / 64][heads d] fp16;
+// o: bf16 [L][ldo], head h at columns h d ...
 template <int GS, int G>
 __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
     const uint8_t* __restrict__ qx, const uint16_t* __restrict__ qs,
@@ -136,43 +160,114 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
     const uint8_t* __restrict__ vx, const uint16_t* __restrict__ vs, int64_t heads, int64_t L,
     float kexp, uint16_t* __restrict__ o, int64_t ldo, int64_t qblocks)
 {
-    constexpr int D = 64 * G;
+    using St = AttnStage<G>;
+    constexpr int D = St::D;
     constexpr int TV = D / 32;                 // channel tiles of the PV product
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2][St::kBytes];
+    // each wave's Q~ operand, [g][j][lane][16 B] (written and read by that wave only)
+    __shared__ __attribute__((aligned(16))) uint8_t qsm[4][G * 2048];
+
     // blocks of one head on one XCD (consecutive block ids go round robin
     // over the 8 XCDs), so its K~ / V~^T chunks are shared in that L2
     const int64_t total = heads * qblocks;
     const int64_t bid = blockIdx.x;
     const int64_t logical = total % 8 == 0 ? (bid % 8) * (total / 8) + bid / 8 : bid;
     const int64_t head = logical / qblocks;
-    const int64_t q0 = (logical % qblocks) * 128 + (threadIdx.x >> 6) * 32;
-    if (q0 >= L)
-        return;                                  // wave-uniform; no barriers follow
-    const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x;
+    const int64_t q0 = (logical % qblocks) * 128 + (tid >> 6) * 32;
+    // a wave past the end of a ragged last block still loads and waits at
+    // the barriers, and computes nothing (wave-uniform)
+    const bool active = q0 < L;
+    const int lane = tid & 63;
     const int n = lane & 31, h = lane >> 5;
     const int64_t rows = heads * L;
+    const int64_t chunks = L / 64;
 
-    v8i qop[G];
-    v8h sqop[G];
+    // ---- cooperative staging: thread tid moves pieces tid + 256 p
+    // K~ piece u: key u / (D / 16), bytes 16 (u % (D / 16)) of its row
+    auto k_lds_off = [](int u) {
+        const int key = u / (D / 16), part = u % (D / 16);
+        const int g = part >> 2, hh = (part >> 1) & 1, j = part & 1;
+        const int t = (key >> 4) & 1;
+        const int rho = 8 * ((key >> 2) & 3) + 4 * (key >> 5) + (key & 3);
+        return (((t * G + g) * 2 + j) * 64 + rho + 32 * hh) * 16;
+    };
+    // V~^T piece u: channel u / 4, bytes 16 (u % 4) of its 64-key row
+    auto v_lds_off = [](int u) {
+        const int ch = u >> 2, part = u & 3;
+        const int i = ch >> 5, nn = ch & 31, hh = part >> 1, j = part & 1;
+        return St::kK + ((i * 2 + j) * 64 + nn + 32 * hh) * 16;
+    };
+    // key scale of key `key`, group g -> [t][g][rho]
+    auto sk_lds_off = [](int key, int g) {
+        const int t = (key >> 4) & 1;
+        const int rho = 8 * ((key >> 2) & 3) + 4 * (key >> 5) + (key & 3);
+        return St::kK + St::kV + ((t * G + g) * 32 + rho) * 2;
+    };
+    v4u kr[St::kKItems], vr[St::kVItems];     // native vectors: kept in registers
+    uint16_t skr = 0, svr = 0;
+    auto load_chunk = [&](int64_t c, bool with_v) {
+        const uint8_t* kc = kx + (head * L + 64 * c) * D;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        qop[g] = load32(qx + (head * L + q0 + n) * D + 64 * g + 32 * h);
-        sqop[g] = scale_operand(qs[g * rows + head * L + q0 + n], h);
-    }
-    // key of row n of key tile t (within the chunk)
-    const int krow = 32 * ((n >> 2) & 1) + 4 * (n >> 3) + (n & 3);
+        for (int p = 0; p < St::kKItems; ++p)
+            kr[p] = reinterpret_cast<const v4u*>(kc)[tid + 256 * p];
+        if (tid < 64 * G)
+            skr = ks[(tid >> 6) * rows + head * L + 64 * c + (tid & 63)];
+        if (with_v) {
+#pragma unroll
+            for (int p = 0; p < St::kVItems; ++p) {
+                const int u = tid + 256 * p;
+                vr[p] = *reinterpret_cast<const v4u*>(vx + (head * D + (u >> 2)) * L + 64 * c + 16 * (u & 3));
+            }
+            if (tid < D)
+                svr = vs[c * heads * D + head * D + tid];
+        }
+    };
+    auto store_chunk = [&](int b, bool with_v) {
+        uint8_t* s = smem[b];
+#pragma unroll
+        for (int p = 0; p < St::kKItems; ++p)
+            *reinterpret_cast<v4u*>(s + k_lds_off(tid + 256 * p)) = kr[p];
+        if (tid < 64 * G)
+            *reinterpret_cast<uint16_t*>(s + sk_lds_off(tid & 63, tid >> 6)) = skr;
+        if (with_v) {
+#pragma unroll
+            for (int p = 0; p < St::kVItems; ++p)
+                *reinterpret_cast<v4u*>(s + v_lds_off(tid + 256 * p)) = vr[p];
+            if (tid < D)
+                *reinterpret_cast<uint16_t*>(s + St::kK + St::kV + St::kSk + 2 * tid) = svr;
+        }
+    };
+    auto lds32 = [&](const uint8_t* s) {
+        const uint4 a = *reinterpret_cast<const uint4*>(s);
+        const uint4 b = *reinterpret_cast<const uint4*>(s + 1024);
+        return v8i{(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
+    };
 
-    // x (the scores before the 1 / sqrt(d)) of chunk c: x[t][r] belongs to
-    // key 64 c + 32 h + 16 t + r of query q0 + n
-    auto scores = [&](int64_t c, v16f (&x)[2]) {
+    uint8_t* const qw = qsm[tid >> 6];
+    v8h sqop[G];
+    if (active) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const uint4* src = reinterpret_cast<const uint4*>(qx + (head * L + q0 + n) * D + 64 * g + 32 * h);
+            *reinterpret_cast<uint4*>(qw + g * 2048 + lane * 16) = src[0];
+            *reinterpret_cast<uint4*>(qw + g * 2048 + 1024 + lane * 16) = src[1];
+            sqop[g] = scale_operand(qs[g * rows + head * L + q0 + n], h);
+        }
+    }
+
+    // x (the scores before the 1 / sqrt(d)) of the chunk in stage s: x[t][r]
+    // belongs to key 32 h + 16 t + r of the chunk and query q0 + n
+    auto scores = [&](const uint8_t* s, v16f (&x)[2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            const int64_t key = head * L + 64 * c + krow + 16 * t;
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                const v8i kop = load32(kx + key * D + 64 * g + 32 * h);
-                const v8h skop = scale_operand(ks[g * rows + key], h);
-                const v16f sc = mfma_outer(skop, sqop[g]);
-                const v16f p = mfma_fp8(kop, qop[g]);
+                const v8i kop = lds32(s + (t * G + g) * 2048 + lane * 16);
+                const uint16_t skb =
+                    *reinterpret_cast<const uint16_t*>(s + St::kK + St::kV + ((t * G + g) * 32 + n) * 2);
+                const v16f sc = mfma_outer(scale_operand(skb, h), sqop[g]);
+                const v16f p = mfma_fp8(kop, lds32(qw + g * 2048 + lane * 16));
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     x[t][r] = g == 0 ? p[r] * sc[r] : fmaf(p[r], sc[r], x[t][r]);
@@ -180,29 +275,40 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
         }
     };
 
-    const int64_t chunks = L / 64;
     // pass 1: per lane the running max and sum of exp over its 32 keys of
     // every chunk, in the base-2 domain: exp(S - m) = 2^((x - m_x) kexp)
     float m = -INFINITY, l = 0.0f;
+    load_chunk(0, false);
+    store_chunk(0, false);
+    __syncthreads();
     for (int64_t c = 0; c < chunks; ++c) {
-        v16f x[2];
-        scores(c, x);
-        float cm = x[0][0];
+        if (c + 1 < chunks)
+            load_chunk(c + 1, false);
+        if (active) {
+            v16f x[2];
+            scores(smem[c & 1], x);
+            // four independent chains per reduction (a lone chain of 32
+            // dependent instructions leaves the SIMD idle between them)
+            float cm4[4] = {x[0][0], x[0][8], x[1][0], x[1][8]};
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                cm = fmaxf(cm, x[t][r]);
-        const float mn = fmaxf(m, cm);
-        const float nmk = -mn * kexp;
-        float cs = 0.0f;
+                for (int r = 0; r < 16; ++r)
+                    cm4[2 * t + r / 8] = fmaxf(cm4[2 * t + r / 8], x[t][r]);
+            const float mn = fmaxf(m, fmaxf(fmaxf(cm4[0], cm4[1]), fmaxf(cm4[2], cm4[3])));
+            const float nmk = -mn * kexp;
+            float cs4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                cs += __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk));
-        l = l * __builtin_amdgcn_exp2f((m - mn) * kexp) + cs;
-        m = mn;
+                for (int r = 0; r < 16; ++r)
+                    cs4[2 * t + r / 8] += __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk));
+            l = l * __builtin_amdgcn_exp2f((m - mn) * kexp) + ((cs4[0] + cs4[1]) + (cs4[2] + cs4[3]));
+            m = mn;
+        }
+        if (c + 1 < chunks)
+            store_chunk((c + 1) & 1, false);
+        __syncthreads();
     }
     {
         // the two half-waves' keys of the same query (identical result in both)
@@ -219,75 +325,99 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
     for (int i = 0; i < TV; ++i)
         acc[i] = v16f{};
     // pass 2
+    load_chunk(0, true);
+    store_chunk(0, true);
+    __syncthreads();
     for (int64_t c = 0; c < chunks; ++c) {
-        v16f x[2];
-        scores(c, x);
-        float amax = 0.0f;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                x[t][r] = __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk)) * inv_l;   // P
-                amax = fmaxf(amax, x[t][r]);
-            }
-        const float alpha = fmaxf(amax, xhalf(amax));
-        const _Float16 s16 = (_Float16)(alpha / 127.0f);
-        const uint16_t sbits = __builtin_bit_cast(uint16_t, s16);
-        const float rs = sbits == 0 ? 0.0f : 1.0f / (float)s16;
-        // Stage-1 codes (P >= 0), the max of each subgroup, FLAG, then the
-        // LZS value d = (q >> FLAG) << FLAG as a float
-        float qmax[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // per 8 registers
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                x[t][r] = fminf(__builtin_rintf(x[t][r] * rs), 127.0f);
-                qmax[2 * t + r / 8] = fmaxf(qmax[2 * t + r / 8], x[t][r]);
-            }
-        uint32_t mask[4];
-        if constexpr (GS == 8) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                mask[k] = ~0u << lzs_flag((uint32_t)qmax[k]);
-        } else if constexpr (GS == 16) {
-#pragma unroll
+        if (c + 1 < chunks)
+            load_chunk(c + 1, true);
+        if (active) {
+            const uint8_t* s = smem[c & 1];
+            v16f x[2];
+            scores(s, x);
+            // e = exp(S - max) and its maximum over each 8 consecutive keys
+            float e8[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    #pragma unroll
             for (int t = 0; t < 2; ++t)
-                mask[2 * t] = mask[2 * t + 1] = ~0u << lzs_flag((uint32_t)fmaxf(qmax[2 * t], qmax[2 * t + 1]));
-        } else {
-            float q4 = fmaxf(fmaxf(qmax[0], qmax[1]), fmaxf(qmax[2], qmax[3]));
-            if constexpr (GS == 64)
-                q4 = fmaxf(q4, xhalf(q4));
-            mask[0] = mask[1] = mask[2] = mask[3] = ~0u << lzs_flag((uint32_t)q4);
+    #pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    x[t][r] = __builtin_amdgcn_exp2f(fmaf(x[t][r], kexp, nmk));
+                    e8[2 * t + r / 8] = fmaxf(e8[2 * t + r / 8], x[t][r]);
+                }
+            // alpha = max of P = e / sum over the 64-key group (binary32 rounding
+            // of e * inv_l is monotone, so max(e) * inv_l is that maximum), the
+            // fp16 scale and r = 1 / s.  The code multiplier R = inv_l r takes
+            // P r in one rounding instead of two.
+            float emax = fmaxf(fmaxf(e8[0], e8[1]), fmaxf(e8[2], e8[3]));
+            emax = fmaxf(emax, xhalf(emax));
+            const float alpha = emax * inv_l;
+            const _Float16 s16 = (_Float16)(alpha / 127.0f);
+            const uint16_t sbits = __builtin_bit_cast(uint16_t, s16);
+            const float R = sbits == 0 ? 0.0f : inv_l * (1.0f / (float)s16);
+            // FLAG of each subgroup from its largest code (q = min(rne(e R), 127)
+            // is monotone in e), as the e4m3 table of c 2^FLAG, c = 0 .. 7: the
+            // base table with FLAG added to the exponent field of entries 1 .. 7
+            auto flag_of = [&](float emx) {
+                return lzs_flag((uint32_t)fminf(__builtin_rintf(emx * R), 127.0f));
+            };
+            int fl[4];
+            if constexpr (GS == 8) {
+    #pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    fl[k] = flag_of(e8[k]);
+            } else if constexpr (GS == 16) {
+    #pragma unroll
+                for (int t = 0; t < 2; ++t)
+                    fl[2 * t] = fl[2 * t + 1] = flag_of(fmaxf(e8[2 * t], e8[2 * t + 1]));
+            } else {
+                float e4 = fmaxf(fmaxf(e8[0], e8[1]), fmaxf(e8[2], e8[3]));
+                if constexpr (GS == 64)
+                    e4 = emax;
+                fl[0] = fl[1] = fl[2] = fl[3] = flag_of(e4);
+            }
+            Fp8Table tab[4];
+    #pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                tab[k].lo = kTabLo + (uint32_t)fl[k] * 0x08080800u;
+                tab[k].hi = kTabHi + (uint32_t)fl[k] * 0x08080808u;
+            }
+            // The k-slice of P~^T: dword k of the operand holds keys (relative to
+            // the half-wave) 8 (k / 2) + {0, 4, 1, 5} (k even) or {2, 6, 3, 7}
+            // (k odd), the byte order of the expanded V~^T rows.  Per dword the
+            // four Stage-1 codes q = min(rne(e R), 127) as bytes (v_cvt_pk_u8_f32
+            // rounds to nearest even), c = q >> FLAG per byte, and the e4m3 value
+            // of c 2^FLAG by table lookup.
+            v8i pop;
+    #pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int t = k >> 2, base = 8 * ((k >> 1) & 1) + 2 * (k & 1);
+                const int sub = k >> 1;
+                uint32_t w = __builtin_amdgcn_cvt_pk_u8_f32(fminf(x[t][base] * R, 127.0f), 0u, 0u);
+                w = __builtin_amdgcn_cvt_pk_u8_f32(fminf(x[t][base + 4] * R, 127.0f), 1u, w);
+                w = __builtin_amdgcn_cvt_pk_u8_f32(fminf(x[t][base + 1] * R, 127.0f), 2u, w);
+                w = __builtin_amdgcn_cvt_pk_u8_f32(fminf(x[t][base + 5] * R, 127.0f), 3u, w);
+                const uint32_t cb = (w >> fl[sub]) & 0x07070707u;
+                pop[k] = (int)__builtin_amdgcn_perm(tab[sub].hi, tab[sub].lo, cb);
+            }
+            const v8h spop = scale_operand(sbits, h);
+#pragma unroll
+            for (int i = 0; i < TV; ++i) {
+                const v8i vop = lds32(s + St::kK + i * 2048 + lane * 16);
+                const uint16_t svb = *reinterpret_cast<const uint16_t*>(
+                    s + St::kK + St::kV + St::kSk + (32 * i + n) * 2);
+                const v16f sc = mfma_outer(scale_operand(svb, h), spop);
+                const v16f p = mfma_fp8(vop, pop);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    acc[i][r] = fmaf(p[r], sc[r], acc[i][r]);
+            }
         }
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                x[t][r] = (float)((uint32_t)x[t][r] & mask[2 * t + r / 8]);
-        // the k-slice of P~^T: dword k of the operand holds keys (relative to
-        // the half-wave) 8 (k / 2) + {0, 4, 1, 5} (k even) or {2, 6, 3, 7}
-        // (k odd), the byte order of the expanded V~^T rows
-        v8i pop;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int t = k >> 2, base = 8 * ((k >> 1) & 1) + 2 * (k & 1);
-            int w = __builtin_amdgcn_cvt_pk_fp8_f32(x[t][base], x[t][base + 4], 0, false);
-            w = __builtin_amdgcn_cvt_pk_fp8_f32(x[t][base + 1], x[t][base + 5], w, true);
-            pop[k] = w;
-        }
-        const v8h spop = scale_operand(sbits, h);
-#pragma unroll
-        for (int i = 0; i < TV; ++i) {
-            const int64_t ch = head * D + 32 * i + n;
-            const v8i vop = load32(vx + ch * L + 64 * c + 32 * h);
-            const v8h svop = scale_operand(vs[c * heads * D + ch], h);
-            const v16f sc = mfma_outer(svop, spop);
-            const v16f p = mfma_fp8(vop, pop);
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                acc[i][r] = fmaf(p[r], sc[r], acc[i][r]);
-        }
+        if (c + 1 < chunks)
+            store_chunk((c + 1) & 1, true);
+        __syncthreads();
     }
+    if (!active)
+        return;
     // O^T tile i, register r: channel 32 i + 8 (r / 4) + 4 h + r % 4 of query
     // q0 + n; four consecutive channels per 8-byte store
     typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
