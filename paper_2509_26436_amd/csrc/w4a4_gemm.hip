@@ -12,9 +12,12 @@ namespace {
 // operands shared less well in L2) eat the gain.  With fewer tiles than
 // workgroups, every workgroup takes at least kMinSplitGroups groups and a
 // tile is shared by about kMaxSplitWays workgroups at most (each extra one
-// costs the finisher a slot read).
+// costs the finisher a slot read), and nothing is split when that leaves
+// fewer than two workgroups per tile on average: the exchange of partial
+// sums then costs more than the balance gains (9 tiles of 18 groups: 36 us
+// split over 40 workgroups against 20 us whole).
 constexpr int64_t kMinSplitSaving = 16;
-constexpr int64_t kMinSplitGroups = 4;
+constexpr int64_t kMinSplitGroups = 16;
 constexpr int64_t kMaxSplitWays = 8;
 
 size_t counter_bytes(const GemmSchedule& s)
@@ -51,6 +54,8 @@ GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool spl
         sk_first = 0;
         const int64_t min_units = std::max(kMinSplitGroups, (G + kMaxSplitWays - 1) / kMaxSplitWays);
         sk_blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, T * G / min_units));
+        if (sk_blocks < 2 * T)
+            return s;                          // under two workgroups per tile: not worth the exchange
     }
     const int64_t units = (T - sk_first) * G;
     if (units >= (int64_t(1) << 30))

@@ -1205,26 +1205,41 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 return true;
             }
             // more contributors: acc = sum of their slots in workgroup order
-            // (this wave's own slot included, re-read: it holds the same values)
-            for (int32_t bb = b_first; bb <= b_last; ++bb) {
-                const Rsrc part = slot_rsrc(sk_slot(sch_, bb, cur.sg.sk_tile));
+            // (this wave's own slot included, re-read: it holds the same values),
+            // per 32 x 32 tile, with two contributors' loads in flight at a time
+            // (a lone slot read per step left the finisher waiting on each
+            // round trip in turn)
 #pragma unroll
-                for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j)
+                for (int j = 0; j < TN; ++j) {
+                    const int toff = (int)(lane_off + (i * TN + j) * 4 * 1024);
+                    for (int32_t bb = b_first; bb <= b_last; bb += 2) {
+                        const bool two = bb < b_last;
+                        v4f va[4], vb[4];
+                        const Rsrc pa = slot_rsrc(sk_slot(sch_, bb, cur.sg.sk_tile));
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const v4f v = __builtin_amdgcn_raw_buffer_load_b128(
-                                part, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
+                        for (int q = 0; q < 4; ++q)
+                            va[q] = __builtin_amdgcn_raw_buffer_load_b128(pa, toff + q * 1024, 0, kCoherent);
+                        if (two) {
+                            const Rsrc pb = slot_rsrc(sk_slot(sch_, bb + 1, cur.sg.sk_tile));
+#pragma unroll
+                            for (int q = 0; q < 4; ++q)
+                                vb[q] = __builtin_amdgcn_raw_buffer_load_b128(pb, toff + q * 1024, 0, kCoherent);
+                        }
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
                                 if (bb == b_first)
-                                    acc[i][j][4 * q + e] = v[e];
+                                    acc[i][j][4 * q + e] = va[q][e];
                                 else
-                                    acc[i][j][4 * q + e] += v[e];
+                                    acc[i][j][4 * q + e] += va[q][e];
+                                if (two)
+                                    acc[i][j][4 * q + e] += vb[q][e];
                             }
-                        }
-            }
+                    }
+                }
             if (lane == 0)
                 __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return true;

@@ -63,7 +63,7 @@ EXACT = [
     (300, 320, 256, 16, 16, True, False, True),     # ragged M, half-used last column tile
     (300, 320, 2048, 8, 32, True, True, False),     # split along K (tiles shared)
     (64, 64, 128, 64, 8, False, False, False),      # one wave column
-    (1, 128, 2048, 32, 64, True, True, False),      # a single row, one tile over 8 workgroups
+    (1, 128, 2048, 32, 64, True, True, False),      # a single row, one tile over 2 workgroups
     (513, 448, 2048, 16, 16, True, True, True),     # three tile rows, split
     (256, 1152, 512, 16, 16, True, False, False),   # the single-linear width
 ]

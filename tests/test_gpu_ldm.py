@@ -113,7 +113,7 @@ def _check(y, y64, S, K, epi):
 CASES = [
     # (cfg, layer, M, N, gs, epilogue, bias, workspace, ldy_pad)
     (1, 0, 200, 136, 16, 0, True, False, 0),
-    (1, 0, 160, 448, 16, 1, True, True, 0),       # split along K
+    (2, 3, 160, 448, 16, 1, True, True, 0),       # K = 4608, split along K
     (3, 0, 300, 200, 8, 0, False, True, 6),       # ragged, no bias, strided output
     (3, 3, 257, 129, 32, 0, True, True, 0),       # K = 12288, split
     (5, 1, 64, 640, 64, 1, True, False, 0),       # K = 5760, GELU

@@ -1,7 +1,7 @@
 """GPU parity of the workspace (stream-K) entry point quartz_w4a4_linear_ws.
 
 Shapes are chosen so that, on a device with 256 compute units, the schedule
-splits tiles along K: fewer tiles than workgroups (tiles shared by up to nine
+splits tiles along K: fewer tiles than workgroups (tiles shared by up to eight
 workgroups), a ragged number of rounds, every LZS subgroup size, GELU, no
 bias and a strided output.  Every output is compared with the oracle within
 the tolerance of tests/helpers.py; repeated calls on one workspace must give
@@ -58,8 +58,8 @@ def _schedule_of(M, N, K):
 
 CASES = [
     # (cfg, layer, M, N, gs, epilogue, bias, ldy_pad)
-    (1, 0, 160, 448, 16, 0, True, 0),      # 4 tiles x 18 groups over 18 workgroups
-    (1, 0, 70, 130, 16, 1, False, 0),      # 2 tiles, GELU, no bias
+    (2, 3, 160, 448, 16, 0, True, 0),      # 4 tiles x 72 groups over 18 workgroups
+    (2, 3, 70, 130, 16, 1, False, 0),      # 2 tiles x 72 groups over 9 workgroups, GELU, no bias
     (3, 0, 300, 200, 8, 0, True, 6),       # ragged rows and columns, strided output
     (3, 3, 257, 129, 32, 0, True, 0),      # K = 12288: 4 tiles x 192 groups
     (5, 0, 513, 320, 64, 1, True, 0),      # 9 tiles, GELU
@@ -95,10 +95,10 @@ def test_ws_slot_contents_do_not_matter():
     (NaN floats) and the result is unchanged."""
     import torch
     q = _q()
-    M, N, K = 160, 448, 1152
-    xb = W.make_x(1, 0, rows=M)
-    wb = W.make_w(1, 0, rows=N)
-    bias = W.make_bias(1, 0, cols=N)
+    M, N, K = 160, 448, 4608
+    xb = W.make_x(2, 3, rows=M)
+    wb = W.make_w(2, 3, rows=N)
+    bias = W.make_bias(2, 3, cols=N)
     qa, pw, a_ref, wq_ref, sw_ref = _gemm_case(xb, wb, 16)
     ws = q.gemm_workspace(M, N, K, "cuda")
     y1 = _ws_linear(qa, pw, bias, 0, ws)
@@ -129,9 +129,9 @@ def test_ws_matches_plain_entry_point_within_order():
 def test_ws_null_and_too_small():
     import torch
     q = _q()
-    M, N, K = 160, 448, 1152
-    xb = W.make_x(1, 0, rows=M)
-    wb = W.make_w(1, 0, rows=N)
+    M, N, K = 160, 448, 4608
+    xb = W.make_x(2, 3, rows=M)
+    wb = W.make_w(2, 3, rows=N)
     qa, pw, a_ref, wq_ref, sw_ref = _gemm_case(xb, wb, 16)
     need = q.quartz_w4a4_linear_workspace_bytes(M, N, K)
     assert need > 0
