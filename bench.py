@@ -26,6 +26,13 @@ counters of a profiled run, each scaled by what the counter reads for a plain
 device copy of known size (--copy-calibration); read from the committed
 summary under profiles/ and reported only while the GEMM sources still hash
 to the values recorded there (null otherwise).
+
+Secondary sections of the same line (not part of `value`): the other
+workloads of the benchmark set (config1, config2, batched_mlp, conv3x3), the
+LDM and asymmetric settings, cold-cache and G_s-sweep timings, and
+`attention`: LZS attention (quartz_lzs_attention) in the heads x dim and
+group settings of Table 8 at the FLUX sequence length, with the stage
+pipeline of one head broken down by stage.
 """
 from __future__ import annotations
 
