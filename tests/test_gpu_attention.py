@@ -13,7 +13,8 @@ and end to end, through the C ABI.
   * PV on the oracle's quantized softmax output and V^T: within the linear
     layer's output tolerance.
   * End to end (the fused kernel for d = 64 and 128, the stage pipeline
-    otherwise): close to the oracle (relative error, and nearly every output
+    otherwise): close to the oracle (relative error within bf16 rounding plus
+    1e-3, and nearly every output
     within the layer tolerance: the softmax codes may differ as above); the
     pipeline also equal to the composition of the stage entry points bit for
     bit.
@@ -227,11 +228,17 @@ def _staged(q, qb, kb, vb, heads, gs):
     return out
 
 
+# Relative Frobenius bound of a head's output: the bf16 rounding of the
+# output alone contributes up to 2^-9 relative; 1e-3 more covers the rare
+# softmax codes that land on the other side of a rounding boundary.
+REL_BOUND = 2.0 ** -9 + 1e-3
+
+
 def _compare_head(O_gpu, O64, A, L):
     err = np.abs(O_gpu - O64)
     rel = np.linalg.norm(O_gpu - O64) / np.linalg.norm(O64)
     within = (err <= y_tolerance(O64, A, L)).mean()
-    assert rel <= 2e-3, f"relative error {rel:.2e}"
+    assert rel <= REL_BOUND, f"relative error {rel:.2e}"
     assert within >= 0.99, f"only {within:.4f} of the outputs within the layer tolerance"
 
 
