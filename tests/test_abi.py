@@ -256,3 +256,69 @@ def test_layers_reject_activations_of_another_mode():
             for fn in fns:
                 with pytest.raises(ValueError, match="mode"):
                     fn(act(other))
+
+
+def test_attention_entry_validation(lib):
+    EWS = 6
+    vt = q.quartz_quantize_vt
+    assert vt(A, 2, 128, 128, 128, 12, A, A, A, None) == EUNSUP
+    assert vt(A, 2, 100, 128, 128, 16, A, A, A, None) == ESHAPE       # L % 64
+    assert vt(A, 2, 128, 96, 128, 16, A, A, A, None) == ESHAPE        # d % 64
+    assert vt(A, 2, 128, 128, 64, 16, A, A, A, None) == ESHAPE        # ldv < d
+    assert vt(A, 2, 128, 128, 132, 16, A, A, A, None) == EALIGN       # ldv % 8
+    assert vt(A, 0, 128, 128, 128, 16, A, A, A, None) == OK
+    assert vt(None, 2, 128, 128, 128, 16, A, A, A, None) == ENULL
+    assert vt(A + 2, 2, 128, 128, 128, 16, A, A, A, None) == EALIGN
+    sm = q.quartz_softmax_quantize
+    assert sm(A, 8, 128, 128, 5, A, A, A, None) == EUNSUP
+    assert sm(A, 8, 100, 128, 16, A, A, A, None) == ESHAPE            # N % 64
+    assert sm(A, 8, 128, 64, 16, A, A, A, None) == ESHAPE             # lds < N
+    assert sm(A, 8, 128, 130, 16, A, A, A, None) == EALIGN            # lds % 4
+    assert sm(A, 0, 128, 128, 16, A, A, A, None) == OK
+    assert sm(None, 8, 128, 128, 16, A, A, A, None) == ENULL
+    assert sm(A + 4, 8, 128, 128, 16, A, A, A, None) == EALIGN
+    sc = q.quartz_attn_scores
+
+    def scores(q_plane=256, q_row0=0, Lq=128, Lk=128, d=128, gs=16, scale=0.1, s=A, lds=128):
+        return sc(A, A, A, q_plane, q_row0, A, A, A, 256, 0, Lq, Lk, d, gs, scale, s, lds, None)
+    assert scores(scale=float("inf")) == EUNSUP
+    assert scores(gs=3) == EUNSUP
+    assert scores(d=96) == ESHAPE
+    assert scores(q_row0=200) == ESHAPE                                # rows past the plane
+    assert scores(lds=64) == ESHAPE
+    assert scores(Lq=0) == OK
+    assert scores(s=None) == ENULL
+    assert scores(s=A + 4) == EALIGN
+    pv = q.quartz_attn_pv
+
+    def pvc(vt_plane=256, vt_row0=0, Lq=128, Lk=128, d=128, o=A, ldo=128, ws=None, wsb=0):
+        return pv(A, A, A, A, A, A, vt_plane, vt_row0, Lq, Lk, d, 16, o, ldo, ws, wsb, None)
+    assert pvc(Lk=100) == ESHAPE
+    assert pvc(vt_row0=200) == ESHAPE                                  # d channels past the plane
+    assert pvc(ldo=64) == ESHAPE
+    assert pvc(Lq=0) == OK
+    assert pvc(o=None) == ENULL
+    assert pvc(o=A + 2) == EALIGN
+    assert pvc(ws=A + 4, wsb=1 << 20) == EALIGN
+    # the whole attention: for d = 64 and 128 the workspace holds the codes,
+    # flags and scales of Q, K and V^T and their fp8 expansions (256-byte aligned)
+    heads, L, d, gs = 2, 256, 128, 16
+    al = lambda n: (n + 255) // 256 * 256
+    act = lambda rows, k: al(rows * k // 2) + al(rows * k // gs) + al(rows * k // 64 * 2)
+    need = 2 * act(heads * L, d) + act(heads * d, L) + 3 * al(heads * L * d)
+    assert q.quartz_lzs_attention_workspace_bytes(heads, L, d, gs) == need
+    assert q.quartz_lzs_attention_workspace_bytes(heads, 100, d, gs) == 0
+    assert q.quartz_lzs_attention_workspace_bytes(heads, L, d, 7) == 0
+    la = q.quartz_lzs_attention
+
+    def att(heads=2, L=256, d=128, gs=16, o=A, ldo=256, ws=A, wsb=need):
+        return la(A, A, A, heads, L, d, gs, o, ldo, ws, wsb, None)
+    assert att(gs=12) == EUNSUP
+    assert att(L=100) == ESHAPE
+    assert att(L=1 << 17) == ESHAPE                                    # L <= 2^16
+    assert att(ldo=128) == ESHAPE                                      # ldo < heads d
+    assert att(ldo=258) == EALIGN                                      # ldo % 4
+    assert att(heads=0) == OK
+    assert att(ws=None) == ENULL
+    assert att(o=A + 2) == EALIGN
+    assert att(wsb=need - 256) == EWS                                  # nothing launched
