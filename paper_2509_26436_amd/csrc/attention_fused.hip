@@ -34,6 +34,7 @@
 // a 64-key group takes one exchange between the two half-waves.  The same
 // registers, converted to e4m3 and packed in the byte order the fp8 expansion
 // gives V~^T's keys, are the k-slice of the PV product O^T = V~^T P~^T.
+#include <algorithm>
 #include <cmath>
 
 #include "lzs_device.h"
@@ -44,6 +45,7 @@ namespace quartz {
 namespace {
 
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
 
 // ------------------------------------------------------------ fp8 expansion
 // One (group, row) of a K-group-major LZS activation per thread: its 32 code
@@ -137,7 +139,7 @@ __device__ __forceinline__ float xhalf(float v)       // value of lane l ^ 32
 //   V~^T [i][j][lane][16 B]: lane (n, h) holds bytes 32 h + 16 j .. of the
 //        chunk's 64 keys of channel 32 i + n;
 //   the key scales [t][g][rho] and the channel scales [D] (fp16).
-template <int G>
+template <int G, int W>
 struct AttnStage {
     static constexpr int D = 64 * G;
     static constexpr int kK = 64 * D;               // K~ bytes
@@ -145,27 +147,29 @@ struct AttnStage {
     static constexpr int kSk = 64 * G * 2;
     static constexpr int kSv = D * 2;
     static constexpr int kBytes = kK + kV + kSk + kSv;
-    static constexpr int kKItems = kK / 16 / 256;   // 16-byte pieces per thread
-    static constexpr int kVItems = kV / 16 / 256;
+    static constexpr int kThreads = 64 * W;
+    static constexpr int kKPieces = kK / 16, kVPieces = kV / 16;   // 16-byte pieces
+    static constexpr int kKItems = (kKPieces + kThreads - 1) / kThreads;   // per thread
+    static constexpr int kVItems = (kVPieces + kThreads - 1) / kThreads;
 };
 
 // One block: 4 waves, queries qb * 128 + 32 w .. + 31 of head `head`, which
 // share the staged chunks.  qx / kx: [heads L][64 G] e4m3, qs / ks:
 // [G][heads L] fp16; vx: [heads d][L] e4m3 (V^T), vs: [L / 64][heads d] fp16;
 // o: bf16 [L][ldo], head h at columns h d ...
-template <int GS, int G>
-__global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
+template <int GS, int G, int W>
+__global__ __launch_bounds__(64 * W, 8 / W) void lzs_attention_fused_kernel(
     const uint8_t* __restrict__ qx, const uint16_t* __restrict__ qs,
     const uint8_t* __restrict__ kx, const uint16_t* __restrict__ ks,
     const uint8_t* __restrict__ vx, const uint16_t* __restrict__ vs, int64_t heads, int64_t L,
     float kexp, uint16_t* __restrict__ o, int64_t ldo, int64_t qblocks)
 {
-    using St = AttnStage<G>;
+    using St = AttnStage<G, W>;
     constexpr int D = St::D;
     constexpr int TV = D / 32;                 // channel tiles of the PV product
     __shared__ __attribute__((aligned(16))) uint8_t smem[2][St::kBytes];
     // each wave's Q~ operand, [g][j][lane][16 B] (written and read by that wave only)
-    __shared__ __attribute__((aligned(16))) uint8_t qsm[4][G * 2048];
+    __shared__ __attribute__((aligned(16))) uint8_t qsm[W][G * 2048];
 
     // blocks of one head on one XCD (consecutive block ids go round robin
     // over the 8 XCDs), so its K~ / V~^T chunks are shared in that L2
@@ -174,7 +178,7 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
     const int64_t logical = total % 8 == 0 ? (bid % 8) * (total / 8) + bid / 8 : bid;
     const int64_t head = logical / qblocks;
     const int tid = threadIdx.x;
-    const int64_t q0 = (logical % qblocks) * 128 + (tid >> 6) * 32;
+    const int64_t q0 = (logical % qblocks) * (32 * W) + (tid >> 6) * 32;
     // a wave past the end of a ragged last block still loads and waits at
     // the barriers, and computes nothing (wave-uniform)
     const bool active = q0 < L;
@@ -210,14 +214,16 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
         const uint8_t* kc = kx + (head * L + 64 * c) * D;
 #pragma unroll
         for (int p = 0; p < St::kKItems; ++p)
-            kr[p] = reinterpret_cast<const v4u*>(kc)[tid + 256 * p];
+            if (tid + St::kThreads * p < St::kKPieces)
+                kr[p] = reinterpret_cast<const v4u*>(kc)[tid + St::kThreads * p];
         if (tid < 64 * G)
             skr = ks[(tid >> 6) * rows + head * L + 64 * c + (tid & 63)];
         if (with_v) {
 #pragma unroll
             for (int p = 0; p < St::kVItems; ++p) {
-                const int u = tid + 256 * p;
-                vr[p] = *reinterpret_cast<const v4u*>(vx + (head * D + (u >> 2)) * L + 64 * c + 16 * (u & 3));
+                const int u = tid + St::kThreads * p;
+                if (u < St::kVPieces)
+                    vr[p] = *reinterpret_cast<const v4u*>(vx + (head * D + (u >> 2)) * L + 64 * c + 16 * (u & 3));
             }
             if (tid < D)
                 svr = vs[c * heads * D + head * D + tid];
@@ -227,13 +233,15 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
         uint8_t* s = smem[b];
 #pragma unroll
         for (int p = 0; p < St::kKItems; ++p)
-            *reinterpret_cast<v4u*>(s + k_lds_off(tid + 256 * p)) = kr[p];
+            if (tid + St::kThreads * p < St::kKPieces)
+                *reinterpret_cast<v4u*>(s + k_lds_off(tid + St::kThreads * p)) = kr[p];
         if (tid < 64 * G)
             *reinterpret_cast<uint16_t*>(s + sk_lds_off(tid & 63, tid >> 6)) = skr;
         if (with_v) {
 #pragma unroll
             for (int p = 0; p < St::kVItems; ++p)
-                *reinterpret_cast<v4u*>(s + v_lds_off(tid + 256 * p)) = vr[p];
+                if (tid + St::kThreads * p < St::kVPieces)
+                    *reinterpret_cast<v4u*>(s + v_lds_off(tid + St::kThreads * p)) = vr[p];
             if (tid < D)
                 *reinterpret_cast<uint16_t*>(s + St::kK + St::kV + St::kSk + 2 * tid) = svr;
         }
@@ -435,21 +443,43 @@ __global__ __launch_bounds__(256, 2) void lzs_attention_fused_kernel(
         }
 }
 
+template <int GS, int W>
+void launch_fused_w(const uint8_t* qx, const uint16_t* qs, const uint8_t* kx, const uint16_t* ks,
+                    const uint8_t* vx, const uint16_t* vs, int64_t heads, int64_t L, int64_t d,
+                    uint16_t* o, int64_t ldo, hipStream_t stream)
+{
+    const int64_t qblocks = (L + 32 * W - 1) / (32 * W);
+    const dim3 grid((unsigned)(heads * qblocks)), block(64 * W);
+    const float kexp = (float)(1.4426950408889634 / std::sqrt((double)d));
+    if (d == 64)
+        lzs_attention_fused_kernel<GS, 1, W><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
+                                                                          kexp, o, ldo, qblocks);
+    else
+        lzs_attention_fused_kernel<GS, 2, W><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
+                                                                          kexp, o, ldo, qblocks);
+}
+
+// Block shape: 8 query waves per block share each staged chunk among twice
+// the queries of 4 and cost ~8.5 % less per wave, but run one block per CU,
+// so a launch takes whole rounds of 8-wave blocks; with 4-wave blocks (two
+// per CU) a partial last round is spread one block per CU and runs faster
+// per block, so the time grows about linearly with the block count.  Take 8
+// waves only when the last round of 8-wave blocks is nearly full (measured
+// at L = 4608: 40 heads, 2.81 rounds, 0.88 against 0.93 ms; 32 and 64 heads,
+// 2.25 and 4.5 rounds, favour 4 waves).
 template <int GS>
 hipError_t launch_fused_gs(const uint8_t* qx, const uint16_t* qs, const uint8_t* kx,
                            const uint16_t* ks, const uint8_t* vx, const uint16_t* vs,
                            int64_t heads, int64_t L, int64_t d, uint16_t* o, int64_t ldo,
                            hipStream_t stream)
 {
-    const int64_t qblocks = (L + 127) / 128;
-    const dim3 grid((unsigned)(heads * qblocks)), block(256);
-    const float kexp = (float)(1.4426950408889634 / std::sqrt((double)d));
-    if (d == 64)
-        lzs_attention_fused_kernel<GS, 1><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
-                                                                       kexp, o, ldo, qblocks);
+    const int64_t cus = std::max<int64_t>(1, device_compute_units());
+    const int64_t blocks8 = heads * ((L + 255) / 256);
+    const int64_t rounds8 = (blocks8 + cus - 1) / cus;
+    if (rounds8 * cus * 100 <= blocks8 * 109)
+        launch_fused_w<GS, 8>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
     else
-        lzs_attention_fused_kernel<GS, 2><<<grid, block, 0, stream>>>(qx, qs, kx, ks, vx, vs, heads, L,
-                                                                       kexp, o, ldo, qblocks);
+        launch_fused_w<GS, 4>(qx, qs, kx, ks, vx, vs, heads, L, d, o, ldo, stream);
     return hipGetLastError();
 }
 

@@ -315,3 +315,30 @@ def test_attention_full_size_sampled():
         pa = oracle.quantize_f32(oracle.softmax_rows(S.reshape(rows.size, L)), gs)
         O64, A = oracle.attn_pv_f64(pa, vta)
         _compare_head(Og[rows, h * d:(h + 1) * d], O64, A, L)
+
+
+@pytest.mark.parametrize("heads,L,d", [(120, 320, 128), (240, 256, 64)])
+def test_attention_eight_wave_blocks(heads, L, d):
+    """Head counts whose last round of 8-wave blocks is nearly full run the
+    fused kernel with 8 query waves per block (the launch rule: rounds x CUs
+    <= 1.09 x blocks); L = 320 leaves a ragged block with 6 idle waves.
+    Sampled heads against the oracle."""
+    import torch
+    q = _q()
+    gs = 16
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks8 = heads * ((L + 255) // 256)
+    rounds8 = -(-blocks8 // cus)
+    print(f"8-wave blocks: {blocks8} blocks, {rounds8} rounds on {cus} CUs", flush=True)
+    if rounds8 * cus * 100 > blocks8 * 109:
+        pytest.skip("this device's CU count selects the 4-wave blocks for this shape")
+    qb = rand_bf16(700 + d, (heads * L, d), 1.0, outliers=2)
+    kb = rand_bf16(701 + d, (heads * L, d), 1.0, outliers=2)
+    vb = rand_bf16(702 + d, (heads * L, d), 1.0, outliers=2)
+    O = q.lzs_attention(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb), heads, gs)
+    torch.cuda.synchronize()
+    Og = bf16_bits_to_f64(to_host_u16(O))
+    for h in (0, 1, heads // 2, heads - 2, heads - 1):
+        sl = slice(h * L, (h + 1) * L)
+        O64, parts = oracle.lzs_attention_f64(qb[sl], kb[sl], vb[sl], gs)
+        _compare_head(Og[:, h * d:(h + 1) * d], O64, parts["A"], L)
