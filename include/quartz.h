@@ -104,8 +104,11 @@ size_t quartz_packed_weight_bytes(int64_t N, int64_t K, int32_t group_size);
  *   w_bf16    bf16 [N][K], row-major (the nn.Linear weight layout).
  *   w_packed  quartz_packed_weight_bytes(N, K, 64) bytes, opaque to callers:
  *             panels of 64 output columns; per (panel, group) 64 x 32 bytes of
- *             sign-magnitude nibbles in the activation-code nibble order,
- *             followed by the 64 fp16 scales; columns past N are zero.
+ *             codes, eight sign-magnitude codes per 32-bit word (the
+ *             activation-code nibble order with each sign bit moved next to
+ *             a magnitude so that a mask, or a 4-bit rotation and the mask,
+ *             yields the fp8 operands directly), followed by the 64 fp16
+ *             scales; columns past N are zero.
  *   w_scales  u16 [N][K/64] plain copy of the fp16 scales, or NULL.
  * N = 0 returns QUARTZ_OK without launching.
  */

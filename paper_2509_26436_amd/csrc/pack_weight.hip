@@ -9,8 +9,9 @@
 // A team of 8 lanes owns one (column n, group g): each lane loads 8 bf16,
 // the team reduces max|w| with DPP, every lane computes
 //   s_w = fp16_rne_sat(max|w| / 7),  r = 1/s_w,  |wq| = min(rne(|w| * r), 7)
-// and stores one 32-bit word of 8 sign-magnitude nibbles, in the same nibble
-// order as the activation codes.
+// and stores one 32-bit word of 8 sign-magnitude codes: the nibble word of the
+// activation codes' order with its sign bits moved (weight_word_store), so the
+// GEMM turns it into fp8 operands with a mask and a rotation.
 #include "quartz_internal.h"
 
 namespace quartz {
@@ -96,7 +97,7 @@ __device__ __forceinline__ void pack_group(uint4 v, uint32_t& word, uint32_t& s1
 #pragma unroll
     for (int p = 0; p < 4; ++p)
         S |= (d[p] & 0x80008000u) >> (12 - 4 * p);
-    word = T | (S & (T + 0x77777777u));
+    word = weight_word_store(T | (S & (T + 0x77777777u)));
 }
 
 // A work item is 8 consecutive columns of one panel (one team of 8 lanes per
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(256) void weight_sums_kernel(const uint8_t* __restr
         for (int w = 0; w < 4; ++w)
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t nib = (words[w] >> (4 * i)) & 0xFu;
+                const uint32_t nib = (weight_word_nibbles(words[w]) >> (4 * i)) & 0xFu;
                 const int mag = (int)(nib & 7u);
                 total += (nib & 8u) ? -mag : mag;
             }
@@ -275,8 +276,8 @@ __global__ __launch_bounds__(256) void unpack_weight_kernel(
     const int64_t g = j / 8;
     const int64_t panel = n / kPanel;
     const int64_t cpan = n % kPanel;
-    const uint32_t word = reinterpret_cast<const uint32_t*>(
-        w_packed + (panel * G + g) * kChunkBytes + cpan * 32)[j % 8];
+    const uint32_t word = weight_word_nibbles(reinterpret_cast<const uint32_t*>(
+        w_packed + (panel * G + g) * kChunkBytes + cpan * 32)[j % 8]);
     uint32_t out[2] = {0, 0};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {

@@ -11,9 +11,9 @@
 namespace quartz {
 
 // Packed weight layout: panels of kPanel output columns.  For each (panel p,
-// group g), in [panel][group] order, one chunk of kPanel * 32 bytes of nibbles
-// (column-major within the panel: column c's 64 codes at c * 32) followed by
-// kPanel fp16 scales.
+// group g), in [panel][group] order, one chunk of kPanel * 32 bytes of codes
+// (column-major within the panel: column c's 64 codes at c * 32, eight per
+// 32-bit weight word, see weight_word_store) followed by kPanel fp16 scales.
 constexpr int kGroup = 64;
 constexpr int kPanel = 64;
 constexpr int kChunkCodeBytes = kPanel * kGroup / 2;          // 2048
@@ -251,6 +251,44 @@ __device__ __forceinline__ uint2 decode_nibbles_fp8(uint32_t w, Fp8Table t)
     r.x = __builtin_amdgcn_perm(t.hi, t.lo, mag_even) | ((w << 4) & 0x80808080u);
     r.y = __builtin_amdgcn_perm(t.hi, t.lo, mag_odd) | (w & 0x80808080u);
     return r;
+}
+
+// Weight words.  The pack writes each word of 8 sign-magnitude codes (the
+// nibble word of decode_nibbles_fp8: byte i holds code E_i in its low nibble
+// and O_i in its high nibble, E = elements 0, 4, 1, 5 and O = elements 2, 6,
+// 3, 7 of the word's 8 consecutive k) with its sign bits moved: byte i keeps
+// both magnitudes in bits 0-2 (E_i) and 4-6 (O_i), the sign of E_i in bit 7
+// and the sign of O_(i-1 mod 4) in bit 3.  Then a mask gives the four E codes
+// and a rotation by 4 bits plus the same mask the four O codes, each as the
+// byte s * 128 + |c|: the OCP e4m3 subnormal of c * 2^-9, exact for |c| <= 7.
+// A GEMM on these operands yields every weight product times 2^-9 exactly
+// (all partial sums are integers times 2^-9), and the output code multiplies
+// by 2^9 once (kWeightUnitInv), which is exact.
+constexpr uint32_t kWeightCodeMask = 0x87878787u;
+constexpr float kWeightUnitInv = 512.0f;     // 1 / 2^-9
+
+__host__ __device__ __forceinline__ uint32_t rotl32(uint32_t x, int r)
+{
+    return (x << r) | (x >> (32 - r));
+}
+
+// nibble word (decode_nibbles_fp8 order) -> stored weight word
+__host__ __device__ __forceinline__ uint32_t weight_word_store(uint32_t nib)
+{
+    return (nib & 0x77777777u) | ((nib & 0x08080808u) << 4) | rotl32(nib & 0x80808080u, 4);
+}
+
+// stored weight word -> nibble word
+__host__ __device__ __forceinline__ uint32_t weight_word_nibbles(uint32_t w)
+{
+    return (w & 0x77777777u) | ((w & 0x80808080u) >> 4) | rotl32(w & 0x08080808u, 28);
+}
+
+// stored weight word -> 8 e4m3 bytes (of c * 2^-9) in the byte order of
+// decode_nibbles_fp8 (E codes in the low dword, O codes in the high one)
+__device__ __forceinline__ uint2 decode_weight_fp8(uint32_t w)
+{
+    return uint2{w & kWeightCodeMask, __builtin_amdgcn_alignbit(w, w, 4) & kWeightCodeMask};
 }
 
 }  // namespace quartz

@@ -423,7 +423,8 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 const Rsrc rw = make_rsrc(wsums + (int64_t)g * N + n0,
                                           n0 < N ? (uint32_t)((N - n0) * 2) : 0u);
                 const int ws = (int)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(rw, swc * 2, 0, 0);
-                r.wh = __builtin_bit_cast(uint16_t, (_Float16)ws);
+                // W * 2^-9, the unit of the weight operands (exact: |W| <= 448)
+                r.wh = __builtin_bit_cast(uint16_t, (_Float16)((float)ws * (1.0f / kWeightUnitInv)));
             } else {
                 r.zh = 0;
                 r.wh = 0;
@@ -503,15 +504,15 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(o[0].x, o[0].y, o[1].x, o[1].y);
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(o[2].x, o[2].y, o[3].x, o[3].y);
             }
-            const Fp8Table tw{kTabLo, kTabHi};
-            const uint2 b0 = decode_nibbles_fp8(r.b.x, tw);
-            const uint2 b1 = decode_nibbles_fp8(r.b.y, tw);
+            // weight words: e4m3 of wq * 2^-9 (weight_word_store)
+            const uint2 b0 = decode_weight_fp8(r.b.x);
+            const uint2 b1 = decode_weight_fp8(r.b.y);
             if constexpr (ATTN) {
             } else if constexpr (kSplit) {
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
             } else {
-                const uint2 b2 = decode_nibbles_fp8(r.b.z, tw);
-                const uint2 b3 = decode_nibbles_fp8(r.b.w, tw);
+                const uint2 b2 = decode_weight_fp8(r.b.z);
+                const uint2 b3 = decode_weight_fp8(r.b.w);
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh)) = make_uint4(b0.x, b0.y, b1.x, b1.y);
                 *reinterpret_cast<uint4*>(Bs[buf] + swz(bc, 2 * bh + 1)) = make_uint4(b2.x, b2.y, b3.x, b3.y);
             }
@@ -673,7 +674,7 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     // converted and added in int32, so the sum over K stays exact beyond 2^24
     // (|P_g| <= 50176 converts exactly; |sum| <= 784 K < 2^31 for K <= 2^20).
     auto add_i32 = [](float a, float p) {
-        return __int_as_float(__float_as_int(a) + (int)p);
+        return __int_as_float(__float_as_int(a) + (int)(p * kWeightUnitInv));
     };
     auto fma_tile = [&](int i, int j, const v16f& p, const v16f& sc) {
 #pragma unroll
@@ -864,21 +865,28 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 cscale_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(rs, (j * 32 + l32) * 2, 0, 0);
         }
     };
-    // the value of acc before bias and activation: acc itself, or for STATIC
-    // the integer sum times act_scale * s_w[n]
+    // the value of acc before bias and activation: acc times 2^9 (its unit is
+    // that of the weight operands), or for STATIC the integer sum times
+    // act_scale * s_w[n] (the 2^9 folded into cs)
     float cs[TN];
     auto set_out_scale = [&] {
         if constexpr (STATIC) {
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                cs[j] = act_scale * (float)__builtin_bit_cast(_Float16, cscale_bits[j]);
+                cs[j] = act_scale * (float)__builtin_bit_cast(_Float16, cscale_bits[j]) * kWeightUnitInv;
         }
     };
+    // acc is in units of the weight operands (2^-9, see decode_weight_fp8)
+    // except for ATTN, whose B operand is an activation: the factor 2^9 is
+    // exact, so fmaf(a, 2^9, b) rounds exactly like the sum of the unscaled
+    // accumulator and the bias
     auto out_value = [&](float a, int j, float bj) {
         if constexpr (STATIC)
             return fmaf(a, cs[j], bj);
-        else
+        else if constexpr (ATTN)
             return a + bj;
+        else
+            return fmaf(a, kWeightUnitInv, bj);
     };
     // ---- output quantized for the next layer (QOUT): the bf16 values the
     // plain epilogue would store, run through the activation quantizer with
