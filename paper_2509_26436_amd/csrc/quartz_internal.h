@@ -56,6 +56,14 @@ hipError_t launch_unpack_weight(const uint8_t* w_packed, int64_t N, int64_t K, i
 // of the current device (CUs x resident workgroups per CU; 0 if there is no
 // device).
 GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split);
+// the same for tiles of bm x bn
+GemmSchedule gemm_schedule_tiles(int64_t M, int64_t N, int64_t K, int blocks, bool split,
+                                 int64_t bm, int64_t bn);
+// The per-group linear layer with a bf16 output runs its own kernel
+// (w4a4_linear.hip, tiles of 128 x 256): its schedule, its persistent grid
+// size on the current device, and its launch (a.sch from linear_schedule).
+GemmSchedule linear_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split);
+int linear_resident_blocks();
 size_t gemm_workspace_bytes(const GemmSchedule& s);
 int gemm_resident_blocks();
 // bytes of the workspace's counter part (its start); the slots follow it
@@ -134,6 +142,7 @@ struct GemmLaunch {
 
 // One output mode each (w4a4_gemm_<mode>.hip).
 hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);

@@ -27,11 +27,12 @@ size_t counter_bytes(const GemmSchedule& s)
 
 }  // namespace
 
-GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split)
+GemmSchedule gemm_schedule_tiles(int64_t M, int64_t N, int64_t K, int blocks, bool split,
+                                 int64_t bm, int64_t bn)
 {
     GemmSchedule s{};
-    const int64_t tiles_m = (M + BM - 1) / BM;
-    const int64_t tiles_n = (N + BN - 1) / BN;
+    const int64_t tiles_m = (M + bm - 1) / bm;
+    const int64_t tiles_n = (N + bn - 1) / bn;
     const int64_t T = tiles_m * tiles_n;
     const int64_t G = K / 64;
     s.tiles_n = (int32_t)tiles_n;
@@ -69,6 +70,11 @@ GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool spl
     return s;
 }
 
+GemmSchedule gemm_schedule(int64_t M, int64_t N, int64_t K, int blocks, bool split)
+{
+    return gemm_schedule_tiles(M, N, K, blocks, split, BM, BN);
+}
+
 size_t gemm_counter_bytes(const GemmSchedule& s)
 {
     return s.sk_tiles > 0 ? counter_bytes(s) : 0;
@@ -101,7 +107,9 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
     GemmLaunch a{codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
                  epilogue, sch, nullptr, nullptr, qout, 0.0f};
     split_workspace(sch, workspace, a.counters, a.slots);
-    return qout.codes ? launch_gemm_quant(a, stream) : launch_gemm_plain(a, stream);
+    // the bf16 output runs the 128 x 256 kernel of w4a4_linear.hip (its
+    // schedule from linear_schedule), the quantized output the template
+    return qout.codes ? launch_gemm_quant(a, stream) : launch_linear(a, stream);
 }
 
 hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags, float act_scale,
