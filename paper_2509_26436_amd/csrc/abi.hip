@@ -343,7 +343,7 @@ quartz_status quartz_w4a4_linear_static(const uint8_t* codes, const uint8_t* fla
         (workspace && !aligned16(workspace)))
         return QUARTZ_ERR_ALIGN;
     const quartz::GemmSchedule sch =
-        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+        quartz::linear_schedule(M, N, K, quartz::linear_resident_blocks(), workspace != nullptr);
     if (sch.blocks <= 0)
         return QUARTZ_ERR_HIP;
     if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)

@@ -143,6 +143,7 @@ struct GemmLaunch {
 // One output mode each (w4a4_gemm_<mode>.hip).
 hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_linear_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);

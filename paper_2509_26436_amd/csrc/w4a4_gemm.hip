@@ -123,7 +123,8 @@ hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags,
     GemmLaunch a{codes, flags, nullptr, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
                  epilogue, sch, nullptr, nullptr, QuantOut{}, act_scale};
     split_workspace(sch, workspace, a.counters, a.slots);
-    return launch_gemm_static(a, stream);
+    // the kernel of w4a4_linear.hip (schedule from linear_schedule)
+    return launch_linear_static(a, stream);
 }
 
 hipError_t launch_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,

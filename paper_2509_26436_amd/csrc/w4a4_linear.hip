@@ -41,12 +41,19 @@ constexpr int kLinPanels = LBN / kPanel;    // weight panels per tile
 static_assert(kLinStages == kPipelineStages, "segments are padded to whole rounds of the stages");
 static_assert(64 * kLinDecodeWaves == 2 * LBM && 64 * kLinDecodeWaves == LBN, "decode roles");
 
-template <int GS, bool GELU, bool SPLIT>
+// STATIC: the LDM setting (one per-tensor activation scale, per-channel
+// weight scales): no per-group scales, so the fp8 MFMAs accumulate the exact
+// integer sum in place and the output code applies act_scale * s_w[n].  With
+// no dequantization pipeline the math waves have the registers to take their
+// weight words straight from global memory (a ring three groups deep), and
+// only the decoded activations pass through LDS.
+template <int GS, bool GELU, bool SPLIT, bool STATIC>
 __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int64_t M, int64_t N, int64_t K,
-    int64_t ldy, GemmSchedule sch, uint32_t* __restrict__ counters, float* __restrict__ slots)
+    int64_t ldy, GemmSchedule sch, uint32_t* __restrict__ counters, float* __restrict__ slots,
+    float act_scale)
 {
     // decoded activations, stage-major; row r's 16-byte chunk c at swz(r, c)
     __shared__ __attribute__((aligned(16))) uint8_t As[kLinStages][LBM * 64];
@@ -122,15 +129,17 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
             const int64_t prow = (int64_t)g * M + m0;
             const Rsrc ra = make_rsrc(codes + prow * 32, rows * 32u);
             const Rsrc rf = make_rsrc(flags + prow * FB, rows * (uint32_t)FB);
-            const Rsrc rs = make_rsrc(scales + prow, rows * 2u);
+            const Rsrc rs = make_rsrc(STATIC ? nullptr : scales + prow, STATIC ? 0u : rows * 2u);
             const Rsrc rb = make_rsrc(w_packed + (panel0 * G + g) * kChunkBytes, b_bytes);
             r.a = __builtin_bit_cast(
                 uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)((uint32_t)dr * 32u + ah * 16u), 0, 0));
             r.f = load_half_flags<GS>(rf, (uint32_t)dr * FB, ah);
-            r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, dr * 2, 0, 0);
-            r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
-            r.b0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
-            r.b1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off + 16, 0, 0));
+            if constexpr (!STATIC) {
+                r.sa = __builtin_amdgcn_raw_buffer_load_b16(rs, dr * 2, 0, 0);
+                r.sw = __builtin_amdgcn_raw_buffer_load_b16(rb, (int)sw_off, 0, 0);
+                r.b0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off, 0, 0));
+                r.b1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, (int)b_off + 16, 0, 0));
+            }
             if (!fdone && ++fg == fend) {
                 if (cursor_next(fresh_schedule(), blk, fc)) {
                     fg = fc.sg.g0;
@@ -160,11 +169,13 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
             }
             *reinterpret_cast<uint4*>(As[buf] + swz(dr, 2 * ah)) = make_uint4(o[0].x, o[0].y, o[1].x, o[1].y);
             *reinterpret_cast<uint4*>(As[buf] + swz(dr, 2 * ah + 1)) = make_uint4(o[2].x, o[2].y, o[3].x, o[3].y);
-            *reinterpret_cast<uint4*>(Bs[buf] + d * 16) = r.b0;
-            *reinterpret_cast<uint4*>(Bs[buf] + LBN * 16 + d * 16) = r.b1;
-            if (ah == 0)
-                sas[buf][dr] = r.sa;
-            sws[buf][d] = r.sw;
+            if constexpr (!STATIC) {
+                *reinterpret_cast<uint4*>(Bs[buf] + d * 16) = r.b0;
+                *reinterpret_cast<uint4*>(Bs[buf] + LBN * 16 + d * 16) = r.b1;
+                if (ah == 0)
+                    sas[buf][dr] = r.sa;
+                sws[buf][d] = r.sw;
+            }
         };
 
         // The decode of each group gates the math waves two steps later: these
@@ -174,7 +185,7 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         constexpr int kRing = 2 * kLinStages;
         Raw ring[kRing];
         __builtin_amdgcn_s_setprio(2);
-        if (d < 8 * kLinStages) {
+        if (!STATIC && d < 8 * kLinStages) {
             sas[d >> 3][LBM + (d & 7)] = 0;
             sws[d >> 3][LBN + (d & 7)] = 0;
         }
@@ -238,10 +249,40 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         return v8i{(int)w0.x, (int)w0.y, (int)w1.x, (int)w1.y, (int)w2.x, (int)w2.y, (int)w3.x, (int)w3.y};
     };
 
+    // ---- STATIC: the weight words straight from global memory, in a ring of
+    // three groups (this lane's 16 bytes of each of the wave's two column
+    // tiles) fetched by a cursor of its own that walks the same segments
+    // group by group; ring0 is the group being multiplied.
+    struct WRaw {
+        uint4 c0, c1;
+    };
+    WRaw ring0, ring1, ring2;
+    GemmCursor bcur;
+    int bg = 0;
+    bool bdone = false;
+    int64_t bpanel = 0;
+    auto bfetch = [&](WRaw& r) {
+        const int g = min(bg, bcur.sg.g1 - 1);
+        const Rsrc rb = make_rsrc(w_packed + (bpanel * G + g) * kChunkBytes,
+                                  bpanel < panels ? (uint32_t)kChunkCodeBytes : 0u);
+        const int off = (int)((uint32_t)l32 * 32u + (uint32_t)khalf * 16u);
+        r.c0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, off, 0, 0));
+        r.c1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rb, off + 1024, 0, 0));
+        if (!bdone && ++bg == bcur.sg.g1) {
+            if (cursor_next(fresh_schedule(), blk, bcur)) {
+                bg = bcur.sg.g0;
+                bpanel = (int64_t)bcur.tn * kLinPanels + wn;
+            } else {
+                bdone = true;
+            }
+        }
+    };
+
     v16f acc[TM][TN];
-    v8i bf, af[TM];
+    v8i bf, bf1, af[TM];
     _Float16 sa_h[TM], sw_h[TN];
     uint4 wraw;
+    auto load_af = [&](int i, int buf) { af[i] = frag_at(As[buf], a_lo, a_hi, i * 32); };
     auto load_a = [&](int i, int buf) {
         af[i] = frag_at(As[buf], a_lo, a_hi, i * 32);
         sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][khalf ? LBM : wm * WM + i * 32 + l32]);
@@ -289,8 +330,38 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     // column 0's products are issued; the next group's operands (LDS stage
     // nb) are read after their last use here, unless this is a segment's
     // last group.
+    // STATIC: the four fp8 products of a group accumulate in place; column
+    // 1's operand is decoded while column 0's products run, the next group's
+    // column 0 once the ring has advanced (issuing all four products back to
+    // back, with both columns decoded a group ahead, was slower: the wave
+    // then stalls on the busy matrix unit with its loads and decode behind
+    // the products).
+    auto compute_static = [&](int nb, auto last) {
+        constexpr bool LAST = decltype(last)::value;
+        auto mf = [&](int i, const v8i& b, v16f& c) {
+            c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], b, c, 0, 0, 0, 0, 0, 0);
+        };
+        mf(0, bf, acc[0][0]);
+        mf(1, bf, acc[1][0]);
+        bf1 = decode_w(ring0.c1);
+        mf(0, bf1, acc[0][1]);
+        if (!LAST)
+            load_af(0, nb);
+        mf(1, bf1, acc[1][1]);
+        if (!LAST)
+            load_af(1, nb);
+        ring0 = ring1;
+        ring1 = ring2;
+        bfetch(ring2);
+        bf = decode_w(ring0.c0);
+    };
     auto compute = [&](int cb, int nb, auto last) {
         constexpr bool LAST = decltype(last)::value;
+        if constexpr (STATIC) {
+            (void)cb;
+            compute_static(nb, last);
+            return;
+        }
         p_next = mfma_p(0);
         __builtin_amdgcn_sched_barrier(0);
         fma_tile(TM - 1, TN - 1, p_last, s_last);
@@ -353,13 +424,25 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     };
 
     GemmCursor cur;
-    uint16_t bias_bits[TN];
+    // this lane's bias values of the current tile (bf16 bits), loaded when the
+    // segment starts so the output code does not wait for them; STATIC: also
+    // the channel scales s_w[n] (fp16 bits, from the scale slot of group 0 of
+    // the wave's panel, where the per-channel pack keeps them)
+    uint16_t bias_bits[TN], cscale_bits[TN];
     auto load_bias = [&] {
         const Rsrc rb = make_rsrc(bias, bias ? (uint32_t)(N * 2) : 0u);
 #pragma unroll
         for (int j = 0; j < TN; ++j)
             bias_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(
                 rb, (int)(((int64_t)cur.tn * LBN + wn * WN + j * 32 + l32) * 2), 0, 0);
+        if constexpr (STATIC) {
+            const int64_t panel = (int64_t)cur.tn * kLinPanels + wn;
+            const Rsrc rs = make_rsrc(w_packed + panel * G * kChunkBytes + kChunkCodeBytes,
+                                      panel < panels ? (uint32_t)(kPanel * 2) : 0u);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                cscale_bits[j] = __builtin_amdgcn_raw_buffer_load_b16(rs, (j * 32 + l32) * 2, 0, 0);
+        }
     };
 
     // ---- output: acc is in units of the weight operands (2^-9), so the
@@ -373,10 +456,15 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     auto store_tile = [&] {
         const int64_t row_base = (int64_t)cur.tm * LBM + wm * WM;
         const int64_t col_base = (int64_t)cur.tn * LBN + wn * WN;
-        float b[TN];
+        float b[TN], cs[TN];
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j) {
             b[j] = __uint_as_float((uint32_t)bias_bits[j] << 16);
+            // STATIC: act_scale * s_w[n] times the 2^9 of the weight unit
+            cs[j] = STATIC ? act_scale * (float)__builtin_bit_cast(_Float16, cscale_bits[j]) *
+                                 kWeightUnitInv
+                           : kWeightUnitInv;
+        }
         const int64_t rows_in = max((int64_t)0, min(M - row_base, (int64_t)WM));
         const uint32_t row_bytes = (uint32_t)ldy * 2u;
         const Rsrc out_r = make_rsrc(y + row_base * ldy + col_base, (uint32_t)rows_in * row_bytes);
@@ -387,8 +475,8 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float v0 = fmaf(acc[i][0][r], kWeightUnitInv, b[0]);
-                float v1 = fmaf(acc[i][1][r], kWeightUnitInv, b[1]);
+                float v0 = fmaf(acc[i][0][r], cs[0], b[0]);
+                float v1 = fmaf(acc[i][1][r], cs[1], b[1]);
                 if constexpr (GELU) {
                     v0 = gelu_tanh(v0);
                     v1 = gelu_tanh(v1);
@@ -524,23 +612,41 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 
     if (!cursor_begin(fresh_schedule(), blk, cur))
         return;
+    if constexpr (STATIC) {
+        // the weight fetch cursor starts on the same segment; the ring then
+        // runs continuously, three groups ahead of the multiplication
+        set_fragment_indices();
+        bcur = cur;
+        bg = cur.sg.g0;
+        bpanel = (int64_t)cur.tn * kLinPanels + wn;
+        bfetch(ring0);
+        bfetch(ring1);
+        bfetch(ring2);
+        bf = decode_w(ring0.c0);
+    }
     lds_sync();
     for (;;) {
         const int L = cur.sg.g1 - cur.sg.g0;
         set_fragment_indices();
         load_bias();
         reset_tile();
-        load_a(0, 0);
-        load_a(1, 0);
-        bf = decode_w(raw_w(0, 0));
-        wraw = raw_w(1, 0);
-        load_sw(0, 0);
+        if constexpr (STATIC) {
+            load_af(0, 0);
+            load_af(1, 0);
+        } else {
+            load_a(0, 0);
+            load_a(1, 0);
+            bf = decode_w(raw_w(0, 0));
+            wraw = raw_w(1, 0);
+            load_sw(0, 0);
+        }
         run_groups(L - 1);
         compute((L - 1) % kLinStages, 0, std::integral_constant<bool, true>());
         math_barrier();
         for (int p = L; p < padded_steps(L); ++p)
             math_barrier();
-        fma_tile(TM - 1, TN - 1, p_last, s_last);
+        if constexpr (!STATIC)
+            fma_tile(TM - 1, TN - 1, p_last, s_last);
         set_fragment_indices();
         if (!SPLIT || cur.sg.sk_tile < 0 || finish_partial())
             store_tile();
@@ -571,7 +677,7 @@ int linear_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_linear_kernel<16, false, true>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_linear_kernel<16, false, true, false>),
             kLinThreads, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
@@ -580,13 +686,14 @@ int linear_resident_blocks()
     return n;
 }
 
-hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream)
+template <bool STATIC>
+hipError_t launch_linear_mode(const GemmLaunch& a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.sch.blocks), block(kLinThreads);
     auto go = [&](auto gs, auto gelu, auto split) {
-        w4a4_linear_kernel<decltype(gs)::value, decltype(gelu)::value, decltype(split)::value>
+        w4a4_linear_kernel<decltype(gs)::value, decltype(gelu)::value, decltype(split)::value, STATIC>
             <<<grid, block, 0, stream>>>(a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.M,
-                                         a.N, a.K, a.ldy, a.sch, a.counters, a.slots);
+                                         a.N, a.K, a.ldy, a.sch, a.counters, a.slots, a.act_scale);
     };
     auto with_split = [&](auto gs, auto gelu) {
         if (a.sch.sk_tiles > 0)
@@ -615,6 +722,16 @@ hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream)
         break;
     }
     return hipGetLastError();
+}
+
+hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream)
+{
+    return launch_linear_mode<false>(a, stream);
+}
+
+hipError_t launch_linear_static(const GemmLaunch& a, hipStream_t stream)
+{
+    return launch_linear_mode<true>(a, stream);
 }
 
 }  // namespace quartz
