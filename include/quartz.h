@@ -478,7 +478,10 @@ quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const
  * schedule for a persistent grid of at most `blocks` workgroups (the entry
  * points use the device's compute-unit count), with (split = 1, as
  * quartz_w4a4_linear_ws) or without (split = 0, as quartz_w4a4_linear) tiles
- * cut along K.
+ * cut along K, for tiles of 128 x 256 (tiles = 0: quartz_w4a4_linear and its
+ * variants, quartz_w4a4_linear_static) or of 256 x 128 (tiles = 1: the
+ * quantizing epilogue, the asymmetric mode, the convolutions and the
+ * attention products).
  *   schedule  host int32[10]: tiles_n, groups, split, blocks, whole tiles of
  *             workgroup 0, sk_first, sk_tiles, sk_blocks, sk_q, sk_r.
  *   segments  host int32[capacity][10], one row per (workgroup, segment):
@@ -487,11 +490,12 @@ quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const
  *             sharing the tile (or -1), and the slot the finishing workgroup
  *             reads for this workgroup's share (or -1).
  * Returns the number of segments (rows past `capacity` are not written), -1
- * for invalid arguments, -2 if the schedule is inconsistent (a library bug).
+ * for invalid arguments (tiles not 0 or 1 included), -2 if the schedule is
+ * inconsistent (a library bug).
  */
 int64_t quartz_w4a4_linear_schedule(int64_t M, int64_t N, int64_t K, int32_t blocks,
-                                    int32_t split, int32_t* schedule, int32_t* segments,
-                                    int64_t capacity);
+                                    int32_t split, int32_t tiles, int32_t* schedule,
+                                    int32_t* segments, int64_t capacity);
 
 /* Static, NUL-terminated description of a status code (host memory). */
 const char* quartz_status_string(quartz_status s);

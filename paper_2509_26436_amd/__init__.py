@@ -126,7 +126,7 @@ def load() -> ctypes.CDLL:
     lib.quartz_w4a4_conv3x3_static.argtypes = [P, P, F32, P, P, P, I64, I64, I64, I64, I64, I64,
                                                I32, I32, P, SZ, P]
     lib.quartz_w4a4_conv3x3_static.restype = I32
-    lib.quartz_w4a4_linear_schedule.argtypes = [I64, I64, I64, I32, I32, P, P, I64]
+    lib.quartz_w4a4_linear_schedule.argtypes = [I64, I64, I64, I32, I32, I32, P, P, I64]
     lib.quartz_w4a4_linear_schedule.restype = I64
     lib.quartz_unpack_weight.argtypes = [P, I64, I64, I32, P, P]
     lib.quartz_unpack_weight.restype = I32
@@ -254,8 +254,8 @@ def quartz_w4a4_conv3x3_static(codes, flags, act_scale, w_packed, bias, y, image
                                              workspace_bytes, stream)
 
 
-def quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments, capacity) -> int:
-    return int(load().quartz_w4a4_linear_schedule(M, N, K, blocks, split, schedule, segments,
+def quartz_w4a4_linear_schedule(M, N, K, blocks, split, tiles, schedule, segments, capacity) -> int:
+    return int(load().quartz_w4a4_linear_schedule(M, N, K, blocks, split, tiles, schedule, segments,
                                                   capacity))
 
 
@@ -638,16 +638,18 @@ SEGMENT_FIELDS = ("block", "index", "tile", "g0", "g1", "sk_tile", "slot", "b_fi
                   "finisher_slot")
 
 
-def linear_schedule(M: int, N: int, K: int, blocks: int, split: bool = True):
+def linear_schedule(M: int, N: int, K: int, blocks: int, split: bool = True, tiles: int = 0):
     """Host-side GEMM work schedule for a persistent grid of at most ``blocks``
-    workgroups: (dict of SCHEDULE_FIELDS, int32 numpy array [segments, len(SEGMENT_FIELDS)])."""
+    workgroups, tiles of 128 x 256 (``tiles=0``, the linear layer) or 256 x 128
+    (``tiles=1``, the other GEMM entry points): (dict of SCHEDULE_FIELDS, int32
+    numpy array [segments, len(SEGMENT_FIELDS)])."""
     import numpy as np
     sched = np.zeros(len(SCHEDULE_FIELDS), dtype=np.int32)
-    n = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), sched.ctypes.data, None, 0)
+    n = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), tiles, sched.ctypes.data, None, 0)
     if n < 0:
         raise ValueError(f"schedule error {n}")
     seg = np.zeros((max(n, 1), len(SEGMENT_FIELDS)), dtype=np.int32)
-    n2 = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), sched.ctypes.data,
+    n2 = quartz_w4a4_linear_schedule(M, N, K, blocks, int(split), tiles, sched.ctypes.data,
                                      seg.ctypes.data, n)
     assert n2 == n
     return dict(zip(SCHEDULE_FIELDS, (int(v) for v in sched))), seg[:n]

@@ -410,13 +410,14 @@ quartz_status quartz_w4a4_linear_quantize(const uint8_t* codes, const uint8_t* f
 }
 
 int64_t quartz_w4a4_linear_schedule(int64_t M, int64_t N, int64_t K, int32_t blocks,
-                                    int32_t split, int32_t* schedule, int32_t* segments,
-                                    int64_t capacity)
+                                    int32_t split, int32_t tiles, int32_t* schedule,
+                                    int32_t* segments, int64_t capacity)
 {
     if (M <= 0 || N <= 0 || K <= 0 || !size_ok(M, K) || !size_ok(N, K) || blocks <= 0 ||
-        !schedule || capacity < 0 || (capacity > 0 && !segments))
+        !schedule || capacity < 0 || (capacity > 0 && !segments) || (tiles != 0 && tiles != 1))
         return -1;
-    const quartz::GemmSchedule s = quartz::gemm_schedule(M, N, K, blocks, split != 0);
+    const quartz::GemmSchedule s = tiles == 0 ? quartz::linear_schedule(M, N, K, blocks, split != 0)
+                                              : quartz::gemm_schedule(M, N, K, blocks, split != 0);
     if (s.blocks <= 0)
         return -1;
     const int32_t fields[10] = {s.tiles_n, s.groups, s.sk_tiles > 0 ? 1 : 0, s.blocks,

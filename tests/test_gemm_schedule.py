@@ -3,7 +3,9 @@ stream-K split of the last rounds of tiles), through the library's own
 schedule routine: the same header code the kernel runs.  No GPU needed.  The
 routine also walks the kernel's incremental cursor for every workgroup and
 fails (-2) unless it yields exactly the segments checked here, with a
-pipeline step count that covers them.
+pipeline step count that covers them.  Both tile shapes are covered: 128 x
+256 (tiles = 0, the linear layer's kernel) and 256 x 128 (tiles = 1, the
+kernel template of the other GEMM entry points).
 
 For every shape and persistent grid size, with and without the split: every (tile, 64-group) unit of the
 output is computed exactly once; whole-tile rounds use whole tiles; the
@@ -21,7 +23,7 @@ import pytest
 
 import paper_2509_26436_amd as q
 
-BM, BN = 256, 128
+TILE_SHAPES = {0: (128, 256), 1: (256, 128)}
 
 SHAPES = [
     # (M, K, N): FLUX.1 joint block, batched FLUX MLP, PixArt, SDXL im2col, single layer
@@ -36,13 +38,15 @@ SHAPES = [
 BLOCKS = [256, 304, 80, 32, 7, 1]
 
 
-def _tiles(M, N):
+def _tiles(M, N, tiles):
+    BM, BN = TILE_SHAPES[tiles]
     return -(-M // BM) * -(-N // BN)
 
 
-def _check(M, K, N, blocks, split=True):
-    s, seg = q.linear_schedule(M, N, K, blocks, split)
-    T, G = _tiles(M, N), K // 64
+def _check(M, K, N, blocks, split=True, tiles=0):
+    s, seg = q.linear_schedule(M, N, K, blocks, split, tiles)
+    BN = TILE_SHAPES[tiles][1]
+    T, G = _tiles(M, N, tiles), K // 64
     assert s["groups"] == G
     assert 1 <= s["blocks"] <= blocks and s["sk_blocks"] <= s["blocks"]
     assert s["split"] or s["blocks"] <= T
@@ -114,45 +118,51 @@ def _check(M, K, N, blocks, split=True):
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("blocks", BLOCKS)
 @pytest.mark.parametrize("split", [True, False])
-def test_schedule_invariants(shape, blocks, split):
+@pytest.mark.parametrize("tiles", [0, 1])
+def test_schedule_invariants(shape, blocks, split, tiles):
     M, K, N = shape
-    _check(M, K, N, blocks, split)
+    _check(M, K, N, blocks, split, tiles)
 
 
-def test_schedule_choices_on_256_compute_units():
+@pytest.mark.parametrize("tiles", [0, 1])
+def test_schedule_choices_on_256_compute_units(tiles):
     # Split where the idle part of the last round of whole tiles is worth at
     # least 16 groups per workgroup: FLUX qkv (1296 tiles = 5.06 rounds of 48
     # groups: 45 groups saved) and fc2 (432 tiles of 192 groups: 60), not out
     # (432 tiles of 48 groups: 15) nor fc1 (1728 tiles = 6.75 rounds: 12); a
     # multiple of 256 tiles needs no split
-    s = _check(4608, 3072, 9216, 256)
+    # (both tile shapes give these layers the same tile counts)
+    s = _check(4608, 3072, 9216, 256, tiles=tiles)
     assert s["split"] == 1 and (s["dp_tiles_b0"], s["sk_tiles"]) == (4, 272)
-    assert _check(4608, 3072, 3072, 256)["split"] == 0
-    assert _check(4608, 12288, 3072, 256)["split"] == 1
-    assert _check(4608, 3072, 12288, 256)["split"] == 0
-    assert _check(18432, 3072, 12288, 256)["split"] == 0      # 6912 tiles = 27 rounds
+    assert _check(4608, 3072, 3072, 256, tiles=tiles)["split"] == 0
+    assert _check(4608, 12288, 3072, 256, tiles=tiles)["split"] == 1
+    assert _check(4608, 3072, 12288, 256, tiles=tiles)["split"] == 0
+    assert _check(18432, 3072, 12288, 256, tiles=tiles)["split"] == 0   # 6912 tiles = 27 rounds
     # without a workspace nothing is split: 1296 tiles over 256 workgroups
-    s = _check(4608, 3072, 9216, 256, split=False)
+    s = _check(4608, 3072, 9216, 256, split=False, tiles=tiles)
     assert s["split"] == 0 and s["blocks"] == 256 and s["dp_tiles_b0"] == 6
     # fewer tiles than workgroups: at least 16 groups per workgroup and at
     # least 1/8 of a tile's groups (so about 8 workgroups share a tile at
     # most), and no split at all when that leaves under two workgroups per
-    # tile: the single 256 x 1152 x 1152 linear (9 tiles of 18 groups) stays
-    # whole, as measured faster (20 against 36 us)
-    s = _check(256, 1152, 1152, 256)
-    assert s["split"] == 0 and s["blocks"] == 9
-    s = _check(160, 4608, 448, 256)
-    assert s["split"] == 1 and s["sk_q"] >= 16 and s["sk_blocks"] >= 2 * 4
-    s = _check(257, 12288, 129, 256)
+    # tile: the single 256 x 1152 x 1152 linear (10 tiles of 128 x 256 or 9 of
+    # 256 x 128, 18 groups each) stays whole, as measured faster (20 against
+    # 36 us with the 256 x 128 tiles)
+    T1 = _tiles(256, 1152, tiles)
+    s = _check(256, 1152, 1152, 256, tiles=tiles)
+    assert s["split"] == 0 and s["blocks"] == T1
+    s = _check(160, 4608, 448, 256, tiles=tiles)
+    assert s["split"] == 1 and s["sk_q"] >= 16 and s["sk_blocks"] >= 2 * _tiles(160, 448, tiles)
+    s = _check(257, 12288, 129, 256, tiles=tiles)
     assert s["split"] == 1 and s["sk_q"] >= 192 // 8
-    s = _check(256, 1152, 1152, 256, split=False)
-    assert s["split"] == 0 and s["blocks"] == 9
+    s = _check(256, 1152, 1152, 256, split=False, tiles=tiles)
+    assert s["split"] == 0 and s["blocks"] == T1
 
 
 def test_schedule_rejects_bad_arguments():
     import numpy as np
     sched = np.zeros(10, dtype=np.int32)
-    assert q.quartz_w4a4_linear_schedule(0, 64, 64, 256, 1, sched.ctypes.data, None, 0) == -1
-    assert q.quartz_w4a4_linear_schedule(64, 64, 100, 256, 1, sched.ctypes.data, None, 0) == -1
-    assert q.quartz_w4a4_linear_schedule(64, 64, 64, 256, 1, None, None, 0) == -1
-    assert q.quartz_w4a4_linear_schedule(64, 64, 64, 0, 1, sched.ctypes.data, None, 0) == -1
+    assert q.quartz_w4a4_linear_schedule(0, 64, 64, 256, 1, 0, sched.ctypes.data, None, 0) == -1
+    assert q.quartz_w4a4_linear_schedule(64, 64, 100, 256, 1, 0, sched.ctypes.data, None, 0) == -1
+    assert q.quartz_w4a4_linear_schedule(64, 64, 64, 256, 1, 0, None, None, 0) == -1
+    assert q.quartz_w4a4_linear_schedule(64, 64, 64, 0, 1, 0, sched.ctypes.data, None, 0) == -1
+    assert q.quartz_w4a4_linear_schedule(64, 64, 64, 256, 1, 2, sched.ctypes.data, None, 0) == -1

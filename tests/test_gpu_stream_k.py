@@ -57,13 +57,13 @@ def _schedule_of(M, N, K):
 
 
 CASES = [
-    # (cfg, layer, M, N, gs, epilogue, bias, ldy_pad)
+    # (cfg, layer, M, N, gs, epilogue, bias, ldy_pad); tiles of 128 x 256
     (2, 3, 160, 448, 16, 0, True, 0),      # 4 tiles x 72 groups over 18 workgroups
-    (2, 3, 70, 130, 16, 1, False, 0),      # 2 tiles x 72 groups over 9 workgroups, GELU, no bias
+    (2, 3, 70, 130, 16, 1, False, 0),      # 1 tile x 72 groups over 4 workgroups, GELU, no bias
     (3, 0, 300, 200, 8, 0, True, 6),       # ragged rows and columns, strided output
-    (3, 3, 257, 129, 32, 0, True, 0),      # K = 12288: 4 tiles x 192 groups
-    (5, 0, 513, 320, 64, 1, True, 0),      # 9 tiles, GELU
-    (2, 3, 64, 1152, 16, 0, True, 0),      # one tile row, 9 tiles x 72 groups
+    (3, 3, 257, 129, 32, 0, True, 0),      # K = 12288: 3 tiles x 192 groups
+    (5, 0, 513, 320, 64, 1, True, 0),      # 10 tiles, GELU
+    (2, 3, 64, 1152, 16, 0, True, 0),      # one tile row, 5 tiles x 72 groups
 ]
 
 
