@@ -280,15 +280,21 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 
     v16f acc[TM][TN];
     v8i bf, bf1, af[TM];
-    _Float16 sa_h[TM], sw_h[TN];
+    // operands of the scale outer-product MFMA (fp16 32x32x8, k = 0 the only
+    // non-zero one): dword 0 holds the scale in its low half (a zero-extending
+    // 16-bit LDS load; the upper half-wave, k = 4..7, reads the zero pad),
+    // dword 1 is zero once and never written again, so refilling an operand
+    // is one LDS load and no vector instruction
+    typedef int v2i __attribute__((ext_vector_type(2)));
+    v2i sa_op[TM], sw_op[TN];
     uint4 wraw;
     auto load_af = [&](int i, int buf) { af[i] = frag_at(As[buf], a_lo, a_hi, i * 32); };
     auto load_a = [&](int i, int buf) {
         af[i] = frag_at(As[buf], a_lo, a_hi, i * 32);
-        sa_h[i] = __builtin_bit_cast(_Float16, sas[buf][khalf ? LBM : wm * WM + i * 32 + l32]);
+        sa_op[i][0] = (int)sas[buf][khalf ? LBM : wm * WM + i * 32 + l32];
     };
     auto load_sw = [&](int j, int buf) {
-        sw_h[j] = __builtin_bit_cast(_Float16, sws[buf][khalf ? LBN : wn * WN + j * 32 + l32]);
+        sw_op[j][0] = (int)sws[buf][khalf ? LBN : wn * WN + j * 32 + l32];
     };
 
     v16f p_next, p_last, s_last;
@@ -304,13 +310,13 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         fma_rows(i, j, p, sc, 8);
     };
     // the 32 x 32 tile of scale products: fp16 MFMA with one non-zero k
+    // (32x32x8 runs at the rate of 32x32x16, 15-17 ns, with operands half as
+    // wide)
     auto scale_tile = [&](int i, int j) {
-        typedef _Float16 v8h __attribute__((ext_vector_type(8)));
-        v8h a = {}, b = {};
-        a[0] = sa_h[i];
-        b[0] = sw_h[j];
+        typedef _Float16 v4h __attribute__((ext_vector_type(4)));
         __builtin_amdgcn_s_setprio(3);
-        const v16f sc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, zero, 0, 0, 0);
+        const v16f sc = __builtin_amdgcn_mfma_f32_32x32x8f16(
+            __builtin_bit_cast(v4h, sa_op[i]), __builtin_bit_cast(v4h, sw_op[j]), zero, 0, 0, 0);
         __builtin_amdgcn_s_setprio(0);
         return sc;
     };
@@ -323,8 +329,8 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 
     // One group from LDS stage cb, tiles in the order (0,0) (1,0) (0,1) (1,1),
     // the fp8 product issued one step ahead of the FMAs that use it (see the
-    // template).  On entry af[] and sa_h[] hold this group's activation
-    // operands, bf and sw_h[0] its column-0 weight operands, wraw its column-1
+    // template).  On entry af[] and sa_op[] hold this group's activation
+    // operands, bf and sw_op[0] its column-0 weight operands, wraw its column-1
     // weight words (read a step ahead, so the LDS latency is hidden: each
     // read goes out one step before its decode).  Column 1 is decoded once
     // column 0's products are issued; the next group's operands (LDS stage
@@ -612,6 +618,12 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 
     if (!cursor_begin(fresh_schedule(), blk, cur))
         return;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+        sa_op[i] = v2i{0, 0};
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+        sw_op[j] = v2i{0, 0};
     if constexpr (STATIC) {
         // the weight fetch cursor starts on the same segment; the ring then
         // runs continuously, three groups ahead of the multiplication
