@@ -237,12 +237,9 @@ static quartz_status linear_impl(const uint8_t* codes, const uint8_t* flags,
         (qout && (!aligned16(qout->codes) || !aligned16(qout->flags) ||
                   !aligned16(qout->scales) || (qout->zeros && !aligned16(qout->zeros)))))
         return QUARTZ_ERR_ALIGN;
-    // a bf16 output runs the linear kernel (tiles of 128 x 256), a quantized
-    // one the template (256 x 128)
-    const bool split = workspace != nullptr || use_scratch;
-    const quartz::GemmSchedule sch =
-        qout ? quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), split)
-             : quartz::linear_schedule(M, N, K, quartz::linear_resident_blocks(), split);
+    // the linear kernel (tiles of 128 x 256), bf16 or quantized output
+    const quartz::GemmSchedule sch = quartz::linear_schedule(
+        M, N, K, quartz::linear_resident_blocks(), workspace != nullptr || use_scratch);
     if (sch.blocks <= 0)
         return QUARTZ_ERR_HIP;          // no usable device
     if (use_scratch) {
@@ -281,8 +278,9 @@ size_t quartz_w4a4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int32
 {
     if (group_size != 64 || M <= 0 || N <= 0 || K <= 0 || !size_ok(M, K) || !size_ok(N, K))
         return 0;
-    // the larger of the two kernels' needs: the same workspace serves the
-    // bf16 output and the quantized one
+    // the larger of the two kernels' needs: the same size query serves the
+    // linear layer (tiles of 128 x 256) and the entry points that run the
+    // template (256 x 128: asymmetric mode, convolution)
     return std::max(
         quartz::gemm_workspace_bytes(
             quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), true)),

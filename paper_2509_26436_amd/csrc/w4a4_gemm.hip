@@ -107,9 +107,9 @@ hipError_t launch_w4a4_linear(const uint8_t* codes, const uint8_t* flags,
     GemmLaunch a{codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
                  epilogue, sch, nullptr, nullptr, qout, 0.0f};
     split_workspace(sch, workspace, a.counters, a.slots);
-    // the bf16 output runs the 128 x 256 kernel of w4a4_linear.hip (its
-    // schedule from linear_schedule), the quantized output the template
-    return qout.codes ? launch_gemm_quant(a, stream) : launch_linear(a, stream);
+    // the kernel of w4a4_linear.hip (tiles of 128 x 256, schedule from
+    // linear_schedule), bf16 or quantized output
+    return launch_linear(a, stream);
 }
 
 hipError_t launch_w4a4_linear_static(const uint8_t* codes, const uint8_t* flags, float act_scale,

@@ -188,6 +188,150 @@ typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
 typedef __attribute__((address_space(3))) v4u lds_v4u;
 
+// ---- output quantized for the next layer: one math wave's 64 x 64 tile (2 x 2
+// MFMA tiles of 32 x 32: lane l holds column l % 32, rows 8 (r/4) + 4 khalf
+// + r%4 of register r) becomes the bf16 values the plain epilogue would store,
+// fmaf(acc, cs[j], b[j]) then the optional GELU, run through the activation
+// quantizer with this layer's N as the next layer's K.  The wave's 64 columns
+// are one 64-group of each of its 64 rows (N % 64 == 0).  The bf16 tile goes
+// through the wave's own LDS region tb (8 KB) and comes back one row per lane,
+// so the group maximum, the subgroup ORs and the code packing are in-lane
+// arithmetic (lzs_device.h).  Row r's 16-byte chunk c (its elements 8c..8c+7,
+// one 8-element block) sits at chunk c ^ ((r >> 1) & 7): a read of one chunk
+// per row by 16 consecutive lanes (8 chunk positions x 2 row parities) then
+// covers all 64 banks.  The row is read once; per block the |q| pairs go back
+// over the block's chunk (so they need no registers while the subgroup FLAGs
+// are formed) and are read again for the code words.
+// Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
+// [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside the
+// buffer ranges and are dropped.
+template <bool GELU>
+__device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const float (&cs)[2],
+                                                  const float (&b)[2], lds_u8* tb, int lane,
+                                                  int64_t row_base, int64_t col_base, int64_t M,
+                                                  int64_t N, const QuantOut& qout)
+{
+    if (col_base >= N)
+        return;                              // wave-uniform
+    const uint32_t lane2 = (uint32_t)lane * 2u;
+    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+    typedef float f2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float v0 = fmaf(out[i][0][r], cs[0], b[0]);
+            float v1 = fmaf(out[i][1][r], cs[1], b[1]);
+            if constexpr (GELU) {
+                v0 = gelu_tanh(v0);
+                v1 = gelu_tanh(v1);
+            }
+            // after the swap lane l holds column l of rows row0, row0 + 4
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
+                                                             __float_as_uint(v1), false, false);
+            const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
+            const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
+            const int row0 = i * 32 + 8 * (r >> 2) + (r & 3);
+            const uint32_t x0 = (uint32_t)((row0 >> 1) & 7) << 4;
+            const uint32_t x1 = (uint32_t)(((row0 + 4) >> 1) & 7) << 4;
+            *(lds_u16*)(tb + row0 * 128 + (lane2 ^ x0)) = (uint16_t)pk;
+            *(lds_u16*)(tb + (row0 + 4) * 128 + (lane2 ^ x1)) = (uint16_t)(pk >> 16);
+        }
+    }
+    // the wave reads back only what it wrote itself: LDS order within the
+    // wave suffices, the clobber keeps the compiler's order
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    lds_u8* const row = tb + lane * 128;
+    const uint32_t rx = (uint32_t)((lane >> 1) & 7) << 4;
+    auto chunk = [&](int c) { return (lds_v4u*)(row + (((uint32_t)c << 4) ^ rx)); };
+    uint32_t X[8][4];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const v4u v = *chunk(c);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            X[c][k] = v[k];
+    }
+    // max |x| on the bf16 magnitude bits (their unsigned order is the order
+    // of |x|), two values per instruction
+    lzs_us2 m2 = {0, 0};
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(lzs_us2, X[c][k] & 0x7FFF7FFFu));
+    const uint32_t am = max((uint32_t)m2[0], (uint32_t)m2[1]);
+    const GroupScale gsc = group_scale(__uint_as_float(am << 16));
+    // |q| pairs of each 8-element block (written back over its chunk), their
+    // OR and the sign bits; one branch for the wave
+    uint32_t S[8], m8[8];
+    auto pairs = [&](auto clamp) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            uint32_t p[4];
+            mag_pairs8_t<decltype(clamp)::value>(X[c], gsc.r, p);
+            m8[c] = pairs_or(p);
+            S[c] = sign_nibbles(X[c]);
+            *chunk(c) = v4u{p[0], p[1], p[2], p[3]};
+        }
+    };
+    if (__builtin_amdgcn_ballot_w64(gsc.clamp))
+        pairs(std::integral_constant<bool, true>());
+    else
+        pairs(std::integral_constant<bool, false>());
+    // FLAG per block: the OR over its subgroup, built by OR-ing the blocks at
+    // distance 1, 2 and 4 under wave-uniform masks that keep only partners in
+    // the same subgroup
+    const int qgs = qout.lzs;
+    const uint32_t k16 = qgs >= 16 ? ~0u : 0u, k32 = qgs >= 32 ? ~0u : 0u, k64 = qgs >= 64 ? ~0u : 0u;
+    uint32_t o1[8], o2[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        o1[k] = m8[k] | (m8[k ^ 1] & k16);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        o2[k] = o1[k] | (o1[k ^ 2] & k32);
+    int fl[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        fl[k] = lzs_flag(o2[k] | (o2[k ^ 4] & k64));
+    // code words from the stored pairs
+    uint32_t w[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const v4u v = *chunk(c);
+        const uint32_t p[4] = {v[0], v[1], v[2], v[3]};
+        w[c] = lzs_word(p, S[c], fl[c]);
+    }
+
+    const int64_t g = col_base / 64;
+    const int64_t rg0 = g * M + row_base;           // (group, first row)
+    const uint32_t rows_in = (uint32_t)max((int64_t)0, min(M - row_base, (int64_t)64));
+    const Rsrc rc = make_rsrc(qout.codes + rg0 * 32, rows_in * 32u);
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{w[0], w[1], w[2], w[3]}, rc, lane * 32, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{w[4], w[5], w[6], w[7]}, rc, lane * 32 + 16, 0, 0);
+    const uint32_t fb = (uint32_t)(64 / qgs);
+    const Rsrc rf = make_rsrc(qout.flags + rg0 * fb, rows_in * fb);
+    if (qgs == 8) {
+        const uint32_t lo = fl[0] | fl[1] << 8 | fl[2] << 16 | fl[3] << 24;
+        const uint32_t hi = fl[4] | fl[5] << 8 | fl[6] << 16 | fl[7] << 24;
+        __builtin_amdgcn_raw_buffer_store_b64(v2u{lo, hi}, rf, lane * 8, 0, 0);
+    } else if (qgs == 16) {
+        __builtin_amdgcn_raw_buffer_store_b32(
+            (uint32_t)(fl[0] | fl[2] << 8 | fl[4] << 16 | fl[6] << 24), rf, lane * 4, 0, 0);
+    } else if (qgs == 32) {
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(fl[0] | fl[4] << 8), rf, lane * 2, 0, 0);
+    } else {
+        __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl[0], rf, lane, 0, 0);
+    }
+    const Rsrc rs = make_rsrc(qout.scales + rg0, rows_in * 2u);
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)gsc.s16, rs, lane * 2, 0, 0);
+    if (qout.zeros) {
+        const Rsrc rz = make_rsrc(qout.zeros + rg0, rows_in);
+        __builtin_amdgcn_raw_buffer_store_b8((uint8_t)0, rz, lane, 0, 0);
+    }
+}
+
 // Decode roles (decode thread d = tid - 512, 0..255): A row d (32 code bytes,
 // the row's 64 / G_s flags, s_a) and B column d/2, half d%2 (16 code bytes);
 // threads d < 128 also carry s_w of column d.  Rows past M and columns past
@@ -907,135 +1051,17 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     lds_u8* const tbuf = (lds_u8*)(lds_main + kStageBytes);
     auto quantize_out = [&](const v16f (&out)[TM][TN]) {
         if constexpr (QOUT) {
-            static_assert(TN == 2 && WN == 64, "one 64-group per wave row");
             set_out_scale();
             const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
-            if (col_base >= N)
-                return;                              // wave-uniform
             const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
-            lds_u8* const tb = tbuf + uwave * kTransposeBytes;
-            float b[TN];
+            float b[TN], cq[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
+            for (int j = 0; j < TN; ++j) {
                 b[j] = __uint_as_float((uint32_t)bias_bits[j] << 16);
-            const uint32_t lane2 = (uint32_t)lane * 2u;
-            typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-            typedef float f2 __attribute__((ext_vector_type(2)));
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    float v0 = out_value(out[i][0][r], 0, b[0]);
-                    float v1 = out_value(out[i][1][r], 1, b[1]);
-                    if constexpr (GELU) {
-                        v0 = gelu_tanh(v0);
-                        v1 = gelu_tanh(v1);
-                    }
-                    // after the swap lane l holds column l of rows row0, row0 + 4
-                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0),
-                                                                     __float_as_uint(v1), false, false);
-                    const f2 pair = {__uint_as_float(sw[0]), __uint_as_float(sw[1])};
-                    const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf2));
-                    const int row0 = i * 32 + 8 * (r >> 2) + (r & 3);
-                    const uint32_t x0 = (uint32_t)((row0 >> 1) & 7) << 4;
-                    const uint32_t x1 = (uint32_t)(((row0 + 4) >> 1) & 7) << 4;
-                    *(lds_u16*)(tb + row0 * 128 + (lane2 ^ x0)) = (uint16_t)pk;
-                    *(lds_u16*)(tb + (row0 + 4) * 128 + (lane2 ^ x1)) = (uint16_t)(pk >> 16);
-                }
+                cq[j] = STATIC ? cs[j] : kWeightUnitInv;
             }
-            // the wave reads back only what it wrote itself: LDS order within
-            // the wave suffices, the clobber keeps the compiler's order
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            lds_u8* const row = tb + lane * 128;
-            const uint32_t rx = (uint32_t)((lane >> 1) & 7) << 4;
-            auto chunk = [&](int c) { return (lds_v4u*)(row + (((uint32_t)c << 4) ^ rx)); };
-            uint32_t X[8][4];
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const v4u v = *chunk(c);
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    X[c][k] = v[k];
-            }
-            // max |x| on the bf16 magnitude bits (their unsigned order is the
-            // order of |x|), two values per instruction
-            lzs_us2 m2 = {0, 0};
-#pragma unroll
-            for (int c = 0; c < 8; ++c)
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    m2 = __builtin_elementwise_max(m2, __builtin_bit_cast(lzs_us2, X[c][k] & 0x7FFF7FFFu));
-            const uint32_t am = max((uint32_t)m2[0], (uint32_t)m2[1]);
-            const GroupScale gsc = group_scale(__uint_as_float(am << 16));
-            // |q| pairs of each 8-element block (written back over its chunk),
-            // their OR and the sign bits; one branch for the wave
-            uint32_t S[8], m8[8];
-            auto pairs = [&](auto clamp) {
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    uint32_t p[4];
-                    mag_pairs8_t<decltype(clamp)::value>(X[c], gsc.r, p);
-                    m8[c] = pairs_or(p);
-                    S[c] = sign_nibbles(X[c]);
-                    *chunk(c) = v4u{p[0], p[1], p[2], p[3]};
-                }
-            };
-            if (__builtin_amdgcn_ballot_w64(gsc.clamp))
-                pairs(std::integral_constant<bool, true>());
-            else
-                pairs(std::integral_constant<bool, false>());
-            // FLAG per block: the OR over its subgroup, built by OR-ing the
-            // blocks at distance 1, 2 and 4 under wave-uniform masks that keep
-            // only partners in the same subgroup
-            const int qgs = qout.lzs;
-            const uint32_t k16 = qgs >= 16 ? ~0u : 0u, k32 = qgs >= 32 ? ~0u : 0u,
-                           k64 = qgs >= 64 ? ~0u : 0u;
-            uint32_t o1[8], o2[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                o1[k] = m8[k] | (m8[k ^ 1] & k16);
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                o2[k] = o1[k] | (o1[k ^ 2] & k32);
-            int fl[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                fl[k] = lzs_flag(o2[k] | (o2[k ^ 4] & k64));
-            // code words from the stored pairs
-            uint32_t w[8];
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const v4u v = *chunk(c);
-                const uint32_t p[4] = {v[0], v[1], v[2], v[3]};
-                w[c] = lzs_word(p, S[c], fl[c]);
-            }
-
-            const int64_t g = col_base / 64;
-            const int64_t rg0 = g * M + row_base;           // (group, first row)
-            const uint32_t rows_in = (uint32_t)max((int64_t)0, min(M - row_base, (int64_t)WM));
-            const Rsrc rc = make_rsrc(qout.codes + rg0 * 32, rows_in * 32u);
-            __builtin_amdgcn_raw_buffer_store_b128(v4u{w[0], w[1], w[2], w[3]}, rc, lane * 32, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b128(v4u{w[4], w[5], w[6], w[7]}, rc, lane * 32 + 16, 0, 0);
-            const uint32_t fb = (uint32_t)(64 / qgs);
-            const Rsrc rf = make_rsrc(qout.flags + rg0 * fb, rows_in * fb);
-            if (qgs == 8) {
-                const uint32_t lo = fl[0] | fl[1] << 8 | fl[2] << 16 | fl[3] << 24;
-                const uint32_t hi = fl[4] | fl[5] << 8 | fl[6] << 16 | fl[7] << 24;
-                __builtin_amdgcn_raw_buffer_store_b64(v2u{lo, hi}, rf, lane * 8, 0, 0);
-            } else if (qgs == 16) {
-                __builtin_amdgcn_raw_buffer_store_b32(
-                    (uint32_t)(fl[0] | fl[2] << 8 | fl[4] << 16 | fl[6] << 24), rf, lane * 4, 0, 0);
-            } else if (qgs == 32) {
-                __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(fl[0] | fl[4] << 8), rf, lane * 2, 0, 0);
-            } else {
-                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl[0], rf, lane, 0, 0);
-            }
-            const Rsrc rs = make_rsrc(qout.scales + rg0, rows_in * 2u);
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)gsc.s16, rs, lane * 2, 0, 0);
-            if (qout.zeros) {
-                const Rsrc rz = make_rsrc(qout.zeros + rg0, rows_in);
-                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)0, rz, lane, 0, 0);
-            }
+            quantize_tile_out<GELU>(out, cq, b, tbuf + uwave * kTransposeBytes, lane, row_base,
+                                    col_base, M, N, qout);
         }
     };
 

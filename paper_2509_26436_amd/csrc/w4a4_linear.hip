@@ -47,24 +47,43 @@ static_assert(64 * kLinDecodeWaves == 2 * LBM && 64 * kLinDecodeWaves == LBN, "d
 // no dequantization pipeline the math waves have the registers to take their
 // weight words straight from global memory (a ring three groups deep), and
 // only the decoded activations pass through LDS.
-template <int GS, bool GELU, bool SPLIT, bool STATIC>
+// QOUT: the output quantized for the next layer (quartz_w4a4_linear_quantize)
+// instead of bf16: each math wave runs its 64 x 64 tile through the
+// activation quantizer in its own LDS region (quantize_tile_out).
+template <int GS, bool GELU, bool SPLIT, bool STATIC, bool QOUT>
 __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int64_t M, int64_t N, int64_t K,
     int64_t ldy, GemmSchedule sch, uint32_t* __restrict__ counters, float* __restrict__ slots,
-    float act_scale)
+    float act_scale, QuantOut qout)
 {
-    // decoded activations, stage-major; row r's 16-byte chunk c at swz(r, c)
-    __shared__ __attribute__((aligned(16))) uint8_t As[kLinStages][LBM * 64];
-    // stored weight words of the tile's columns, k half h of column c (16
-    // bytes) at h * LBN * 16 + c * 16: the 16 lanes of a read phase cover
-    // 256 consecutive bytes
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[kLinStages][LBN * 32];
-    // group scales as fp16 bits; entries LBM (LBN) stay 0: the upper
-    // half-wave's k = 8 operand slot of the outer-product MFMA reads them
-    __shared__ uint16_t sas[kLinStages][LBM + 8];
-    __shared__ uint16_t sws[kLinStages][LBN + 8];
+    // One LDS array: the operand stages at the lowest addresses (so every
+    // fragment address of the main loop is a lane offset plus a 16-bit
+    // immediate), then, for QOUT, the math waves' output transpose regions.
+    //   As:  decoded activations, stage-major; row r's 16-byte chunk c at
+    //        swz(r, c)
+    //   Bs:  stored weight words of the tile's columns, k half h of column c
+    //        (16 bytes) at h * LBN * 16 + c * 16: the 16 lanes of a read phase
+    //        cover 256 consecutive bytes
+    //   sas, sws: group scales as fp16 bits; entries LBM (LBN) stay 0: the
+    //        upper half-wave's k slots of the outer-product MFMA read them
+    //   Ts:  QOUT, 8 KB per math wave
+    constexpr int kAsBytes = kLinStages * LBM * 64;
+    constexpr int kBsBytes = kLinStages * LBN * 32;
+    constexpr int kSasBytes = kLinStages * (LBM + 8) * 2;
+    constexpr int kSwsBytes = kLinStages * (LBN + 8) * 2;
+    constexpr int kStageLds = kAsBytes + kBsBytes + kSasBytes + kSwsBytes;
+    static_assert(kStageLds % 16 == 0, "transpose regions stay 16-byte aligned");
+    __shared__ __attribute__((aligned(16)))
+    uint8_t lds_main[kStageLds + (QOUT ? kLinMathWaves * kTransposeBytes : 0)];
+    uint8_t (*const As)[LBM * 64] = reinterpret_cast<uint8_t (*)[LBM * 64]>(lds_main);
+    uint8_t (*const Bs)[LBN * 32] = reinterpret_cast<uint8_t (*)[LBN * 32]>(lds_main + kAsBytes);
+    uint16_t (*const sas)[LBM + 8] =
+        reinterpret_cast<uint16_t (*)[LBM + 8]>(lds_main + kAsBytes + kBsBytes);
+    uint16_t (*const sws)[LBN + 8] =
+        reinterpret_cast<uint16_t (*)[LBN + 8]>(lds_main + kAsBytes + kBsBytes + kSasBytes);
+    uint8_t* const Ts = lds_main + kStageLds;
 
     constexpr int FB = 64 / GS;                 // flag bytes per (group, row)
     const int tid = threadIdx.x;
@@ -88,9 +107,9 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     // ------------------------------------------------------ decode waves
     // Thread d: half ah of activation row dr of the tile (16 code bytes, the
     // half's FLAGs), that row's scale (ah == 0 stores it), and the 32 code
-    // bytes and the scale of tile column d.  Rows past M and columns past the packed panels fall
-    // outside the buffer ranges and read as zero; they only feed outputs that
-    // are never stored.
+    // bytes and the scale of tile column d.  Rows past M and columns past the
+    // packed panels fall outside the buffer ranges and read as zero; they only
+    // feed outputs that are never stored.
     if (uwave >= kLinMathWaves) {
         const int d = tid - kLinMathWaves * 64;
         const int dr = d >> 1, ah = d & 1;
@@ -471,6 +490,11 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
                                  kWeightUnitInv
                            : kWeightUnitInv;
         }
+        if constexpr (QOUT) {
+            quantize_tile_out<GELU>(acc, cs, b, (lds_u8*)(Ts + (uwave & (kLinMathWaves - 1)) * kTransposeBytes),
+                                    lane, row_base, col_base, M, N, qout);
+            return;
+        }
         const int64_t rows_in = max((int64_t)0, min(M - row_base, (int64_t)WM));
         const uint32_t row_bytes = (uint32_t)ldy * 2u;
         const Rsrc out_r = make_rsrc(y + row_base * ldy + col_base, (uint32_t)rows_in * row_bytes);
@@ -689,7 +713,7 @@ int linear_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_linear_kernel<16, false, true, false>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_linear_kernel<16, false, true, false, true>),
             kLinThreads, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
@@ -698,14 +722,15 @@ int linear_resident_blocks()
     return n;
 }
 
-template <bool STATIC>
+template <bool STATIC, bool QOUT>
 hipError_t launch_linear_mode(const GemmLaunch& a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.sch.blocks), block(kLinThreads);
     auto go = [&](auto gs, auto gelu, auto split) {
-        w4a4_linear_kernel<decltype(gs)::value, decltype(gelu)::value, decltype(split)::value, STATIC>
-            <<<grid, block, 0, stream>>>(a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.M,
-                                         a.N, a.K, a.ldy, a.sch, a.counters, a.slots, a.act_scale);
+        w4a4_linear_kernel<decltype(gs)::value, decltype(gelu)::value, decltype(split)::value, STATIC,
+                           QOUT><<<grid, block, 0, stream>>>(
+            a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.M, a.N, a.K, a.ldy, a.sch,
+            a.counters, a.slots, a.act_scale, a.qout);
     };
     auto with_split = [&](auto gs, auto gelu) {
         if (a.sch.sk_tiles > 0)
@@ -738,12 +763,13 @@ hipError_t launch_linear_mode(const GemmLaunch& a, hipStream_t stream)
 
 hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_linear_mode<false>(a, stream);
+    return a.qout.codes ? launch_linear_mode<false, true>(a, stream)
+                        : launch_linear_mode<false, false>(a, stream);
 }
 
 hipError_t launch_linear_static(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_linear_mode<true>(a, stream);
+    return launch_linear_mode<true, false>(a, stream);
 }
 
 }  // namespace quartz
