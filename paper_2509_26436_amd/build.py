@@ -14,9 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libquartz.so")
-SOURCES = ["abi.hip", "quantize_lzs.hip", "pack_weight.hip", "w4a4_gemm.hip",
-           "w4a4_gemm_plain.hip", "w4a4_gemm_quant.hip", "w4a4_gemm_static.hip",
-           "w4a4_gemm_asym.hip", "w4a4_gemm_conv.hip", "w4a4_linear.hip", "scratch.hip", "attention.hip", "attention_fused.hip"]
+SOURCES = ["abi.hip", "quantize_lzs.hip", "pack_weight.hip", "w4a4_gemm.hip", "w4a4_linear.hip",
+           "w4a4_gemm_plain.hip", "w4a4_gemm_asym.hip", "w4a4_gemm_conv.hip", "scratch.hip",
+           "attention.hip", "attention_fused.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

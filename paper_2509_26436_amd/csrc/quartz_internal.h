@@ -141,12 +141,9 @@ struct GemmLaunch {
 };
 
 // One output mode each (w4a4_gemm_<mode>.hip).
-hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_linear_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
-hipError_t launch_gemm_quant(const GemmLaunch& a, hipStream_t stream);
-hipError_t launch_gemm_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv_static(const GemmLaunch& a, hipStream_t stream);

@@ -6,7 +6,7 @@ namespace quartz {
 
 hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, false, false, true>(a, stream);
+    return launch_mode<false, false, true>(a, stream);
 }
 
 }  // namespace quartz

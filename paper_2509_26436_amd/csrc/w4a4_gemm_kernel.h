@@ -180,10 +180,9 @@ __device__ __forceinline__ uint2 flags_dwords(FlagRaw<GS> raw)
 }
 
 // One math wave's 64 x 64 bf16 output tile, staged in LDS by the epilogue
-// that quantizes the output for the next layer (QOUT), addressed through
-// LDS-typed pointers.
+// that quantizes the output for the next layer (quantize_tile_out), addressed
+// through LDS-typed pointers.
 constexpr int kTransposeBytes = WM * WN * 2;
-constexpr int kTransposeLds = kMathWaves * kTransposeBytes;
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
 typedef __attribute__((address_space(3))) v4u lds_v4u;
@@ -342,8 +341,7 @@ __device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const
 // single pipeline.  The decode waves fetch and decode across segment
 // boundaries without a break, so while the math waves write one tile's
 // output the next tile's first groups are already being staged.  SPLIT
-// instantiations carry the partial-sum code of shared tiles; QOUT ones write
-// the output quantized for the next layer instead of bf16 (QuantOut).
+// instantiations carry the partial-sum code of shared tiles.
 // STATIC instantiations are the LDM setting (the experimental-details
 // appendix): one per-tensor activation scale and per-channel weight scales,
 // so the K loop has no per-group scales at all: the fp8 MFMAs accumulate the
@@ -365,14 +363,14 @@ __device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const
 // tables like A, and A and B address one head's rows inside the arrays of
 // all heads (plane stride and row offset).  With OUT32 the output is fp32,
 // y32 = acc * scale (the scores); otherwise the bf16 output of the layer.
-template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool QOUT, bool STATIC, bool ASYM,
+template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool STATIC, bool ASYM,
           bool CONV = false, bool ATTN = false, bool OUT32 = false>
 __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
-    uint32_t* __restrict__ counters, float* __restrict__ slots, QuantOut qout, float act_scale,
+    uint32_t* __restrict__ counters, float* __restrict__ slots, float act_scale,
     const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums, ConvGeom conv,
     AttnGeom attn)
 {
@@ -381,17 +379,17 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     // three LDS stages: group g + 2 is decoded into one while the math waves
     // read the operands of group g + 1 from another (and multiply group g
     // from registers)
-    // One LDS array holds the operand stages and, in QOUT kernels, the
-    // output transpose regions after them: the stages stay at the lowest
-    // addresses, where every fragment address of the main loop is a lane
-    // offset plus an immediate (a larger array placed first would push them
-    // past the 16-bit immediate range and cost a register per stage).
+    // One LDS array holds the operand stages and, in ASYM kernels, the zero
+    // point operands after them: the stages stay at the lowest addresses,
+    // where every fragment address of the main loop is a lane offset plus an
+    // immediate (a larger array placed first would push them past the 16-bit
+    // immediate range and cost a register per stage).
     constexpr int kStageBytes = kStages * (BM + BN) * 64;
     // ASYM: the fp16 operands -z and W of the correction MFMA, per stage, with
     // the same zero pads as the scales
     constexpr int kZeroLds = kStages * (BM + 8 + BN + 8) * 2;
     __shared__ __attribute__((aligned(16))) uint8_t
-        lds_main[kStageBytes + (QOUT ? kTransposeLds : 0) + (ASYM ? kZeroLds : 0)];
+        lds_main[kStageBytes + (ASYM ? kZeroLds : 0)];
     uint8_t (*const As)[BM * 64] = reinterpret_cast<uint8_t (*)[BM * 64]>(lds_main);
     uint8_t (*const Bs)[BN * 64] = reinterpret_cast<uint8_t (*)[BN * 64]>(lds_main + kStages * BM * 64);
     uint16_t (*const szs)[BM + 8] = reinterpret_cast<uint16_t (*)[BM + 8]>(lds_main + kStageBytes);
@@ -1032,45 +1030,10 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
         else
             return fmaf(a, kWeightUnitInv, bj);
     };
-    // ---- output quantized for the next layer (QOUT): the bf16 values the
-    // plain epilogue would store, run through the activation quantizer with
-    // this layer's N as the next layer's K.  The wave's 64 columns are one
-    // 64-group of each of its 64 rows (N % 64 == 0).  The bf16 tile goes
-    // through the wave's own LDS region and comes back one row per lane, so
-    // the group maximum, the subgroup ORs and the code packing are in-lane
-    // arithmetic (lzs_device.h).  Row r's 16-byte chunk c (its elements
-    // 8c..8c+7, one 8-element block) sits at chunk c ^ ((r >> 1) & 7): a read
-    // of one chunk per row by 16 consecutive lanes (8 chunk positions x 2 row
-    // parities) then covers all 64 banks.  The row is read once; per block
-    // the |q| pairs go back over the block's chunk (so they need no registers
-    // while the subgroup FLAGs are formed) and are read again for the code
-    // words.
-    // Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
-    // [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside
-    // the buffer ranges and are dropped.
-    lds_u8* const tbuf = (lds_u8*)(lds_main + kStageBytes);
-    auto quantize_out = [&](const v16f (&out)[TM][TN]) {
-        if constexpr (QOUT) {
-            set_out_scale();
-            const int64_t col_base = (int64_t)cur.tn * BN + wn * WN;
-            const int64_t row_base = (int64_t)cur.tm * BM + wm * WM;
-            float b[TN], cq[TN];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                b[j] = __uint_as_float((uint32_t)bias_bits[j] << 16);
-                cq[j] = STATIC ? cs[j] : kWeightUnitInv;
-            }
-            quantize_tile_out<GELU>(out, cq, b, tbuf + uwave * kTransposeBytes, lane, row_base,
-                                    col_base, M, N, qout);
-        }
-    };
-
     // ---- output.  Lane l holds column l % 32 of each 32 x 32 tile, rows
     // 8 (r/4) + 4 khalf + r%4 of register r.
     auto store_tile = [&](const v16f (&out)[TM][TN]) {
-        if constexpr (QOUT) {
-            quantize_out(out);
-        } else if constexpr (OUT32) {
+        if constexpr (OUT32) {
             // fp32 y32[row][ldy] = acc * scale; lane l holds column l % 32,
             // so each store instruction writes two rows' 32 consecutive floats
 #pragma unroll
@@ -1346,7 +1309,7 @@ template <bool B>
 using bool_c = std::integral_constant<bool, B>;
 
 // Launch of one output mode, every G_s / epilogue / split combination of it.
-template <bool I32OUT, bool QOUT, bool STATIC, bool ASYM, bool CONV = false, bool ATTN = false,
+template <bool I32OUT, bool STATIC, bool ASYM, bool CONV = false, bool ATTN = false,
           bool OUT32 = false>
 hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
 {
@@ -1354,9 +1317,9 @@ hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
     const dim3 block(STATIC && a.sch.sk_tiles == 0 ? kSplitThreadsPerBlock : kThreadsPerBlock);
     auto go = [&](auto gs, auto gelu, auto split) {
         w4a4_gemm_kernel<decltype(gs)::value, I32OUT, decltype(gelu)::value, decltype(split)::value,
-                         QOUT, STATIC, ASYM, CONV, ATTN, OUT32><<<grid, block, 0, stream>>>(
+                         STATIC, ASYM, CONV, ATTN, OUT32><<<grid, block, 0, stream>>>(
             a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.yi, a.M, a.N, a.K, a.ldy, a.sch,
-            a.counters, a.slots, a.qout, a.act_scale, a.zeros, a.wsums, a.conv, a.attn);
+            a.counters, a.slots, a.act_scale, a.zeros, a.wsums, a.conv, a.attn);
     };
     auto with_split = [&](auto gs, auto gelu) {
         if (!I32OUT && !OUT32 && a.sch.sk_tiles > 0)

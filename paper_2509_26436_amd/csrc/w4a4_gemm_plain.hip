@@ -1,17 +1,12 @@
-// W4A4 GEMM instantiations: the bf16 output and the exact integer
-// accumulator, plus the occupancy query the persistent grid is sized by.
+// W4A4 GEMM template instantiations: the exact integer accumulator, plus the
+// occupancy query the template's persistent grid is sized by.
 #include "w4a4_gemm_kernel.h"
 
 namespace quartz {
 
-hipError_t launch_gemm_plain(const GemmLaunch& a, hipStream_t stream)
-{
-    return launch_mode<false, false, false, false>(a, stream);
-}
-
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<true, false, false, false>(a, stream);
+    return launch_mode<true, false, false>(a, stream);
 }
 
 int device_compute_units()
@@ -50,7 +45,7 @@ int gemm_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false, false>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false, true>),
             kThreadsPerBlock, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
