@@ -187,31 +187,24 @@ typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
 typedef __attribute__((address_space(3))) v4u lds_v4u;
 
-// ---- output quantized for the next layer: one math wave's 64 x 64 tile (2 x 2
-// MFMA tiles of 32 x 32: lane l holds column l % 32, rows 8 (r/4) + 4 khalf
-// + r%4 of register r) becomes the bf16 values the plain epilogue would store,
-// fmaf(acc, cs[j], b[j]) then the optional GELU, run through the activation
-// quantizer with this layer's N as the next layer's K.  The wave's 64 columns
-// are one 64-group of each of its 64 rows (N % 64 == 0).  The bf16 tile goes
-// through the wave's own LDS region tb (8 KB) and comes back one row per lane,
-// so the group maximum, the subgroup ORs and the code packing are in-lane
-// arithmetic (lzs_device.h).  Row r's 16-byte chunk c (its elements 8c..8c+7,
-// one 8-element block) sits at chunk c ^ ((r >> 1) & 7): a read of one chunk
-// per row by 16 consecutive lanes (8 chunk positions x 2 row parities) then
-// covers all 64 banks.  The row is read once; per block the |q| pairs go back
-// over the block's chunk (so they need no registers while the subgroup FLAGs
-// are formed) and are read again for the code words.
-// Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
-// [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside the
-// buffer ranges and are dropped.
-template <bool GELU>
-__device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const float (&cs)[2],
-                                                  const float (&b)[2], lds_u8* tb, int lane,
-                                                  int64_t row_base, int64_t col_base, int64_t M,
-                                                  int64_t N, const QuantOut& qout)
+// One math wave's 64 x 64 output tile (2 x 2 MFMA tiles of 32 x 32: lane l
+// holds column l % 32, rows 8 (r/4) + 4 khalf + r%4 of register r) as the bf16
+// values of the plain epilogue, fmaf(acc, cs[j], b[j]) then the optional
+// GELU, written row-major into the wave's LDS region tb (8 KB, 128 bytes per
+// row).  Row r's 16-byte chunk c (its elements 8c..8c+7) sits at chunk
+// c ^ ((r >> 1) & 7) (tile_chunk_offset): the column-per-lane writes of one
+// row, and a read of one chunk per row by 16 consecutive lanes (8 chunk
+// positions x 2 row parities), both cover all 64 banks.  The caller waits for
+// the writes before reading them back (the wave reads only its own region).
+__device__ __forceinline__ uint32_t tile_chunk_offset(uint32_t row, uint32_t c)
 {
-    if (col_base >= N)
-        return;                              // wave-uniform
+    return row * 128u + ((c ^ ((row >> 1) & 7u)) << 4);
+}
+
+template <bool GELU>
+__device__ __forceinline__ void stage_tile_bf16(const v16f (&out)[2][2], const float (&cs)[2],
+                                                const float (&b)[2], lds_u8* tb, int lane)
+{
     const uint32_t lane2 = (uint32_t)lane * 2u;
     typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
     typedef float f2 __attribute__((ext_vector_type(2)));
@@ -237,6 +230,32 @@ __device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const
             *(lds_u16*)(tb + (row0 + 4) * 128 + (lane2 ^ x1)) = (uint16_t)(pk >> 16);
         }
     }
+}
+
+// ---- output quantized for the next layer: one math wave's 64 x 64 tile (2 x 2
+// MFMA tiles of 32 x 32: lane l holds column l % 32, rows 8 (r/4) + 4 khalf
+// + r%4 of register r) becomes the bf16 values the plain epilogue would store,
+// fmaf(acc, cs[j], b[j]) then the optional GELU, run through the activation
+// quantizer with this layer's N as the next layer's K.  The wave's 64 columns
+// are one 64-group of each of its 64 rows (N % 64 == 0).  The bf16 tile goes
+// through the wave's own LDS region tb (stage_tile_bf16) and comes back one
+// row per lane, so the group maximum, the subgroup ORs and the code packing
+// are in-lane arithmetic (lzs_device.h); a chunk is one 8-element block.  The
+// row is read once; per block the |q| pairs go back over the block's chunk
+// (so they need no registers while the subgroup FLAGs are formed) and are
+// read again for the code words.
+// Outputs, K-group-major with g = column / 64: codes [g][M][32], flags
+// [g][M][64 / lzs], scales [g][M], zeros [g][M]; rows past M fall outside the
+// buffer ranges and are dropped.
+template <bool GELU>
+__device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const float (&cs)[2],
+                                                  const float (&b)[2], lds_u8* tb, int lane,
+                                                  int64_t row_base, int64_t col_base, int64_t M,
+                                                  int64_t N, const QuantOut& qout)
+{
+    if (col_base >= N)
+        return;                              // wave-uniform
+    stage_tile_bf16<GELU>(out, cs, b, tb, lane);
     // the wave reads back only what it wrote itself: LDS order within the
     // wave suffices, the clobber keeps the compiler's order
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 {
     // One LDS array: the operand stages at the lowest addresses (so every
     // fragment address of the main loop is a lane offset plus a 16-bit
-    // immediate), then, for QOUT, the math waves' output transpose regions.
+    // immediate), then the math waves' output transpose regions.
     //   As:  decoded activations, stage-major; row r's 16-byte chunk c at
     //        swz(r, c)
     //   Bs:  stored weight words of the tile's columns, k half h of column c
@@ -68,7 +68,8 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     //        cover 256 consecutive bytes
     //   sas, sws: group scales as fp16 bits; entries LBM (LBN) stay 0: the
     //        upper half-wave's k slots of the outer-product MFMA read them
-    //   Ts:  QOUT, 8 KB per math wave
+    //   Ts:  8 KB per math wave: its bf16 output tile on the way to 16-byte
+    //        stores, or to the quantizer (QOUT)
     constexpr int kAsBytes = kLinStages * LBM * 64;
     constexpr int kBsBytes = kLinStages * LBN * 32;
     constexpr int kSasBytes = kLinStages * (LBM + 8) * 2;
@@ -76,7 +77,7 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
     constexpr int kStageLds = kAsBytes + kBsBytes + kSasBytes + kSwsBytes;
     static_assert(kStageLds % 16 == 0, "transpose regions stay 16-byte aligned");
     __shared__ __attribute__((aligned(16)))
-    uint8_t lds_main[kStageLds + (QOUT ? kLinMathWaves * kTransposeBytes : 0)];
+    uint8_t lds_main[kStageLds + kLinMathWaves * kTransposeBytes];
     uint8_t (*const As)[LBM * 64] = reinterpret_cast<uint8_t (*)[LBM * 64]>(lds_main);
     uint8_t (*const Bs)[LBN * 32] = reinterpret_cast<uint8_t (*)[LBN * 32]>(lds_main + kAsBytes);
     uint16_t (*const sas)[LBM + 8] =
@@ -316,7 +317,7 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         sw_op[j][0] = (int)sws[buf][khalf ? LBN : wn * WN + j * 32 + l32];
     };
 
-    v16f p_next, p_last, s_last;
+    v16f pc, sc;                             // tile product and scale tile in flight
     const v16f zero = {};
     auto fma_rows = [&](int i, int j, const v16f& p, const v16f& sc, int r0) {
 #pragma unroll
@@ -380,6 +381,23 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
         bfetch(ring2);
         bf = decode_w(ring0.c0);
     };
+    // Per-group order, tiles t = (0,0) (1,0) (0,1) (1,1): at step t the fp8
+    // product of tile t+1 is issued first, then the 16 FMAs of tile t (whose
+    // product and scale tile were issued one step earlier and are done), then
+    // the scale tile of tile t+1, then the operand work (LDS reads, weight
+    // decode).  No FMA waits on an MFMA issued just before it, and each MFMA
+    // goes out once the matrix unit has drained the previous one (an MFMA
+    // issued while the unit is busy stalls its wave, and with it the FMAs
+    // behind it).  The scale tile needs one buffer: it is overwritten only
+    // after its FMAs.  Step 3 issues the next group's tile-0 product and scale
+    // tile (not for a segment's last group), so the pipeline runs across the
+    // barrier.  On entry pc and sc hold (in flight) this group's tile-0
+    // product and scale tile, af[], sa_op[] and sw_op[] this group's
+    // operands, bf its column-0 weight operand and wraw its column-1 weight
+    // words.  The next group's operands (LDS stage nb) are read after their
+    // last use here: column-0 words and s_w at step 0, rows 0 at step 1, rows
+    // 1 at step 2 (with the decode of the column-0 words), column-1 words and
+    // s_w at step 3.
     auto compute = [&](int cb, int nb, auto last) {
         constexpr bool LAST = decltype(last)::value;
         if constexpr (STATIC) {
@@ -387,46 +405,59 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
             compute_static(nb, last);
             return;
         }
-        p_next = mfma_p(0);
+        (void)cb;
+        v16f pn;
+        // step 0: tile (0,0)
+        pn = mfma_p(1);                       // tile (1,0): rows 1 x column 0
         __builtin_amdgcn_sched_barrier(0);
-        fma_tile(TM - 1, TN - 1, p_last, s_last);
+        fma_tile(0, 0, pc, sc);
         __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < TM * TN; ++t) {
-            const int i = t % TM, j = t / TM;
-            const v16f p = p_next;
-            const v16f sc = scale_tile(i, j);
-            if (t == 1 && !LAST)
-                wraw = raw_w(0, nb);          // the next group's column 0
-            if (t == 3 && !LAST)
-                wraw = raw_w(1, nb);          // the next group's column 1
-            __builtin_amdgcn_sched_barrier(0);
-            if (t + 1 < TM * TN)
-                fma_rows(i, j, p, sc, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (t + 1 < TM * TN)
-                p_next = mfma_p((t + 1) % TM);
-            __builtin_amdgcn_sched_barrier(0);
-            if (t == 0) {
-                bf = decode_w(wraw);          // column 0's products are issued
-                load_sw(1, cb);
-            }
-            if (t == 2 && !LAST) {
-                load_a(0, nb);
-                bf = decode_w(wraw);          // the next group's column 0
-                load_sw(0, nb);
-            }
-            if (t == 3 && !LAST)
-                load_a(1, nb);
-            __builtin_amdgcn_sched_barrier(0);
-            if (t + 1 < TM * TN) {
-                fma_rows(i, j, p, sc, 8);
-            } else {
-                p_last = p;
-                s_last = sc;
-            }
-            __builtin_amdgcn_sched_barrier(0);
+        sc = scale_tile(1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        bf = decode_w(wraw);                  // column 1: column 0's products are issued
+        if (!LAST) {
+            wraw = raw_w(0, nb);
+            load_sw(0, nb);
         }
+        __builtin_amdgcn_sched_barrier(0);
+        pc = pn;
+        // step 1: tile (1,0)
+        pn = mfma_p(0);                       // tile (0,1)
+        __builtin_amdgcn_sched_barrier(0);
+        fma_tile(1, 0, pc, sc);
+        __builtin_amdgcn_sched_barrier(0);
+        sc = scale_tile(0, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!LAST)
+            load_a(0, nb);
+        __builtin_amdgcn_sched_barrier(0);
+        pc = pn;
+        // step 2: tile (0,1)
+        pn = mfma_p(1);                       // tile (1,1)
+        __builtin_amdgcn_sched_barrier(0);
+        fma_tile(0, 1, pc, sc);
+        __builtin_amdgcn_sched_barrier(0);
+        sc = scale_tile(1, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!LAST) {
+            load_a(1, nb);
+            bf = decode_w(wraw);              // the next group's column 0
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        pc = pn;
+        // step 3: tile (1,1)
+        if (!LAST)
+            pn = mfma_p(0);                   // the next group's tile (0,0)
+        __builtin_amdgcn_sched_barrier(0);
+        fma_tile(1, 1, pc, sc);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!LAST) {
+            sc = scale_tile(0, 0);
+            wraw = raw_w(1, nb);
+            load_sw(1, nb);
+            pc = pn;
+        }
+        __builtin_amdgcn_sched_barrier(0);
     };
     auto math_barrier = [] { asm volatile("s_barrier" ::: "memory"); };
     using NotLast = std::integral_constant<bool, false>;
@@ -490,14 +521,30 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
                                  kWeightUnitInv
                            : kWeightUnitInv;
         }
+        lds_u8* const tw = (lds_u8*)(Ts + (uwave & (kLinMathWaves - 1)) * kTransposeBytes);
         if constexpr (QOUT) {
-            quantize_tile_out<GELU>(acc, cs, b, (lds_u8*)(Ts + (uwave & (kLinMathWaves - 1)) * kTransposeBytes),
-                                    lane, row_base, col_base, M, N, qout);
+            quantize_tile_out<GELU>(acc, cs, b, tw, lane, row_base, col_base, M, N, qout);
             return;
         }
         const int64_t rows_in = max((int64_t)0, min(M - row_base, (int64_t)WM));
         const uint32_t row_bytes = (uint32_t)ldy * 2u;
         const Rsrc out_r = make_rsrc(y + row_base * ldy + col_base, (uint32_t)rows_in * row_bytes);
+        // The tile through LDS, 16 bytes per lane and store: 8 stores of 8
+        // rows each (a short store per element and row costs the vector
+        // memory path as much as a full one).  Needs the wave's 64 columns
+        // inside N and 16-byte aligned rows (wave-uniform); otherwise the
+        // element stores below.
+        if (col_base + WN <= N && ((reinterpret_cast<uintptr_t>(y) | (uint64_t)row_bytes) & 15u) == 0) {
+            stage_tile_bf16<GELU>(acc, cs, b, tw, lane);
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t row = (uint32_t)(8 * q) + ((uint32_t)lane >> 3), c = (uint32_t)lane & 7u;
+                const v4u v = *(lds_v4u*)(tw + tile_chunk_offset(row, c));
+                __builtin_amdgcn_raw_buffer_store_b128(v, out_r, (int)(row * row_bytes + c * 16u), 0, 0);
+            }
+            return;
+        }
         const uint32_t voff = col_base + lane < N ? (uint32_t)lane * 2u : 0x80000000u;
         typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
         typedef float f2 __attribute__((ext_vector_type(2)));
@@ -633,11 +680,6 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     acc[i][j][r] = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            p_last[r] = 0.0f;
-            s_last[r] = 0.0f;
-        }
     };
 
     if (!cursor_begin(fresh_schedule(), blk, cur))
@@ -675,14 +717,15 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
             bf = decode_w(raw_w(0, 0));
             wraw = raw_w(1, 0);
             load_sw(0, 0);
+            load_sw(1, 0);
+            pc = mfma_p(0);
+            sc = scale_tile(0, 0);
         }
         run_groups(L - 1);
         compute((L - 1) % kLinStages, 0, std::integral_constant<bool, true>());
         math_barrier();
         for (int p = L; p < padded_steps(L); ++p)
             math_barrier();
-        if constexpr (!STATIC)
-            fma_tile(TM - 1, TN - 1, p_last, s_last);
         set_fragment_indices();
         if (!SPLIT || cur.sg.sk_tile < 0 || finish_partial())
             store_tile();
