@@ -609,61 +609,43 @@ __global__ __launch_bounds__(kLinThreads) void w4a4_linear_kernel(
             if (arrived != (uint32_t)(b_last - b_first))
                 return false;
             asm volatile("" ::: "memory");
-            if (b_last - b_first == 1) {
-                const int32_t other = b_first == blk ? b_last : b_first;
-                const Rsrc part = slot_rsrc(sk_slot(sch_, other, cur.sg.sk_tile));
-#pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    v4f v[TN][4];
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            v[j][q] = __builtin_amdgcn_raw_buffer_load_b128(
-                                part, (int)(lane_off + ((i * TN + j) * 4 + q) * 1024), 0, kCoherent);
-#pragma unroll
-                    for (int j = 0; j < TN; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                acc[i][j][4 * q + e] += v[j][q][e];
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-                if (lane == 0)
-                    __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                return true;
-            }
+            // contributors in workgroup order (with two, this one's own share
+            // stays in acc; with more, every share is read back from its
+            // slot), a 32 x 32 tile (four 16-byte loads per lane) per
+            // contributor in flight, so the finisher needs few registers
+            const int32_t other = b_first == blk ? b_last : b_first;
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const int toff = (int)(lane_off + (i * TN + j) * 4 * 1024);
-                    for (int32_t bb = b_first; bb <= b_last; bb += 2) {
-                        const bool two = bb < b_last;
-                        v4f va[4], vb[4];
-                        const Rsrc pa = slot_rsrc(sk_slot(sch_, bb, cur.sg.sk_tile));
+                    auto load_tile = [&](int32_t bb, v4f (&v)[4]) {
+                        const Rsrc part = slot_rsrc(sk_slot(sch_, bb, cur.sg.sk_tile));
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
-                            va[q] = __builtin_amdgcn_raw_buffer_load_b128(pa, toff + q * 1024, 0, kCoherent);
-                        if (two) {
-                            const Rsrc pb = slot_rsrc(sk_slot(sch_, bb + 1, cur.sg.sk_tile));
+                            v[q] = __builtin_amdgcn_raw_buffer_load_b128(part, toff + q * 1024, 0, kCoherent);
+                    };
+                    if (b_last - b_first == 1) {
+                        v4f v[4];
+                        load_tile(other, v);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                acc[i][j][4 * q + e] += v[q][e];
+                    } else {
+                        for (int32_t bb = b_first; bb <= b_last; ++bb) {
+                            v4f v[4];
+                            load_tile(bb, v);
 #pragma unroll
                             for (int q = 0; q < 4; ++q)
-                                vb[q] = __builtin_amdgcn_raw_buffer_load_b128(pb, toff + q * 1024, 0, kCoherent);
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    acc[i][j][4 * q + e] =
+                                        bb == b_first ? v[q][e] : acc[i][j][4 * q + e] + v[q][e];
                         }
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                if (bb == b_first)
-                                    acc[i][j][4 * q + e] = va[q][e];
-                                else
-                                    acc[i][j][4 * q + e] += va[q][e];
-                                if (two)
-                                    acc[i][j][4 * q + e] += vb[q][e];
-                            }
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             if (lane == 0)
                 __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
