@@ -53,7 +53,8 @@ PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 SETTLE_S = 0.25               # untimed load before the timed steps (clock settling)
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "w4a4_gemm_hbm_traffic_flux_block_m4608.md")
 GEMM_SOURCES = [os.path.join(ROOT, "paper_2509_26436_amd", "csrc", f)
-                for f in ("w4a4_linear.hip", "w4a4_gemm_kernel.h", "w4a4_gemm.hip", "w4a4_gemm_plain.hip",
+                for f in ("w4a4_linear.hip", "w4a4_linear_kernel.h", "w4a4_gemm_kernel.h", "w4a4_gemm.hip",
+                          "w4a4_gemm_plain.hip",
                           "gemm_schedule.h", "quartz_internal.h", "lzs_device.h")]
 
 

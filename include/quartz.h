@@ -479,9 +479,9 @@ quartz_status quartz_lzs_attention(const void* q_bf16, const void* k_bf16, const
  * points use the device's compute-unit count), with (split = 1, as
  * quartz_w4a4_linear_ws) or without (split = 0, as quartz_w4a4_linear) tiles
  * cut along K, for tiles of 128 x 256 (tiles = 0: quartz_w4a4_linear and its
- * variants, quartz_w4a4_linear_static) or of 256 x 128 (tiles = 1: the
- * quantizing epilogue, the asymmetric mode, the convolutions and the
- * attention products).
+ * variants, quartz_w4a4_linear_quantize, quartz_w4a4_linear_static and
+ * quartz_w4a4_linear_asym) or of 256 x 128 (tiles = 1: the convolutions, the
+ * exact integer accumulator and the attention products).
  *   schedule  host int32[10]: tiles_n, groups, split, blocks, whole tiles of
  *             workgroup 0, sk_first, sk_tiles, sk_blocks, sk_q, sk_r.
  *   segments  host int32[capacity][10], one row per (workgroup, segment):

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libquartz.so")
 SOURCES = ["abi.hip", "quantize_lzs.hip", "pack_weight.hip", "w4a4_gemm.hip", "w4a4_linear.hip",
-           "w4a4_gemm_plain.hip", "w4a4_gemm_asym.hip", "w4a4_gemm_conv.hip", "scratch.hip",
+           "w4a4_gemm_plain.hip", "w4a4_linear_asym.hip", "w4a4_gemm_conv.hip", "scratch.hip",
            "attention.hip", "attention_fused.hip"]
 
 HIPCC_FLAGS = [

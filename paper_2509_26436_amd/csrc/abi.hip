@@ -375,7 +375,7 @@ quartz_status quartz_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags
         (bias_bf16 && !aligned16(bias_bf16)) || (workspace && !aligned16(workspace)))
         return QUARTZ_ERR_ALIGN;
     const quartz::GemmSchedule sch =
-        quartz::gemm_schedule(M, N, K, quartz::gemm_resident_blocks(), workspace != nullptr);
+        quartz::linear_schedule(M, N, K, quartz::linear_resident_blocks(), workspace != nullptr);
     if (sch.blocks <= 0)
         return QUARTZ_ERR_HIP;
     if (quartz::gemm_workspace_bytes(sch) > workspace_bytes)

@@ -24,12 +24,12 @@ namespace quartz {
 
 hipError_t launch_gemm_attn_scores(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, false, false, false, true, true>(a, stream);
+    return launch_mode<false, false, false, true, true>(a, stream);
 }
 
 hipError_t launch_gemm_attn_pv(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, false, false, false, true, false>(a, stream);
+    return launch_mode<false, false, false, true, false>(a, stream);
 }
 
 namespace {

@@ -143,8 +143,8 @@ struct GemmLaunch {
 // One output mode each (w4a4_gemm_<mode>.hip).
 hipError_t launch_linear(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_linear_static(const GemmLaunch& a, hipStream_t stream);
+hipError_t launch_linear_asym(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream);
-hipError_t launch_gemm_asym(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_conv_static(const GemmLaunch& a, hipStream_t stream);
 hipError_t launch_gemm_attn_scores(const GemmLaunch& a, hipStream_t stream);

@@ -139,7 +139,8 @@ hipError_t launch_w4a4_linear_asym(const uint8_t* codes, const uint8_t* flags,
     GemmLaunch a{codes, flags, scales, w_packed, bias, y, nullptr, M, N, K, ldy, lzs_group,
                  epilogue, sch, nullptr, nullptr, QuantOut{}, 0.0f, zeros, wsums};
     split_workspace(sch, workspace, a.counters, a.slots);
-    return launch_gemm_asym(a, stream);
+    // the kernel of w4a4_linear_asym.hip (schedule from linear_schedule)
+    return launch_linear_asym(a, stream);
 }
 
 hipError_t launch_w4a4_conv3x3(const uint8_t* codes, const uint8_t* flags,

@@ -6,12 +6,12 @@ namespace quartz {
 
 hipError_t launch_gemm_conv(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, false, false, true>(a, stream);
+    return launch_mode<false, false, true>(a, stream);
 }
 
 hipError_t launch_gemm_conv_static(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<false, true, false, true>(a, stream);
+    return launch_mode<false, true, true>(a, stream);
 }
 
 }  // namespace quartz

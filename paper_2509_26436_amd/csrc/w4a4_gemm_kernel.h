@@ -365,10 +365,6 @@ __device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const
 // appendix): one per-tensor activation scale and per-channel weight scales,
 // so the K loop has no per-group scales at all: the fp8 MFMAs accumulate the
 // exact integer sum in place and the epilogue applies act_scale * s_w[n].
-// ASYM instantiations take the asymmetric mode's zero points z[g][m] and the
-// weight group sums W[g][n]: the fp8 MFMA of each tile starts from the
-// correction -z (x) W (one more fp16 outer-product MFMA, exact), so it yields
-// P_g - z W_g, the group product of the activations s (d - z).
 // CONV instantiations are a 3 x 3 convolution (stride 1, padding 1) as an
 // implicit GEMM (ConvGeom): codes, flags and scales are those of the feature
 // map [M][C], and the A row of output pixel m for K-group g is the row of the
@@ -382,15 +378,14 @@ __device__ __forceinline__ void quantize_tile_out(const v16f (&out)[2][2], const
 // tables like A, and A and B address one head's rows inside the arrays of
 // all heads (plane stride and row offset).  With OUT32 the output is fp32,
 // y32 = acc * scale (the scores); otherwise the bf16 output of the layer.
-template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool STATIC, bool ASYM,
-          bool CONV = false, bool ATTN = false, bool OUT32 = false>
+template <int GS, bool I32OUT, bool GELU, bool SPLIT, bool STATIC, bool CONV = false,
+          bool ATTN = false, bool OUT32 = false>
 __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreadsPerBlock) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ codes, const uint8_t* __restrict__ flags,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ w_packed,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, int32_t* __restrict__ yi,
     int64_t M, int64_t N, int64_t K, int64_t ldy, GemmSchedule sch,
-    uint32_t* __restrict__ counters, float* __restrict__ slots, float act_scale,
-    const int8_t* __restrict__ zeros, const int16_t* __restrict__ wsums, ConvGeom conv,
+    uint32_t* __restrict__ counters, float* __restrict__ slots, float act_scale, ConvGeom conv,
     AttnGeom attn)
 {
     // per-group scales are staged and applied only by the per-group kernels
@@ -398,22 +393,14 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     // three LDS stages: group g + 2 is decoded into one while the math waves
     // read the operands of group g + 1 from another (and multiply group g
     // from registers)
-    // One LDS array holds the operand stages and, in ASYM kernels, the zero
-    // point operands after them: the stages stay at the lowest addresses,
-    // where every fragment address of the main loop is a lane offset plus an
+    // One LDS array holds the operand stages, at the lowest addresses, where
+    // every fragment address of the main loop is a lane offset plus an
     // immediate (a larger array placed first would push them past the 16-bit
     // immediate range and cost a register per stage).
     constexpr int kStageBytes = kStages * (BM + BN) * 64;
-    // ASYM: the fp16 operands -z and W of the correction MFMA, per stage, with
-    // the same zero pads as the scales
-    constexpr int kZeroLds = kStages * (BM + 8 + BN + 8) * 2;
-    __shared__ __attribute__((aligned(16))) uint8_t
-        lds_main[kStageBytes + (ASYM ? kZeroLds : 0)];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_main[kStageBytes];
     uint8_t (*const As)[BM * 64] = reinterpret_cast<uint8_t (*)[BM * 64]>(lds_main);
     uint8_t (*const Bs)[BN * 64] = reinterpret_cast<uint8_t (*)[BN * 64]>(lds_main + kStages * BM * 64);
-    uint16_t (*const szs)[BM + 8] = reinterpret_cast<uint16_t (*)[BM + 8]>(lds_main + kStageBytes);
-    uint16_t (*const sWs)[BN + 8] =
-        reinterpret_cast<uint16_t (*)[BN + 8]>(lds_main + kStageBytes + kStages * (BM + 8) * 2);
     // group scales as fp16 bits; entries BM (BN) stay 0: the upper half-wave's
     // k = 8 operand slot of the outer-product MFMA reads them
     __shared__ uint16_t sas[kStages][BM + 8];
@@ -504,7 +491,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
             FlagRaw<GS> f;
             uint32_t fb;             // ATTN: flags of this thread's half B row
             uint16_t sa, sw;
-            uint16_t zh, wh;         // ASYM: fp16 bits of -z and of W
         };
         // fetch the cursor's group into r, then advance the cursor by one step.
         // A no-op step (and any step past the end) reloads the segment's last
@@ -575,20 +561,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 r.fb = load_half_flags<GS>(rbf, (uint32_t)(bc * FB), bh);
             } else {
                 r.fb = 0;
-            }
-            if constexpr (ASYM) {
-                const Rsrc rz = make_rsrc(zeros + (int64_t)g * M + m0, s_bytes / 2);
-                const int z = (int)(int8_t)__builtin_amdgcn_raw_buffer_load_b8(rz, dr, 0, 0);
-                r.zh = __builtin_bit_cast(uint16_t, (_Float16)(-z));
-                const int64_t n0 = panel0 * kPanel;
-                const Rsrc rw = make_rsrc(wsums + (int64_t)g * N + n0,
-                                          n0 < N ? (uint32_t)((N - n0) * 2) : 0u);
-                const int ws = (int)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(rw, swc * 2, 0, 0);
-                // W * 2^-9, the unit of the weight operands (exact: |W| <= 448)
-                r.wh = __builtin_bit_cast(uint16_t, (_Float16)((float)ws * (1.0f / kWeightUnitInv)));
-            } else {
-                r.zh = 0;
-                r.wh = 0;
             }
             if (!fdone && ++fg == fend) {
                 if (cursor_next(fresh_schedule(), blk, fc)) {
@@ -682,11 +654,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
                 if (d < BN)
                     sws[buf][swc] = r.sw;
             }
-            if constexpr (ASYM) {
-                szs[buf][dr] = r.zh;
-                if (d < BN)
-                    sWs[buf][swc] = r.wh;
-            }
         };
 
         // The decode of each group is on the critical path of the next ones:
@@ -703,10 +670,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
         if (d < 8 * kStages) {
             sas[d >> 3][BM + (d & 7)] = 0;
             sws[d >> 3][BN + (d & 7)] = 0;
-            if constexpr (ASYM) {
-                szs[d >> 3][BM + (d & 7)] = 0;
-                sWs[d >> 3][BN + (d & 7)] = 0;
-            }
         }
         const int steps = gemm_steps(fresh_schedule(), blk);
 #pragma unroll
@@ -788,11 +751,10 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     // sums) needs the 16 registers more than its main loop needs the saved
     // instructions (measured: 2.5 % either way).
     typedef int v4i __attribute__((ext_vector_type(4)));
-    constexpr bool kKeepScaleOps = !SPLIT && kGroupScales && !ASYM;
+    constexpr bool kKeepScaleOps = !SPLIT && kGroupScales;
     v8i bf, af[TM];
     v4i sa_op[TM], sw_op[TN];
     _Float16 sa_h[TM], sw_h[TN];
-    _Float16 z_h[TM], w_h[TN];      // ASYM: -z of the tile rows, W of the tile columns
     auto load_a = [&](int i, int buf) {
         af[i] = frag_at(As[buf], a_lo, a_hi, i * 32);
         if constexpr (kGroupScales) {
@@ -802,8 +764,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
             else
                 sa_h[i] = __builtin_bit_cast(_Float16, v);
         }
-        if constexpr (ASYM)
-            z_h[i] = __builtin_bit_cast(_Float16, szs[buf][khalf ? BM : wm * WM + i * 32 + l32]);
     };
     auto load_b = [&](int j, int buf) {
         bf = frag_at(Bs[buf], b_lo, b_hi, j * 32);
@@ -814,8 +774,6 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
             else
                 sw_h[j] = __builtin_bit_cast(_Float16, v);
         }
-        if constexpr (ASYM)
-            w_h[j] = __builtin_bit_cast(_Float16, sWs[buf][khalf ? BN : wn * WN + j * 32 + l32]);
     };
 
     // One group, tiles in the order (0,0) (1,0) (0,1) (1,1).  The fp8 product
@@ -870,20 +828,10 @@ __global__ __launch_bounds__(STATIC && !SPLIT ? kSplitThreadsPerBlock : kThreads
     // MFMA issue runs at raised wave priority (above the decode waves): the
     // matrix unit is the resource to keep fed, and a math wave whose MFMA is
     // held back also holds back the FMAs behind it.
-    // ASYM: the product starts from the correction tile -z (x) W (fp16 MFMA
-    // with one non-zero k, exact in fp32), so it is P_g - z W_g.
     auto mfma_p = [&](int i, int j) {
-        v16f c = zero;
-        if constexpr (ASYM) {
-            typedef _Float16 v8h __attribute__((ext_vector_type(8)));
-            v8h za = {}, wb = {};
-            za[0] = z_h[i];
-            wb[0] = w_h[j];
-            __builtin_amdgcn_s_setprio(3);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_f16(za, wb, zero, 0, 0, 0);
-        }
+        (void)j;
         __builtin_amdgcn_s_setprio(3);
-        const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf, c, 0, 0, 0, 0, 0, 0);
+        const v16f p = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[i], bf, zero, 0, 0, 0, 0, 0, 0);
         __builtin_amdgcn_s_setprio(0);
         return p;
     };
@@ -1328,17 +1276,16 @@ template <bool B>
 using bool_c = std::integral_constant<bool, B>;
 
 // Launch of one output mode, every G_s / epilogue / split combination of it.
-template <bool I32OUT, bool STATIC, bool ASYM, bool CONV = false, bool ATTN = false,
-          bool OUT32 = false>
+template <bool I32OUT, bool STATIC, bool CONV = false, bool ATTN = false, bool OUT32 = false>
 hipError_t launch_mode(const GemmLaunch& a, hipStream_t stream)
 {
     const dim3 grid((unsigned)a.sch.blocks);
     const dim3 block(STATIC && a.sch.sk_tiles == 0 ? kSplitThreadsPerBlock : kThreadsPerBlock);
     auto go = [&](auto gs, auto gelu, auto split) {
         w4a4_gemm_kernel<decltype(gs)::value, I32OUT, decltype(gelu)::value, decltype(split)::value,
-                         STATIC, ASYM, CONV, ATTN, OUT32><<<grid, block, 0, stream>>>(
+                         STATIC, CONV, ATTN, OUT32><<<grid, block, 0, stream>>>(
             a.codes, a.flags, a.scales, a.w_packed, a.bias, a.y, a.yi, a.M, a.N, a.K, a.ldy, a.sch,
-            a.counters, a.slots, a.act_scale, a.zeros, a.wsums, a.conv, a.attn);
+            a.counters, a.slots, a.act_scale, a.conv, a.attn);
     };
     auto with_split = [&](auto gs, auto gelu) {
         if (!I32OUT && !OUT32 && a.sch.sk_tiles > 0)

@@ -6,7 +6,7 @@ namespace quartz {
 
 hipError_t launch_gemm_i32(const GemmLaunch& a, hipStream_t stream)
 {
-    return launch_mode<true, false, false>(a, stream);
+    return launch_mode<true, false>(a, stream);
 }
 
 int device_compute_units()
@@ -45,7 +45,7 @@ int gemm_resident_blocks()
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, false, true>),
+            &per_cu, reinterpret_cast<const void*>(&w4a4_gemm_kernel<16, false, false, true, false, true>),
             kThreadsPerBlock, 0) != hipSuccess)
         return 0;
     const int n = cus * std::max(per_cu, 1);
