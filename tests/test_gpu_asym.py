@@ -107,3 +107,47 @@ def test_asym_linear_parity(case):
     tol = y_tolerance(y64, S, K, gelu=(epi == 1))
     bad = err > tol
     assert not bad.any(), f"{bad.sum()} outputs out of tolerance; worst excess {(err - tol).max():.3e}"
+
+
+def _sample(n: int, count: int, seed: int, tile: int) -> np.ndarray:
+    """Sorted distinct indices < n: both ends, both sides of the first and of
+    the last tile boundary, plus seeded random ones."""
+    fixed = {0, 1, n - 1, n - 2, tile - 1, tile, n // tile * tile - 1, n // tile * tile}
+    rng = np.random.Generator(np.random.PCG64(seed))
+    rest = rng.choice(n, size=min(n, count), replace=False)
+    return np.array(sorted({i for i in fixed if 0 <= i < n} | set(int(i) for i in rest)), np.int64)
+
+
+@pytest.mark.parametrize("layer", [0, 3], ids=["qkv", "fc2"])
+def test_asym_full_size_flux(layer):
+    """A FLUX block layer at full size through the workspace entry point, the
+    launch the bench times (qkv splits its last round along K, fc2 every tile):
+    the quantizer bit for bit and the outputs within tolerance on a sampled
+    grid of rows (tiles of 128) and columns (tiles of 256)."""
+    import torch
+    q = _q()
+    L = W.CONFIGS[3].layers[layer]
+    gs = 16
+    print(f"asym full size {L.name} M={L.M} K={L.K} N={L.N}", flush=True)
+    xb, wb, bias_b = W.make_x(3, layer), W.make_w(3, layer), W.make_bias(3, layer)
+    qa = q.quantize_act(to_dev_bf16(xb), gs, mode=q.MODE_ASYMMETRIC)
+    pw = q.pack_weight(to_dev_bf16(wb))
+    sums = q.weight_group_sums(pw)
+    ws = q.gemm_workspace(L.M, L.N, L.K, "cuda")
+    y = q.w4a4_linear_asym(qa, pw, sums, to_dev_bf16(bias_b), L.epilogue, workspace=ws)
+    torch.cuda.synchronize()
+    rows = _sample(L.M, 32, 700 + layer, 128)
+    cols = _sample(L.N, 40, 800 + layer, 256)
+    a_ref = oracle.quantize_act_asym(xb[rows], gs)
+    r = rows.tolist()
+    np.testing.assert_array_equal(qa.codes[:, r, :].cpu().numpy(), a_ref.codes)
+    np.testing.assert_array_equal(qa.flags[:, r, :].cpu().numpy(), a_ref.abi_flags)
+    np.testing.assert_array_equal(to_host_u16(qa.scales[:, r]), a_ref.abi_scales)
+    np.testing.assert_array_equal(qa.zeros[:, r].cpu().numpy(), a_ref.abi_zeros)
+    wq, sw = oracle.quantize_weight(wb[cols])
+    y64, S = oracle.linear_asym_f64(a_ref, wq, sw, bias_b[cols], L.epilogue)
+    got = bf16_bits_to_f64(to_host_u16(y[r][:, cols.tolist()].contiguous()))
+    err = np.abs(got - y64)
+    tol = y_tolerance(y64, S, L.K, gelu=(L.epilogue == 1))
+    bad = err > tol
+    assert not bad.any(), f"{bad.sum()} of {bad.size} sampled outputs out of tolerance; worst excess {(err - tol).max():.3e}"
