@@ -220,3 +220,23 @@ def test_zero_activations():
     torch.cuda.synchronize()
     codes, flags, scales, _ = _host(out)
     assert not codes.any() and not flags.any() and not scales.any()
+
+
+def test_full_size_batched_mlp_fc1_equals_quantizing_the_stored_output():
+    """The batched FLUX MLP's fc1 (M = 18432, K = 3072, N = 12288, GELU) at full
+    size through the workspace entry point, as the bench times it: every
+    code, FLAG and scale of the fused output equals the quantizer applied to
+    the layer's stored bf16 output (whose parity with the oracle the
+    full-size pipeline test checks on sampled rows)."""
+    import torch
+    q = _q()
+    L = W.CONFIGS[4].layers[0]
+    print(f"fused vs unfused full size M={L.M} K={L.K} N={L.N}", flush=True)
+    qa, pw, bias, ws, out = _fused(W.make_x(4, 0), W.make_w(4, 0), W.make_bias(4, 0), 16, 16,
+                                   L.epilogue, True)
+    y = q.w4a4_linear(qa, pw, bias, L.epilogue, workspace=ws)
+    ref = q.quantize_act(y, 16)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("codes", "flags", "scales"), (out.codes, out.flags, out.scales),
+                          (ref.codes, ref.flags, ref.scales)):
+        assert torch.equal(a, b), f"fused {name} differ from quantizing the stored output"
